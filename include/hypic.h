@@ -1,0 +1,182 @@
+/*
+ * hypic.h -- C ABI of libhypic.so, the MI355X (gfx950) hot path of
+ * position-independent caching for gated-delta-rule (GDN) linear-attention
+ * layers (Hypic, arXiv 2607.01299).
+ *
+ * Three operations:
+ *   hypic_build_segment    zero-start prefill of independent segments, emitting
+ *                          per-token outputs o, the zero-start end state S_{C|0}
+ *                          and the segment-cumulative transition operator T_C
+ *                          (Sec. 4.2 cache tuple; Sec. 5 state construction).
+ *   hypic_compose_segments chains cached tuples behind a prefix state by the
+ *                          composition law, Eq. (6).
+ *   hypic_seam_rescan      runs the first w tokens of segments through the
+ *                          recurrence from a composed incoming state, emitting
+ *                          their outputs and the advanced state (Sec. 4.3, seam
+ *                          propagation through linear-attention layers).
+ *
+ * Math (Tab. 1 GDN row, Eq. (2)), per head, S in R^{d_k x d_v}:
+ *   S_t = alpha_t (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T,
+ *   o_t = S_t^T q_t          (the token reads the state after its own write),
+ *   alpha_t = exp(log_alpha_t).
+ * T_C is stored factored as in the Tab. 3 GDN closed form:
+ *   T_C = exp(log_decay) * P_hat,  log_decay = sum_t log_alpha_t,
+ *   P_hat = (I - beta_L k_L k_L^T) ... (I - beta_1 k_1 k_1^T)   (later tokens left).
+ *
+ * Conventions common to every entry point
+ * ---------------------------------------
+ * - Return value: HYPIC_OK (0) or a negative hypic_status.  Every argument is
+ *   validated on the host before anything is enqueued; on error nothing is
+ *   enqueued and no output is touched.
+ * - Pointers are DEVICE pointers unless the name ends in _host (host memory,
+ *   read only during the call).  The caller owns all memory; the library never
+ *   allocates or frees, keeps no pointer after returning and has no mutable
+ *   global state, so calls are reentrant.
+ * - Every call enqueues its kernels on `stream` (a hipStream_t; NULL means the
+ *   default stream) and returns without synchronising.
+ * - Layouts are dense row-major (C order).  Token tensors are packed:
+ *     q, k : [T, h_qk, d_k]      v, o : [T, h_v, d_v]
+ *     beta, log_alpha : [T, h_v] float32
+ *   in the element type given by dims->dtype for q, k, v, o.  States, P_hat and
+ *   log_decay are always float32.
+ * - Grouped heads: h_v must be a multiple of h_qk; v-head h reads qk-head
+ *   h / (h_v / h_qk).  beta and log_alpha are per v-head.
+ * - Supported: d_k, d_v in {64, 128}; chunk in {16, 32, 64}; dtype F32 or BF16.
+ *   Other values return HYPIC_EUNSUPPORTED.
+ * - Device-side index arrays must hold the same values as their _host copies;
+ *   the kernels clamp token ranges to [0, T) but do not re-validate.
+ */
+#ifndef HYPIC_H
+#define HYPIC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum hypic_status {
+  HYPIC_OK = 0,
+  HYPIC_EINVAL = -1,       /* bad pointer, size, offset or index */
+  HYPIC_EUNSUPPORTED = -2, /* dims outside the supported set */
+  HYPIC_EWORKSPACE = -3,   /* workspace missing or smaller than required */
+  HYPIC_EHIP = -4          /* a HIP runtime call failed (launch error) */
+} hypic_status;
+
+typedef enum hypic_dtype { HYPIC_F32 = 0, HYPIC_BF16 = 1 } hypic_dtype;
+
+typedef enum hypic_op {
+  HYPIC_OP_BUILD = 0,
+  HYPIC_OP_COMPOSE = 1,
+  HYPIC_OP_SEAM = 2
+} hypic_op;
+
+typedef struct hypic_dims {
+  int32_t h_qk;  /* key/query heads */
+  int32_t h_v;   /* value heads (multiple of h_qk) */
+  int32_t d_k;   /* key dimension: 64 or 128 */
+  int32_t d_v;   /* value dimension: 64 or 128 */
+  int32_t dtype; /* hypic_dtype of q, k, v, o */
+  int32_t chunk; /* tokens per chunk of the scan: 16, 32 or 64 */
+} hypic_dims;
+
+/* Bytes of device workspace `op` needs for `n` items (segments for BUILD,
+ * requests for COMPOSE, entries for SEAM).  Returns 0 when none is needed, and
+ * 0 as well for invalid dims (the operation itself then reports the error). */
+size_t hypic_workspace_bytes(int32_t op, const hypic_dims* dims, int64_t n);
+
+/* Static, NUL-terminated description of a status code. */
+const char* hypic_status_str(int32_t status);
+
+/*
+ * hypic_build_segment -- zero-start prefill of n_seg independent segments
+ * (Sec. 4.2 cache tuple; Sec. 5: the end state from S_0 = 0 and the operator
+ * from S_0 = I with writes zeroed; Tab. 3 GDN row for the factored operator).
+ *
+ *   q, k        [T, h_qk, d_k] dtype    v [T, h_v, d_v] dtype
+ *   beta        [T, h_v] f32            log_alpha [T, h_v] f32 (any finite values)
+ *   cu_seqlens  [n_seg + 1] int32 device; cu_seqlens_host the same values on the
+ *               host: 0 = cu[0] <= cu[1] <= ... <= cu[n_seg] = T.  Segment s
+ *               covers tokens [cu[s], cu[s+1]); a zero-length segment yields
+ *               S_seg = 0, P_hat = I, log_decay = 0.
+ *   o           [T, h_v, d_v] dtype, or NULL to skip the outputs.
+ *   S_seg       [n_seg, h_v, d_k, d_v] f32: end state from S_0 = 0.
+ *   P_hat       [n_seg, h_v, d_k, d_k] f32, or NULL to skip the operator path.
+ *   log_decay   [n_seg, h_v] f32, or NULL.
+ *   workspace   device scratch of at least
+ *               hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg) bytes
+ *               (holds the longest-first segment order; contents are not
+ *               preserved across calls).
+ * Segments are scheduled longest first (Eq. (9) LPT order, ties by index);
+ * results do not depend on the schedule.  n_seg == 0 enqueues nothing.
+ */
+int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k,
+                            const void* v, const float* beta,
+                            const float* log_alpha, const int32_t* cu_seqlens,
+                            const int32_t* cu_seqlens_host, int32_t n_seg,
+                            void* o, float* S_seg, float* P_hat,
+                            float* log_decay, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/*
+ * hypic_compose_segments -- Eq. (6): for each request r and v-head h, start
+ * from S = S_prefix[r, h] (zero when S_prefix is NULL) and for each listed
+ * segment i = seg_ids[j], j = req_offsets[r] .. req_offsets[r+1]-1 in order:
+ *     S_incoming[j, h] = S;   S <- exp(log_decay[i, h]) * P_hat[i, h] @ S + S_seg[i, h]
+ * then S_out[r, h] = S.
+ *
+ *   P_hat       [n_pool, h_v, d_k, d_k] f32   log_decay [n_pool, h_v] f32
+ *   S_seg       [n_pool, h_v, d_k, d_v] f32   (the pool of cached tuples)
+ *   seg_ids     [nnz] int32 device, seg_ids_host the same on the host, every
+ *               value in [0, n_pool); nnz = req_offsets_host[n_req].
+ *   req_offsets [n_req + 1] int32 device / req_offsets_host on the host:
+ *               0 = off[0] <= off[1] <= ... (CSR).  A request with no segment
+ *               returns its prefix.
+ *   S_prefix    [n_req, h_v, d_k, d_v] f32 or NULL.
+ *   S_out       [n_req, h_v, d_k, d_v] f32.
+ *   S_incoming  [nnz, h_v, d_k, d_v] f32 or NULL.
+ * dims->dtype selects the arithmetic: F32 uses float32 matrix cores, BF16 uses
+ * three-term split-bf16 products with float32 accumulation.  Workspace: none
+ * (pass NULL, 0).  n_req == 0 enqueues nothing.
+ */
+int32_t hypic_compose_segments(const hypic_dims* dims, const float* P_hat,
+                               const float* log_decay, const float* S_seg,
+                               int32_t n_pool, const int32_t* seg_ids,
+                               const int32_t* seg_ids_host,
+                               const int32_t* req_offsets,
+                               const int32_t* req_offsets_host, int32_t n_req,
+                               const float* S_prefix, float* S_out,
+                               float* S_incoming, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/*
+ * hypic_seam_rescan -- Sec. 4.3 seam propagation through a linear-attention
+ * layer: entry e covers tokens [tok_start[e], tok_start[e] + w_eff) of the packed
+ * token arrays, w_eff = min(w, tok_len[e]); they run through the recurrence
+ * starting from S_in[e] (the composed state entering the segment).
+ *
+ *   q, k, v, beta, log_alpha   packed token arrays as in build, n_tokens rows.
+ *   tok_start, tok_len  [n_entries] int32 device; *_host the same on the host.
+ *               Each tok_len >= 1 and tok_start + w_eff <= n_tokens.
+ *   w           seam width, >= 1.
+ *   S_in        [n_entries, h_v, d_k, d_v] f32.
+ *   o_seam      [n_entries, w, h_v, d_v] dtype; rows >= w_eff are not written.
+ *   S_post      [n_entries, h_v, d_k, d_v] f32 state after the w_eff tokens, or NULL.
+ * Workspace: none (pass NULL, 0).  n_entries == 0 enqueues nothing.
+ */
+int32_t hypic_seam_rescan(const hypic_dims* dims, const void* q, const void* k,
+                          const void* v, const float* beta,
+                          const float* log_alpha, int32_t n_tokens,
+                          const int32_t* tok_start, const int32_t* tok_len,
+                          const int32_t* tok_start_host,
+                          const int32_t* tok_len_host, int32_t n_entries,
+                          int32_t w, const float* S_in, void* o_seam,
+                          float* S_post, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HYPIC_H */

@@ -1,0 +1,15 @@
+"""MI355X (gfx950) hot path of Hypic position-independent caching for
+gated-delta-rule linear-attention layers: segment build, Eq. (6) composition
+and seam rescan, as HIP kernels behind the C ABI of include/hypic.h.
+"""
+
+from ._lib import HypicError  # noqa: F401
+
+
+def __getattr__(name):
+    # the torch-facing calls load torch lazily so that the generators and the
+    # library loader stay importable without it
+    if name in ("build_segment", "compose_segments", "seam_rescan", "make_dims"):
+        from . import ops
+        return getattr(ops, name)
+    raise AttributeError(name)

@@ -1,0 +1,191 @@
+// C ABI of libhypic.so: argument validation on the host, workspace sizing and
+// kernel dispatch.  Nothing is enqueued unless every check passes.
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/hypic.h"
+#include "scan.hpp"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Checks shared by every entry point.  Returns HYPIC_OK or an error code.
+int32_t check_dims(const hypic_dims* d) {
+  if (d == nullptr) return HYPIC_EINVAL;
+  if (d->h_qk < 1 || d->h_v < 1) return HYPIC_EINVAL;
+  if (d->h_v % d->h_qk != 0) return HYPIC_EINVAL;
+  if (d->d_k != 64 && d->d_k != 128) return HYPIC_EUNSUPPORTED;
+  if (d->d_v != 64 && d->d_v != 128) return HYPIC_EUNSUPPORTED;
+  if (d->chunk != 16 && d->chunk != 32 && d->chunk != 64) return HYPIC_EUNSUPPORTED;
+  if (d->dtype != HYPIC_F32 && d->dtype != HYPIC_BF16) return HYPIC_EUNSUPPORTED;
+  return HYPIC_OK;
+}
+
+int32_t hip_status(hipError_t e) { return e == hipSuccess ? HYPIC_OK : HYPIC_EHIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* hypic_status_str(int32_t status) {
+  switch (status) {
+    case HYPIC_OK: return "ok";
+    case HYPIC_EINVAL: return "invalid argument (pointer, size, offset or index)";
+    case HYPIC_EUNSUPPORTED: return "unsupported dims (d_k, d_v in {64,128}; chunk in {16,32,64}; dtype F32 or BF16)";
+    case HYPIC_EWORKSPACE: return "workspace missing or too small";
+    case HYPIC_EHIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+size_t hypic_workspace_bytes(int32_t op, const hypic_dims* dims, int64_t n) {
+  if (check_dims(dims) != HYPIC_OK || n <= 0) return 0;
+  if (op == HYPIC_OP_BUILD) return round_up(static_cast<size_t>(n) * sizeof(int32_t));
+  return 0;
+}
+
+int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k,
+                            const void* v, const float* beta, const float* log_alpha,
+                            const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                            int32_t n_seg, void* o, float* S_seg, float* P_hat,
+                            float* log_decay, void* workspace, size_t workspace_bytes,
+                            void* stream) {
+  int32_t st = check_dims(dims);
+  if (st != HYPIC_OK) return st;
+  if (n_seg < 0) return HYPIC_EINVAL;
+  if (n_seg == 0) return HYPIC_OK;
+  if (!q || !k || !v || !beta || !log_alpha || !cu_seqlens || !cu_seqlens_host || !S_seg)
+    return HYPIC_EINVAL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || (o && !aligned16(o)))
+    return HYPIC_EINVAL;
+  if (cu_seqlens_host[0] != 0) return HYPIC_EINVAL;
+  for (int32_t s = 0; s < n_seg; ++s)
+    if (cu_seqlens_host[s + 1] < cu_seqlens_host[s]) return HYPIC_EINVAL;
+  const int64_t n_items = static_cast<int64_t>(n_seg) * dims->h_v * (P_hat ? 2 : 1);
+  if (n_items > 0x7fffffff) return HYPIC_EINVAL;
+  const size_t need = hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg);
+  if (workspace == nullptr || workspace_bytes < need) return HYPIC_EWORKSPACE;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int32_t* order = static_cast<int32_t*>(workspace);
+  st = hip_status(hypic::launch_lpt_order(cu_seqlens, n_seg, order, s));
+  if (st != HYPIC_OK) return st;
+
+  hypic::ScanArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.log_alpha = log_alpha;
+  a.h_qk = dims->h_qk;
+  a.h_v = dims->h_v;
+  a.group = dims->h_v / dims->h_qk;
+  a.n_tokens = cu_seqlens_host[n_seg];
+  a.mode = 0;
+  a.n_roles = P_hat ? 2 : 1;
+  a.cu_seqlens = cu_seqlens;
+  a.order = order;
+  a.o = o;
+  a.S_out = S_seg;
+  a.P_hat = P_hat;
+  a.log_decay = log_decay;
+  return hip_status(hypic::launch_scan(a, dims->dtype == HYPIC_BF16, dims->d_k, dims->d_v,
+                                       dims->chunk, static_cast<int>(n_items), s));
+}
+
+int32_t hypic_compose_segments(const hypic_dims* dims, const float* P_hat,
+                               const float* log_decay, const float* S_seg, int32_t n_pool,
+                               const int32_t* seg_ids, const int32_t* seg_ids_host,
+                               const int32_t* req_offsets, const int32_t* req_offsets_host,
+                               int32_t n_req, const float* S_prefix, float* S_out,
+                               float* S_incoming, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  int32_t st = check_dims(dims);
+  if (st != HYPIC_OK) return st;
+  if (n_req < 0 || n_pool < 0) return HYPIC_EINVAL;
+  if (n_req == 0) return HYPIC_OK;
+  if (!req_offsets || !req_offsets_host || !S_out) return HYPIC_EINVAL;
+  if (req_offsets_host[0] != 0) return HYPIC_EINVAL;
+  for (int32_t r = 0; r < n_req; ++r)
+    if (req_offsets_host[r + 1] < req_offsets_host[r]) return HYPIC_EINVAL;
+  const int32_t nnz = req_offsets_host[n_req];
+  if (nnz > 0) {
+    if (!P_hat || !log_decay || !S_seg || !seg_ids || !seg_ids_host) return HYPIC_EINVAL;
+    for (int32_t j = 0; j < nnz; ++j)
+      if (seg_ids_host[j] < 0 || seg_ids_host[j] >= n_pool) return HYPIC_EINVAL;
+  }
+  if (static_cast<int64_t>(n_req) * dims->h_v > 0x7fffffff) return HYPIC_EINVAL;
+
+  hypic::ComposeArgs a{};
+  a.P_hat = P_hat;
+  a.log_decay = log_decay;
+  a.S_seg = S_seg;
+  a.seg_ids = seg_ids;
+  a.req_offsets = req_offsets;
+  a.S_prefix = S_prefix;
+  a.S_out = S_out;
+  a.S_incoming = S_incoming;
+  a.h_v = dims->h_v;
+  return hip_status(hypic::launch_compose(a, dims->dtype == HYPIC_F32, dims->d_k, dims->d_v,
+                                          n_req, static_cast<hipStream_t>(stream)));
+}
+
+int32_t hypic_seam_rescan(const hypic_dims* dims, const void* q, const void* k,
+                          const void* v, const float* beta, const float* log_alpha,
+                          int32_t n_tokens, const int32_t* tok_start, const int32_t* tok_len,
+                          const int32_t* tok_start_host, const int32_t* tok_len_host,
+                          int32_t n_entries, int32_t w, const float* S_in, void* o_seam,
+                          float* S_post, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  int32_t st = check_dims(dims);
+  if (st != HYPIC_OK) return st;
+  if (n_entries < 0 || n_tokens < 0 || w < 1) return HYPIC_EINVAL;
+  if (n_entries == 0) return HYPIC_OK;
+  if (!q || !k || !v || !beta || !log_alpha || !tok_start || !tok_len || !tok_start_host ||
+      !tok_len_host || !S_in || !o_seam)
+    return HYPIC_EINVAL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o_seam))
+    return HYPIC_EINVAL;
+  for (int32_t e = 0; e < n_entries; ++e) {
+    const int64_t len = tok_len_host[e];
+    const int64_t start = tok_start_host[e];
+    if (len < 1 || start < 0) return HYPIC_EINVAL;
+    const int64_t w_eff = len < w ? len : w;
+    if (start + w_eff > n_tokens) return HYPIC_EINVAL;
+  }
+  if (static_cast<int64_t>(n_entries) * dims->h_v > 0x7fffffff) return HYPIC_EINVAL;
+
+  hypic::ScanArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.log_alpha = log_alpha;
+  a.h_qk = dims->h_qk;
+  a.h_v = dims->h_v;
+  a.group = dims->h_v / dims->h_qk;
+  a.n_tokens = n_tokens;
+  a.mode = 1;
+  a.n_roles = 1;
+  a.tok_start = tok_start;
+  a.tok_len = tok_len;
+  a.w = w;
+  a.S_in = S_in;
+  a.o = o_seam;
+  a.S_out = S_post;
+  return hip_status(hypic::launch_scan(a, dims->dtype == HYPIC_BF16, dims->d_k, dims->d_v,
+                                       dims->chunk, n_entries * dims->h_v,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,51 @@
+// Launch interface between the C ABI layer and the scan / compose kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hypic {
+
+// Arguments of the chunked scan kernel (segment build when mode == 0, seam
+// rescan when mode == 1).  All pointers are device pointers.
+struct ScanArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const float* beta;
+  const float* log_alpha;
+  int32_t h_qk, h_v, group;  // group = h_v / h_qk
+  int32_t n_tokens;
+  int32_t mode;              // 0 build, 1 seam
+  int32_t n_roles;           // 1: state only, 2: state and operator
+  const int32_t* cu_seqlens; // build: segment offsets
+  const int32_t* order;      // build: longest-first segment order
+  const int32_t* tok_start;  // seam: first token of each entry
+  const int32_t* tok_len;    // seam: segment length of each entry
+  int32_t w;                 // seam width
+  const float* S_in;         // seam: incoming states
+  void* o;                   // outputs (build: [T,h_v,d_v]; seam: [n,w,h_v,d_v])
+  float* S_out;              // build: S_seg; seam: S_post (may be null)
+  float* P_hat;              // build, role 1
+  float* log_decay;          // build, may be null
+};
+
+struct ComposeArgs {
+  const float* P_hat;
+  const float* log_decay;
+  const float* S_seg;
+  const int32_t* seg_ids;
+  const int32_t* req_offsets;
+  const float* S_prefix;
+  float* S_out;
+  float* S_incoming;
+  int32_t h_v;
+};
+
+hipError_t launch_lpt_order(const int32_t* cu, int n, int32_t* order, hipStream_t s);
+hipError_t launch_scan(const ScanArgs& a, int bf16, int d_k, int d_v, int chunk,
+                       int n_items, hipStream_t s);
+hipError_t launch_compose(const ComposeArgs& a, int f32, int d_k, int d_v, int n_req,
+                          hipStream_t s);
+
+}  // namespace hypic

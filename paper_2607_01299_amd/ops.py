@@ -1,0 +1,166 @@
+"""PyTorch-facing calls of the C ABI: allocate outputs with torch on the
+inputs' device, pass raw pointers and the current HIP stream, raise on error.
+
+Index arrays (cu_seqlens, seg_ids, req_offsets, tok_start, tok_len) are given
+as host int32 arrays (numpy / list / CPU tensor) and, optionally, as device
+int32 tensors holding the same values; when the device copy is omitted it is
+made here with a synchronous copy.
+"""
+
+import ctypes
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import Dims, HypicError  # noqa: F401
+
+_ws_cache = {}
+
+
+def _dtype_code(t):
+    if t.dtype == torch.bfloat16:
+        return _lib.HYPIC_BF16
+    if t.dtype == torch.float32:
+        return _lib.HYPIC_F32
+    raise HypicError(_lib.HYPIC_EUNSUPPORTED, "q/k/v must be bfloat16 or float32")
+
+
+def _ptr(t):
+    return ctypes.c_void_p(0 if t is None else t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _host_i32(x):
+    if isinstance(x, torch.Tensor):
+        x = x.detach().cpu().numpy()
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+
+
+def _index_pair(host, dev, device):
+    h = _host_i32(host)
+    if dev is None:
+        dev = torch.from_numpy(h.copy()).to(device)
+    if dev.dtype != torch.int32 or not dev.is_contiguous():
+        raise HypicError(_lib.HYPIC_EINVAL, "device index arrays must be contiguous int32")
+    return h, dev
+
+
+def _hptr(h):
+    return h.ctypes.data_as(ctypes.c_void_p)
+
+
+def _contig(t, name):
+    if not t.is_contiguous():
+        raise HypicError(_lib.HYPIC_EINVAL, "%s must be contiguous" % name)
+    return t
+
+
+def _workspace(op, dims, n, device):
+    lib = _lib.load()
+    need = lib.hypic_workspace_bytes(op, ctypes.byref(dims), n)
+    if need == 0:
+        return None, 0
+    key = (str(device), op)
+    buf = _ws_cache.get(key)
+    if buf is None or buf.numel() < need:
+        buf = torch.empty(need, dtype=torch.uint8, device=device)
+        _ws_cache[key] = buf
+    return buf, need
+
+
+def make_dims(q, v, chunk, h_qk=None):
+    return Dims(h_qk=q.shape[1] if h_qk is None else h_qk, h_v=v.shape[1], d_k=q.shape[2],
+                d_v=v.shape[2], dtype=_dtype_code(q), chunk=chunk)
+
+
+def build_segment(q, k, v, beta, log_alpha, cu_seqlens, cu_seqlens_dev=None, *, chunk=64,
+                  want_operator=True, want_o=True):
+    """Zero-start build of every segment of a packed batch.
+
+    q, k [T, h_qk, d_k], v [T, h_v, d_v] (bf16 or f32, CUDA); beta, log_alpha
+    [T, h_v] float32; cu_seqlens host int32 [n_seg + 1].
+    Returns dict(o, S_seg, P_hat, log_decay) of torch tensors (o / P_hat /
+    log_decay are None when not requested).
+    """
+    lib = _lib.load()
+    for name, t in (("q", q), ("k", k), ("v", v), ("beta", beta), ("log_alpha", log_alpha)):
+        _contig(t, name)
+    dev = q.device
+    dims = make_dims(q, v, chunk)
+    cu_h, cu_d = _index_pair(cu_seqlens, cu_seqlens_dev, dev)
+    n_seg = len(cu_h) - 1
+    T, h_v, d_v = v.shape
+    d_k = q.shape[2]
+    o = torch.empty((T, h_v, d_v), dtype=q.dtype, device=dev) if want_o else None
+    S_seg = torch.empty((n_seg, h_v, d_k, d_v), dtype=torch.float32, device=dev)
+    P_hat = (torch.empty((n_seg, h_v, d_k, d_k), dtype=torch.float32, device=dev)
+             if want_operator else None)
+    log_decay = torch.empty((n_seg, h_v), dtype=torch.float32, device=dev) if want_operator else None
+    ws, ws_bytes = _workspace(_lib.HYPIC_OP_BUILD, dims, n_seg, dev)
+    _lib.check(lib.hypic_build_segment(
+        ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(log_alpha),
+        _ptr(cu_d), _hptr(cu_h), n_seg, _ptr(o), _ptr(S_seg), _ptr(P_hat), _ptr(log_decay),
+        _ptr(ws), ws_bytes, _stream(dev)))
+    return {"o": o, "S_seg": S_seg, "P_hat": P_hat, "log_decay": log_decay}
+
+
+def compose_segments(P_hat, log_decay, S_seg, seg_ids, req_offsets, S_prefix=None, *,
+                     seg_ids_dev=None, req_offsets_dev=None, precision="split",
+                     want_incoming=True, h_qk=None):
+    """Eq. (6) composition of pool tuples for each request (CSR lists).
+
+    precision: "split" (three-term split-bf16 matrix cores) or "f32".
+    Returns (S_out [n_req, h_v, d_k, d_v], S_incoming [nnz, h_v, d_k, d_v] or None).
+    """
+    lib = _lib.load()
+    for name, t in (("P_hat", P_hat), ("log_decay", log_decay), ("S_seg", S_seg)):
+        _contig(t, name)
+    dev = S_seg.device
+    n_pool, h_v, d_k, d_v = S_seg.shape
+    dims = Dims(h_qk=h_v if h_qk is None else h_qk, h_v=h_v, d_k=d_k, d_v=d_v,
+                dtype=_lib.HYPIC_F32 if precision == "f32" else _lib.HYPIC_BF16, chunk=64)
+    ids_h, ids_d = _index_pair(seg_ids, seg_ids_dev, dev)
+    off_h, off_d = _index_pair(req_offsets, req_offsets_dev, dev)
+    n_req = len(off_h) - 1
+    nnz = int(off_h[-1]) if n_req >= 0 and len(off_h) else 0
+    S_out = torch.empty((max(n_req, 0), h_v, d_k, d_v), dtype=torch.float32, device=dev)
+    S_inc = (torch.empty((nnz, h_v, d_k, d_v), dtype=torch.float32, device=dev)
+             if want_incoming else None)
+    if S_prefix is not None:
+        _contig(S_prefix, "S_prefix")
+    _lib.check(lib.hypic_compose_segments(
+        ctypes.byref(dims), _ptr(P_hat), _ptr(log_decay), _ptr(S_seg), n_pool, _ptr(ids_d),
+        _hptr(ids_h), _ptr(off_d), _hptr(off_h), n_req, _ptr(S_prefix), _ptr(S_out),
+        _ptr(S_inc), None, 0, _stream(dev)))
+    return S_out, S_inc
+
+
+def seam_rescan(q, k, v, beta, log_alpha, tok_start, tok_len, w, S_in, *, tok_start_dev=None,
+                tok_len_dev=None, chunk=64, want_post=True):
+    """Seam-window rescan of each entry's first min(w, tok_len) tokens from S_in.
+
+    Returns (o_seam [n_entries, w, h_v, d_v] (rows >= w_eff left unwritten),
+    S_post [n_entries, h_v, d_k, d_v] or None).
+    """
+    lib = _lib.load()
+    for name, t in (("q", q), ("k", k), ("v", v), ("beta", beta), ("log_alpha", log_alpha),
+                    ("S_in", S_in)):
+        _contig(t, name)
+    dev = q.device
+    dims = make_dims(q, v, chunk)
+    st_h, st_d = _index_pair(tok_start, tok_start_dev, dev)
+    ln_h, ln_d = _index_pair(tok_len, tok_len_dev, dev)
+    n_e = len(st_h)
+    T, h_v, d_v = v.shape
+    d_k = q.shape[2]
+    o_seam = torch.empty((n_e, w, h_v, d_v), dtype=q.dtype, device=dev)
+    S_post = torch.empty((n_e, h_v, d_k, d_v), dtype=torch.float32, device=dev) if want_post else None
+    _lib.check(lib.hypic_seam_rescan(
+        ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(log_alpha), T,
+        _ptr(st_d), _ptr(ln_d), _hptr(st_h), _hptr(ln_h), n_e, int(w), _ptr(S_in), _ptr(o_seam),
+        _ptr(S_post), None, 0, _stream(dev)))
+    return o_seam, S_post

@@ -1,0 +1,149 @@
+"""C ABI: the library loads, exports every declared symbol, and rejects bad
+arguments on the host before touching the GPU.  CPU only: every call here
+returns from validation, so nothing is launched (fake device pointers are
+never dereferenced)."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2607_01299_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hypic.h")
+
+FAKE = ctypes.c_void_p(0x10000)      # 16-byte aligned, never dereferenced
+FAKE_ODD = ctypes.c_void_p(0x10004)  # misaligned
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(hypic_[a-z_]+)\s*\(", text)))
+
+
+def _dims(h_qk=2, h_v=4, d_k=128, d_v=128, dtype=_lib.HYPIC_BF16, chunk=64):
+    return _lib.Dims(h_qk=h_qk, h_v=h_v, d_k=d_k, d_v=d_v, dtype=dtype, chunk=chunk)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        pytest.fail("libhypic.so is not built; run `python -m paper_2607_01299_amd.build`")
+    return _lib.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    declared = _declared()
+    assert set(declared) == set(_lib.EXPORTS)
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (hypic_\w+)", out))
+    for name in declared:
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4):
+        assert lib.hypic_status_str(code)
+    assert lib.hypic_status_str(-99) == b"unknown status"
+
+
+def test_workspace_sizes(lib):
+    d = _dims()
+    assert lib.hypic_workspace_bytes(_lib.HYPIC_OP_BUILD, ctypes.byref(d), 64) >= 64 * 4
+    assert lib.hypic_workspace_bytes(_lib.HYPIC_OP_BUILD, ctypes.byref(d), 0) == 0
+    assert lib.hypic_workspace_bytes(_lib.HYPIC_OP_COMPOSE, ctypes.byref(d), 10) == 0
+    bad = _dims(d_k=96)
+    assert lib.hypic_workspace_bytes(_lib.HYPIC_OP_BUILD, ctypes.byref(bad), 64) == 0
+
+
+def _build(lib, dims, cu, n_seg=None, q=FAKE, S=FAKE, ws=FAKE, ws_bytes=1 << 20, o=FAKE,
+           cu_dev=FAKE):
+    cu = np.asarray(cu, dtype=np.int32)
+    n_seg = len(cu) - 1 if n_seg is None else n_seg
+    return lib.hypic_build_segment(
+        ctypes.byref(dims) if dims is not None else None, q, FAKE, FAKE, FAKE, FAKE, cu_dev,
+        cu.ctypes.data_as(ctypes.c_void_p), n_seg, o, S, FAKE, FAKE, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(d_k=96), _lib.HYPIC_EUNSUPPORTED),
+    (dict(d_v=32), _lib.HYPIC_EUNSUPPORTED),
+    (dict(chunk=48), _lib.HYPIC_EUNSUPPORTED),
+    (dict(dtype=7), _lib.HYPIC_EUNSUPPORTED),
+    (dict(h_qk=3, h_v=4), _lib.HYPIC_EINVAL),
+    (dict(h_v=0), _lib.HYPIC_EINVAL),
+])
+def test_build_rejects_bad_dims(lib, kw, code):
+    assert _build(lib, _dims(**kw), [0, 10, 20]) == code
+
+
+def test_build_rejects_bad_arguments(lib):
+    d = _dims()
+    assert _build(lib, None, [0, 10]) == _lib.HYPIC_EINVAL
+    assert _build(lib, d, [0, 10], q=None) == _lib.HYPIC_EINVAL
+    assert _build(lib, d, [0, 10], S=None) == _lib.HYPIC_EINVAL
+    assert _build(lib, d, [0, 10], cu_dev=None) == _lib.HYPIC_EINVAL
+    assert _build(lib, d, [0, 10], q=FAKE_ODD) == _lib.HYPIC_EINVAL
+    assert _build(lib, d, [0, 10], o=FAKE_ODD) == _lib.HYPIC_EINVAL
+    assert _build(lib, d, [1, 10]) == _lib.HYPIC_EINVAL            # must start at 0
+    assert _build(lib, d, [0, 10, 5]) == _lib.HYPIC_EINVAL         # decreasing
+    assert _build(lib, d, [0, 10], n_seg=-1) == _lib.HYPIC_EINVAL
+    assert _build(lib, d, [0, 10, 20], ws=None) == _lib.HYPIC_EWORKSPACE
+    assert _build(lib, d, [0, 10, 20], ws_bytes=4) == _lib.HYPIC_EWORKSPACE
+    # nothing to do is not an error (and launches nothing)
+    assert _build(lib, d, [0], n_seg=0) == _lib.HYPIC_OK
+
+
+def _compose(lib, dims, ids, offs, n_pool=8, S_out=FAKE, P=FAKE):
+    ids = np.asarray(ids, dtype=np.int32)
+    offs = np.asarray(offs, dtype=np.int32)
+    return lib.hypic_compose_segments(
+        ctypes.byref(dims), P, FAKE, FAKE, n_pool, FAKE, ids.ctypes.data_as(ctypes.c_void_p),
+        FAKE, offs.ctypes.data_as(ctypes.c_void_p), len(offs) - 1, None, S_out, None, None, 0,
+        None)
+
+
+def test_compose_rejects_bad_arguments(lib):
+    d = _dims()
+    assert _compose(lib, d, [0, 8], [0, 2]) == _lib.HYPIC_EINVAL       # id == n_pool
+    assert _compose(lib, d, [0, -1], [0, 2]) == _lib.HYPIC_EINVAL      # negative id
+    assert _compose(lib, d, [0, 1], [0, 2, 1]) == _lib.HYPIC_EINVAL    # decreasing offsets
+    assert _compose(lib, d, [0, 1], [1, 2]) == _lib.HYPIC_EINVAL       # must start at 0
+    assert _compose(lib, d, [0, 1], [0, 2], S_out=None) == _lib.HYPIC_EINVAL
+    assert _compose(lib, d, [0, 1], [0, 2], P=None) == _lib.HYPIC_EINVAL
+    assert _compose(lib, _dims(d_k=32), [0], [0, 1]) == _lib.HYPIC_EUNSUPPORTED
+    assert _compose(lib, d, [], [0]) == _lib.HYPIC_OK                  # no request
+
+
+def _seam(lib, dims, start, length, w=8, n_tokens=100, o=FAKE, S_in=FAKE):
+    st = np.asarray(start, dtype=np.int32)
+    ln = np.asarray(length, dtype=np.int32)
+    return lib.hypic_seam_rescan(
+        ctypes.byref(dims), FAKE, FAKE, FAKE, FAKE, FAKE, n_tokens, FAKE, FAKE,
+        st.ctypes.data_as(ctypes.c_void_p), ln.ctypes.data_as(ctypes.c_void_p), len(st), w,
+        S_in, o, None, None, 0, None)
+
+
+def test_seam_rejects_bad_arguments(lib):
+    d = _dims()
+    assert _seam(lib, d, [0, 95], [10, 10]) == _lib.HYPIC_EINVAL       # 95 + 8 > 100
+    assert _seam(lib, d, [0], [0]) == _lib.HYPIC_EINVAL                # empty entry
+    assert _seam(lib, d, [-1], [4]) == _lib.HYPIC_EINVAL
+    assert _seam(lib, d, [0], [4], w=0) == _lib.HYPIC_EINVAL
+    assert _seam(lib, d, [0], [4], o=None) == _lib.HYPIC_EINVAL
+    assert _seam(lib, d, [0], [4], o=FAKE_ODD) == _lib.HYPIC_EINVAL
+    assert _seam(lib, d, [0], [4], S_in=None) == _lib.HYPIC_EINVAL
+    assert _seam(lib, d, [], []) == _lib.HYPIC_OK
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(_lib.HypicError):
+        _lib.load()
