@@ -1,0 +1,262 @@
+#!/usr/bin/env python3
+"""Benchmark of the Hypic GDN hot path on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+segment build (o, S_seg, P_hat, log_decay for every segment and head), Eq. (6)
+composition of the batch's segments in order (emitting the state entering
+each segment) and the seam rescan of every segment's first w tokens from that
+state.  Default workload: 16 heads, d_k = d_v = 128, 8 independent segments of
+2048 bf16 tokens, chunk 64, seam w = 8.  value = tokens / s over the timed
+steps, inputs resident in HBM.
+
+Also reported:
+  roofline      the build scan kernel: algorithmic FLOP per launch over its
+                average duration (HIP events on the launch stream) vs the
+                dense bf16 matrix-core peak;
+  compose_burst serve-time burst: 256 requests x U{8..64} segments of a
+                512-entry float32 pool (16 heads, 128 x 128), then a w = 64
+                seam per listed segment; compositions / s and the composition
+                kernel's algorithmic HBM bandwidth;
+  cpu_baseline  the float64 oracle on the host cores on a bounded sample.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+
+from paper_2607_01299_amd import workloads as W  # noqa: E402
+
+METRIC = "segment-build tokens/s + MFMA util; compositions/s + HBM GB/s (1 MI355X)"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+# Algorithmic work of the chunked scan per (token, v-head) at chunk C:
+#   2C(3 d_k + 2 d_v)   K K^T, Q K^T, W, U, (Q K^T . Gamma) Vn
+#   6 d_k d_v           W' S0, Q S0, K^T Vn
+#   4 d_k^2             W P0, K^T X (operator path)
+def flop_per_token_head(d_k, d_v, chunk):
+    return 2 * chunk * (3 * d_k + 2 * d_v) + 6 * d_k * d_v + 4 * d_k * d_k
+
+
+def compose_bytes_per_head_step(d_k, d_v, write_incoming=True):
+    # read P_hat_i and S_i, write the incoming state, read log_decay_i
+    return 4 * (d_k * d_k + d_k * d_v * (2 if write_incoming else 1)) + 4
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle, run before the GPU is touched
+# ---------------------------------------------------------------------------
+
+def _oracle_pair(args):
+    cfg, seg, head = args
+    import oracle
+    w = _CACHE.get(cfg)
+    lo, hi = int(w["cu_seqlens"][seg]), int(w["cu_seqlens"][seg + 1])
+    sl = slice(lo, hi)
+    oracle.build_segments(w["q"][sl], w["k"][sl], w["v"][sl], w["beta"][sl],
+                          w["log_alpha"][sl], [0, hi - lo], seg_head_pairs=[(0, head)])
+    return hi - lo
+
+
+_CACHE = {}
+
+
+def _worker_init(cfg):
+    _CACHE[cfg] = W.segment_workload(cfg)
+
+
+def cpu_baseline(cfg, h_v, pairs_per_worker=12):
+    import multiprocessing as mp
+    workers = min(len(os.sched_getaffinity(0)), 16)
+    for var in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
+        os.environ[var] = "1"
+    wl = W.segment_workload(cfg)
+    n_seg = len(wl["cu_seqlens"]) - 1
+    pairs = [(cfg, s, h) for h in range(h_v) for s in range(n_seg)]
+    pairs = pairs[:workers * pairs_per_worker]
+    ctx = mp.get_context("spawn")
+    with ctx.Pool(workers, initializer=_worker_init, initargs=(cfg,)) as pool:
+        pool.map(_oracle_pair, pairs[:workers])           # warm the workers
+        t0 = time.perf_counter()
+        toks = pool.map(_oracle_pair, pairs)
+        dt = time.perf_counter() - t0
+    token_heads = float(sum(toks))
+    return {
+        "value": token_heads / dt / h_v,
+        "unit": "tokens/s",
+        "cores": workers,
+        "kind": "oracle",
+        "sample": "%d (segment, head) builds of %d tokens (S and operator, float64 token "
+                  "recurrence) on %d processes, %.1f s; tokens/s = token-heads/s / %d heads"
+                  % (len(pairs), int(toks[0]), workers, dt, h_v),
+    }
+
+
+# ---------------------------------------------------------------------------
+# GPU legs
+# ---------------------------------------------------------------------------
+
+def _to_dev(w, torch):
+    dt = torch.bfloat16 if w["dtype"] == W.BF16 else torch.float32
+    q = torch.from_numpy(w["q"]).cuda().to(dt).contiguous()
+    k = torch.from_numpy(w["k"]).cuda().to(dt).contiguous()
+    v = torch.from_numpy(w["v"]).cuda().to(dt).contiguous()
+    beta = torch.from_numpy(w["beta"]).cuda().contiguous()
+    la = torch.from_numpy(w["log_alpha"]).cuda().contiguous()
+    return q, k, v, beta, la
+
+
+def bench_segments(torch, cfg, steps, warmup, seam_w):
+    from paper_2607_01299_amd.pipeline import SegmentPipeline
+    w = W.segment_workload(cfg)
+    q, k, v, beta, la = _to_dev(w, torch)
+    pipe = SegmentPipeline(q, k, v, beta, la, w["cu_seqlens"], chunk=w["chunk"], seam_w=seam_w)
+    for _ in range(warmup):
+        pipe.run()
+    torch.cuda.synchronize()
+    stream = pipe.stream
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        pipe.build()
+        ev[i][1].record(stream)
+        pipe.compose()
+        pipe.seam()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    build_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    T = int(w["cu_seqlens"][-1])
+    h_v, d_k, d_v = w["v"].shape[1], w["d_k"], w["d_v"]
+    flop = float(flop_per_token_head(d_k, d_v, w["chunk"])) * T * h_v
+    achieved = flop / (build_ms * 1e-3) / 1e12
+    return {
+        "ms_per_step": dt / steps * 1e3,
+        "tokens": T,
+        "build_ms": build_ms,
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "kernel": "scan_kernel (segment build)",
+                     "flop_per_launch": flop},
+        "config": {"workload": W.CONFIG_NAMES[cfg], "segments": len(w["lengths"]),
+                   "tokens": T, "h_qk": int(w["q"].shape[1]), "h_v": int(h_v), "d_k": d_k,
+                   "d_v": d_v, "chunk": w["chunk"], "seam_w": seam_w, "seed": w["seed"]},
+    }
+
+
+def bench_compose_burst(torch, steps, warmup):
+    from paper_2607_01299_amd.pipeline import ComposeBurst
+    p = W.pool_workload()
+    dev = "cuda"
+    P = torch.from_numpy(p["P_hat"]).to(dev)
+    g = torch.from_numpy(p["log_decay"]).to(dev)
+    S = torch.from_numpy(p["S_seg"]).to(dev)
+    t = p["tokens"]
+    toks = (torch.from_numpy(t["q"]).to(dev).to(torch.bfloat16).contiguous(),
+            torch.from_numpy(t["k"]).to(dev).to(torch.bfloat16).contiguous(),
+            torch.from_numpy(t["v"]).to(dev).to(torch.bfloat16).contiguous(),
+            torch.from_numpy(t["beta"]).to(dev), torch.from_numpy(t["log_alpha"]).to(dev))
+    burst = ComposeBurst(P, g, S, p["seg_ids"], p["req_offsets"], toks, p["tok_start"],
+                         p["tok_len"], p["w"])
+    for _ in range(warmup):
+        burst.run()
+    torch.cuda.synchronize()
+    stream = burst.stream
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        burst.compose()
+        ev[i][1].record(stream)
+        burst.seam()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    comp_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    nnz, h_v = burst.nnz, burst.h_v
+    byts = float(compose_bytes_per_head_step(burst.d_k, burst.d_v)) * nnz * h_v
+    gbs = byts / (comp_ms * 1e-3) / 1e9
+    return {
+        "compositions_per_s": nnz / (dt / steps),
+        "requests_per_s": burst.n_req / (dt / steps),
+        "ms_per_burst": dt / steps * 1e3,
+        "compose_ms": comp_ms,
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": gbs / PEAK_HBM_GBS, "traffic": None,
+                     "kernel": "compose_kernel", "bytes_per_launch": byts},
+        "config": {"workload": W.CONFIG_NAMES[5], "requests": burst.n_req,
+                   "compositions": nnz, "pool": int(p["n_pool"]), "h_v": h_v,
+                   "d_k": burst.d_k, "d_v": burst.d_v, "seam_w": p["w"], "seed": p["seed"]},
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=2, choices=[2, 3, 4])
+    ap.add_argument("--seam-w", type=int, default=8)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-burst", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(segments shard across GPUs with no exchange; see the design notes). "
+              "Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        wl = W.segment_workload(args.config)
+        cpu = cpu_baseline(args.config, int(wl["v"].shape[1]))
+        print("[bench] cpu baseline done: %.1f tokens/s" % cpu["value"], file=sys.stderr,
+              flush=True)
+
+    import torch
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    from paper_2607_01299_amd import _lib
+    _lib.load()
+
+    seg = bench_segments(torch, args.config, args.steps, args.warmup, args.seam_w)
+    print("[bench] segment step done: %.3f ms/step" % seg["ms_per_step"], file=sys.stderr,
+          flush=True)
+    burst = None if args.no_burst else bench_compose_burst(torch, max(args.steps // 2, 3),
+                                                           max(args.warmup // 2, 1))
+    value = seg["tokens"] / (seg["ms_per_step"] * 1e-3)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": seg["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded generators; the paper's datasets are not used)",
+        "config": seg["config"],
+        "roofline": seg["roofline"],
+        "build_ms": seg["build_ms"],
+        "cpu_baseline": cpu,
+        "compose_burst": burst,
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

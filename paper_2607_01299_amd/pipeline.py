@@ -1,0 +1,167 @@
+"""Pre-bound passes over the hot path.
+
+``SegmentPipeline``: build every segment of a packed batch, compose the
+segments behind an optional prefix (one request in batch order unless a CSR
+request list is given), and rescan each listed segment's first w tokens from
+its composed incoming state.
+
+``ComposeBurst``: compose many requests from a pool of cached tuples and
+rescan the seam of every listed segment.
+
+All outputs, device index arrays and C-ABI arguments are allocated once, so a
+call to ``run()`` only enqueues the kernels on the stream that was current at
+construction.
+"""
+
+import ctypes
+
+import numpy as np
+import torch
+
+from . import _lib
+from ._lib import Dims
+
+
+def _i32_pair(x, device):
+    h = np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+    return h, torch.from_numpy(h.copy()).to(device)
+
+
+def _p(t):
+    return ctypes.c_void_p(0 if t is None else t.data_ptr())
+
+
+def _dtype_code(t):
+    return _lib.HYPIC_BF16 if t.dtype == torch.bfloat16 else _lib.HYPIC_F32
+
+
+class SegmentPipeline:
+    def __init__(self, q, k, v, beta, log_alpha, cu_seqlens, *, chunk=64, seam_w=8,
+                 seg_ids=None, req_offsets=None, S_prefix=None, compose_precision="split",
+                 want_post=False):
+        self.lib = _lib.load()
+        dev = q.device
+        self.device = dev
+        self.stream = torch.cuda.current_stream(dev)
+        sp = ctypes.c_void_p(self.stream.cuda_stream)
+        T, h_qk, d_k = q.shape
+        h_v, d_v = v.shape[1], v.shape[2]
+        self.T, self.h_v, self.d_k, self.d_v = T, h_v, d_k, d_v
+        self.dims = Dims(h_qk=h_qk, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_dtype_code(q), chunk=chunk)
+        self.cdims = Dims(h_qk=h_v, h_v=h_v, d_k=d_k, d_v=d_v,
+                          dtype=_lib.HYPIC_F32 if compose_precision == "f32" else _lib.HYPIC_BF16,
+                          chunk=chunk)
+        self.inputs = (q, k, v, beta, log_alpha)
+        self.cu_h, self.cu_d = _i32_pair(cu_seqlens, dev)
+        n_seg = len(self.cu_h) - 1
+        self.n_seg = n_seg
+        f32 = torch.float32
+        self.o = torch.empty((T, h_v, d_v), dtype=q.dtype, device=dev)
+        self.S_seg = torch.empty((n_seg, h_v, d_k, d_v), dtype=f32, device=dev)
+        self.P_hat = torch.empty((n_seg, h_v, d_k, d_k), dtype=f32, device=dev)
+        self.log_decay = torch.empty((n_seg, h_v), dtype=f32, device=dev)
+        ws_bytes = self.lib.hypic_workspace_bytes(_lib.HYPIC_OP_BUILD, ctypes.byref(self.dims),
+                                                  n_seg)
+        self.ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        self._build_args = (
+            ctypes.byref(self.dims), _p(q), _p(k), _p(v), _p(beta), _p(log_alpha), _p(self.cu_d),
+            self.cu_h.ctypes.data_as(ctypes.c_void_p), n_seg, _p(self.o), _p(self.S_seg),
+            _p(self.P_hat), _p(self.log_decay), _p(self.ws), ws_bytes, sp)
+        # composition: one request of all segments in batch order by default
+        if seg_ids is None:
+            seg_ids = np.arange(n_seg, dtype=np.int32)
+            req_offsets = np.array([0, n_seg], dtype=np.int32)
+        self.ids_h, self.ids_d = _i32_pair(seg_ids, dev)
+        self.off_h, self.off_d = _i32_pair(req_offsets, dev)
+        n_req = len(self.off_h) - 1
+        nnz = int(self.off_h[-1])
+        self.n_req, self.nnz = n_req, nnz
+        self.S_prefix = S_prefix
+        self.S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=f32, device=dev)
+        self.S_inc = torch.empty((nnz, h_v, d_k, d_v), dtype=f32, device=dev)
+        self._compose_args = (
+            ctypes.byref(self.cdims), _p(self.P_hat), _p(self.log_decay), _p(self.S_seg), n_seg,
+            _p(self.ids_d), self.ids_h.ctypes.data_as(ctypes.c_void_p), _p(self.off_d),
+            self.off_h.ctypes.data_as(ctypes.c_void_p), n_req, _p(S_prefix), _p(self.S_out),
+            _p(self.S_inc), None, 0, sp)
+        # seam: the first w tokens of every listed segment
+        lens = np.diff(self.cu_h)
+        self.seam_w = seam_w
+        self.ts_h, self.ts_d = _i32_pair(self.cu_h[:-1][self.ids_h], dev)
+        self.tl_h, self.tl_d = _i32_pair(lens[self.ids_h], dev)
+        self.o_seam = torch.empty((nnz, seam_w, h_v, d_v), dtype=q.dtype, device=dev)
+        self.S_post = (torch.empty((nnz, h_v, d_k, d_v), dtype=f32, device=dev)
+                       if want_post else None)
+        self._seam_args = (
+            ctypes.byref(self.dims), _p(q), _p(k), _p(v), _p(beta), _p(log_alpha), T,
+            _p(self.ts_d), _p(self.tl_d), self.ts_h.ctypes.data_as(ctypes.c_void_p),
+            self.tl_h.ctypes.data_as(ctypes.c_void_p), nnz, seam_w, _p(self.S_inc),
+            _p(self.o_seam), _p(self.S_post), None, 0, sp)
+
+    def build(self):
+        _lib.check(self.lib.hypic_build_segment(*self._build_args))
+
+    def compose(self):
+        _lib.check(self.lib.hypic_compose_segments(*self._compose_args))
+
+    def seam(self):
+        _lib.check(self.lib.hypic_seam_rescan(*self._seam_args))
+
+    def run(self):
+        self.build()
+        self.compose()
+        self.seam()
+
+
+class ComposeBurst:
+    """Requests composed from a pool of cached tuples, then seam rescans."""
+
+    def __init__(self, P_hat, log_decay, S_seg, seg_ids, req_offsets, tokens, tok_start,
+                 tok_len, w, *, chunk=64, precision="split", want_post=False):
+        self.lib = _lib.load()
+        dev = S_seg.device
+        self.stream = torch.cuda.current_stream(dev)
+        sp = ctypes.c_void_p(self.stream.cuda_stream)
+        n_pool, h_v, d_k, d_v = S_seg.shape
+        q, k, v, beta, log_alpha = tokens
+        self.tokens = tokens
+        self.pool = (P_hat, log_decay, S_seg)
+        self.cdims = Dims(h_qk=h_v, h_v=h_v, d_k=d_k, d_v=d_v,
+                          dtype=_lib.HYPIC_F32 if precision == "f32" else _lib.HYPIC_BF16,
+                          chunk=chunk)
+        self.dims = Dims(h_qk=q.shape[1], h_v=h_v, d_k=d_k, d_v=d_v, dtype=_dtype_code(q),
+                         chunk=chunk)
+        self.ids_h, self.ids_d = _i32_pair(seg_ids, dev)
+        self.off_h, self.off_d = _i32_pair(req_offsets, dev)
+        n_req = len(self.off_h) - 1
+        nnz = int(self.off_h[-1])
+        self.n_req, self.nnz, self.h_v, self.d_k, self.d_v = n_req, nnz, h_v, d_k, d_v
+        f32 = torch.float32
+        self.S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=f32, device=dev)
+        self.S_inc = torch.empty((nnz, h_v, d_k, d_v), dtype=f32, device=dev)
+        self._compose_args = (
+            ctypes.byref(self.cdims), _p(P_hat), _p(log_decay), _p(S_seg), n_pool, _p(self.ids_d),
+            self.ids_h.ctypes.data_as(ctypes.c_void_p), _p(self.off_d),
+            self.off_h.ctypes.data_as(ctypes.c_void_p), n_req, None, _p(self.S_out),
+            _p(self.S_inc), None, 0, sp)
+        self.ts_h, self.ts_d = _i32_pair(tok_start, dev)
+        self.tl_h, self.tl_d = _i32_pair(tok_len, dev)
+        self.w = w
+        self.o_seam = torch.empty((nnz, w, h_v, d_v), dtype=q.dtype, device=dev)
+        self.S_post = (torch.empty((nnz, h_v, d_k, d_v), dtype=f32, device=dev)
+                       if want_post else None)
+        self._seam_args = (
+            ctypes.byref(self.dims), _p(q), _p(k), _p(v), _p(beta), _p(log_alpha), q.shape[0],
+            _p(self.ts_d), _p(self.tl_d), self.ts_h.ctypes.data_as(ctypes.c_void_p),
+            self.tl_h.ctypes.data_as(ctypes.c_void_p), nnz, w, _p(self.S_inc), _p(self.o_seam),
+            _p(self.S_post), None, 0, sp)
+
+    def compose(self):
+        _lib.check(self.lib.hypic_compose_segments(*self._compose_args))
+
+    def seam(self):
+        _lib.check(self.lib.hypic_seam_rescan(*self._seam_args))
+
+    def run(self):
+        self.compose()
+        self.seam()
