@@ -67,7 +67,7 @@ int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k
   if (cu_seqlens_host[0] != 0) return HYPIC_EINVAL;
   for (int32_t s = 0; s < n_seg; ++s)
     if (cu_seqlens_host[s + 1] < cu_seqlens_host[s]) return HYPIC_EINVAL;
-  const int64_t n_items = static_cast<int64_t>(n_seg) * dims->h_v * (P_hat ? 2 : 1);
+  const int64_t n_items = static_cast<int64_t>(n_seg) * dims->h_v * 4;
   if (n_items > 0x7fffffff) return HYPIC_EINVAL;
   const size_t need = hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg);
   if (workspace == nullptr || workspace_bytes < need) return HYPIC_EWORKSPACE;
@@ -96,7 +96,7 @@ int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k
   a.P_hat = P_hat;
   a.log_decay = log_decay;
   return hip_status(hypic::launch_scan(a, dims->dtype == HYPIC_BF16, dims->d_k, dims->d_v,
-                                       dims->chunk, static_cast<int>(n_items), s));
+                                       dims->chunk, n_seg, s));
 }
 
 int32_t hypic_compose_segments(const hypic_dims* dims, const float* P_hat,
@@ -163,7 +163,7 @@ int32_t hypic_seam_rescan(const hypic_dims* dims, const void* q, const void* k,
     const int64_t w_eff = len < w ? len : w;
     if (start + w_eff > n_tokens) return HYPIC_EINVAL;
   }
-  if (static_cast<int64_t>(n_entries) * dims->h_v > 0x7fffffff) return HYPIC_EINVAL;
+  if (static_cast<int64_t>(n_entries) * dims->h_v * 4 > 0x7fffffff) return HYPIC_EINVAL;
 
   hypic::ScanArgs a{};
   a.q = q;
@@ -184,8 +184,7 @@ int32_t hypic_seam_rescan(const hypic_dims* dims, const void* q, const void* k,
   a.o = o_seam;
   a.S_out = S_post;
   return hip_status(hypic::launch_scan(a, dims->dtype == HYPIC_BF16, dims->d_k, dims->d_v,
-                                       dims->chunk, n_entries * dims->h_v,
-                                       static_cast<hipStream_t>(stream)));
+                                       dims->chunk, n_entries, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

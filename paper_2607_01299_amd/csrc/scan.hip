@@ -565,10 +565,17 @@ hipError_t launch_lpt_order(const int32_t* cu, int n, int32_t* order, hipStream_
 }
 
 hipError_t launch_scan(const ScanArgs& a, int bf16, int d_k, int d_v, int chunk,
-                       int n_items, hipStream_t s) {
-  if (n_items <= 0) return hipSuccess;
-  if (bf16) return launch_scan_d<uint16_t>(a, d_k, d_v, chunk, n_items, s);
-  return launch_scan_d<float>(a, d_k, d_v, chunk, n_items, s);
+                       int n_chains, hipStream_t s) {
+  if (n_chains <= 0) return hipSuccess;
+  const bool fast = bf16 && chunk == 64;
+  const int64_t per_head =
+      fast ? scan_bf16_items_per_head(d_k, d_v, a.n_roles == 2) : a.n_roles;
+  const int64_t n_items = static_cast<int64_t>(n_chains) * a.h_v * per_head;
+  if (n_items > 0x7fffffff) return hipErrorInvalidValue;
+  if (fast) return launch_scan_bf16(a, d_k, d_v, static_cast<int>(n_items), s);
+  if (bf16)
+    return launch_scan_d<uint16_t>(a, d_k, d_v, chunk, static_cast<int>(n_items), s);
+  return launch_scan_d<float>(a, d_k, d_v, chunk, static_cast<int>(n_items), s);
 }
 
 }  // namespace hypic

@@ -43,8 +43,13 @@ struct ComposeArgs {
 };
 
 hipError_t launch_lpt_order(const int32_t* cu, int n, int32_t* order, hipStream_t s);
+// Launches the scan over n_chains (segments or seam entries) x h_v heads;
+// returns hipErrorInvalidValue if the grid would exceed 2^31 - 1 workgroups.
 hipError_t launch_scan(const ScanArgs& a, int bf16, int d_k, int d_v, int chunk,
-                       int n_items, hipStream_t s);
+                       int n_chains, hipStream_t s);
+// Workgroups per (chain, head) of the bf16 chunk-64 scan.
+int scan_bf16_items_per_head(int d_k, int d_v, int with_operator);
+hipError_t launch_scan_bf16(const ScanArgs& a, int d_k, int d_v, int n_items, hipStream_t s);
 hipError_t launch_compose(const ComposeArgs& a, int f32, int d_k, int d_v, int n_req,
                           hipStream_t s);
 

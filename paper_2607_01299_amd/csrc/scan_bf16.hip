@@ -1,0 +1,718 @@
+// Chunked gated-delta-rule scan, bf16 inputs, chunk 64: the production path
+// of the segment build and the seam rescan on gfx950.
+//
+// Same mathematics as scan.hip (per chunk: Gram matrix, unit-lower-triangular
+// inverse A1 = (I + L)^{-1}, WY factor W, then the state / operator update),
+// organised for the CDNA4 matrix cores:
+//
+// * Work split.  One workgroup of 8 waves runs one (segment, v-head, column
+//   block) chain: waves 0-3 own 16 columns each of a 64-column block of the
+//   state S (and emit those output columns), waves 4-7 own the same 64 columns
+//   of the operator P_hat.  The chunk's Gram matrix, inverse and W are computed
+//   once per workgroup and shared by both halves; each SIMD runs one state
+//   wave and one operator wave, so one's matrix-core work hides the other's
+//   latency.
+// * Operand layout.  Every matrix-core operand is staged in LDS "fragment
+//   major": a 16 x 32 (rows x contraction) tile is 64 lanes x 8 bf16 stored in
+//   lane order, so a lane reads its fragment with one 16-byte load and a wave
+//   reads 1 KiB of consecutive bytes.  Products whose result feeds another
+//   product are computed transposed where that makes the accumulator tile
+//   already be the next operand's fragment (W^T = K^T (A1 diag beta)^T,
+//   K Q^T, O^T), and states are used as operands straight from registers.
+// * Gates are exponentiated once per chunk (b = prefix sum of log alpha,
+//   gamma = exp(b), exp(b_last - b)); every decay factor is exp of a
+//   non-positive number.
+// * The inverse: 16 x 16 diagonal blocks by column-parallel substitution, then
+//   the off-diagonal blocks A_ij = -sum_k N_ik A_kj with N_ik = A_ii L_ik on
+//   float32 matrix cores, one block diagonal at a time.
+// * The next chunk's q, k, v, beta, log alpha are loaded into registers while
+//   the current chunk computes.
+// * Precision: W is formed in two bf16 passes (A1 diag(beta) split hi + lo, K
+//   exact) and kept as hi + lo; the state path uses single bf16 passes (its
+//   decay keeps rounding from accumulating); the operator path, which has no
+//   decay, uses W hi + lo and splits P0 (three passes for W P0, two for K^T X).
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mfma.hpp"
+#include "scan.hpp"
+
+namespace hypic {
+
+namespace {
+
+constexpr int kThreads = 512;
+constexpr int C = 64;        // tokens per chunk
+constexpr int NCOL = 64;     // state / operator columns per workgroup
+constexpr int KTC = C / 32;  // 32-wide contraction blocks over the chunk's tokens
+constexpr int LDC = C + 4;   // row stride (floats) of the float32 chunk x chunk matrices
+
+typedef unsigned short u16;
+typedef u16 u16x4 __attribute__((ext_vector_type(4)));
+
+// ---- fragment-major layout -------------------------------------------------
+// logical R x K matrix (contraction over K), KT = K / 32 blocks per row tile.
+__device__ __forceinline__ int frag_slot(int rt, int kt, int KT, int lane) {
+  return ((rt * KT + kt) * 64 + lane) * 8;
+}
+// element index of (row, k): lane (g, row % 16) with g = (k % 16) / 4,
+// slot j = 4 * ((k % 32) / 16) + k % 4
+__device__ __forceinline__ int frag_index(int row, int k, int KT) {
+  const int kk = k & 31;
+  const int g = (kk & 15) >> 2;
+  const int j = ((kk >> 4) << 2) | (kk & 3);
+  return (((row >> 4) * KT + (k >> 5)) * 64 + g * 16 + (row & 15)) * 8 + j;
+}
+
+__device__ __forceinline__ bf16x8 ld_frag(const u16* base, int slot) {
+  return *reinterpret_cast<const bf16x8*>(base + slot);
+}
+__device__ __forceinline__ void st_frag(u16* base, int slot, bf16x8 v) {
+  *reinterpret_cast<bf16x8*>(base + slot) = v;
+}
+
+__device__ __forceinline__ f32x4 mma(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 pack(const f32x4& lo, const f32x4& hi) {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    r[i] = static_cast<__bf16>(lo[i]);
+    r[4 + i] = static_cast<__bf16>(hi[i]);
+  }
+  return r;
+}
+__device__ __forceinline__ void pack_split(const f32x4& lo, const f32x4& hi, bf16x8& h,
+                                           bf16x8& l) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    h[i] = static_cast<__bf16>(lo[i]);
+    h[4 + i] = static_cast<__bf16>(hi[i]);
+    l[i] = static_cast<__bf16>(lo[i] - static_cast<float>(h[i]));
+    l[4 + i] = static_cast<__bf16>(hi[i] - static_cast<float>(h[4 + i]));
+  }
+}
+
+// float32 16x16x16 product on matrix cores: a[s] = A[m][4g+s], b[s] = B[4g+s][n]
+__device__ __forceinline__ f32x4 mma16_f32(const float4& a, const float4& b, f32x4 c) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
+  return c;
+}
+
+__device__ __forceinline__ u16 bf16_bits(uint4 v, int e) {
+  const uint32_t w = (e < 2) ? v.x : (e < 4) ? v.y : (e < 6) ? v.z : v.w;
+  return static_cast<u16>((e & 1) ? (w >> 16) : (w & 0xffffu));
+}
+__device__ __forceinline__ u16 bf16_of(float x) {
+  __bf16 h = static_cast<__bf16>(x);
+  return *reinterpret_cast<u16*>(&h);
+}
+
+// lower-triangle tile t in 0..9 -> (row tile, column tile) with column <= row
+__device__ __forceinline__ int tri_row(int t) { return (t < 1) ? 0 : (t < 3) ? 1 : (t < 6) ? 2 : 3; }
+__device__ __forceinline__ int tri_col(int t) { return t - tri_row(t) * (tri_row(t) + 1) / 2; }
+
+// ---- LDS plan (bytes); regions are reused across the phases of a chunk ------
+template <int DK>
+struct Lds {
+  static constexpr int FK = C * DK * 2;     // bytes of a 64 x DK bf16 fragment matrix
+  static constexpr int F32M = C * LDC * 4;  // padded 64 x 64 float32 matrix
+  static constexpr int RA = (FK > F32M) ? FK : F32M;
+  static constexpr int O_KD = 0;            // K over d -> A1 (f32) -> W hi
+  static constexpr int O_Q = O_KD + RA;     // Q over d -> A1^T -> (QK . Gamma), (A1 . Gamma) beta
+  static constexpr int O_KT = O_Q + RA;     // K over tokens
+  static constexpr int O_L = O_KT + FK;     // L^T (f32) + N blocks -> A1 beta hi / lo
+  static constexpr int O_V = O_L + F32M;    // V (64 columns) over tokens
+  static constexpr int O_WS = O_V + NCOL * C * 2;  // gamma W (state path)
+  static constexpr int O_WL = O_WS + FK;           // W lo (operator path)
+  static constexpr int O_G = O_WL + FK;            // gates
+  static constexpr int TOTAL = O_G + 4 * C * 4;
+  static_assert(2 * C * C * 2 <= F32M, "A1 beta hi + lo fit the L region");
+  static_assert(2 * C * C * 2 <= RA, "QK and (A1 . Gamma) beta fit the Q region");
+  static_assert(TOTAL <= 160 * 1024, "LDS budget");
+};
+
+template <int DK, int DV>
+__global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
+  using LP = Lds<DK>;
+  constexpr int KTD = DK / 32;  // contraction blocks over d_k
+  constexpr int DT = DK / 16;   // d_k row tiles of the state
+  constexpr int NS = DV / NCOL;
+  constexpr int NP = DK / NCOL;
+  constexpr int KQU = 16 * (DK / 8);  // (4-token, 8-d) load units of K (and of Q)
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  u16* fKd = reinterpret_cast<u16*>(smem + LP::O_KD);
+  float* A1 = reinterpret_cast<float*>(smem + LP::O_KD);
+  u16* fWh = reinterpret_cast<u16*>(smem + LP::O_KD);
+  u16* fQ = reinterpret_cast<u16*>(smem + LP::O_Q);
+  float* A1t = reinterpret_cast<float*>(smem + LP::O_Q);
+  u16* fQK = reinterpret_cast<u16*>(smem + LP::O_Q);
+  u16* fAgb = fQK + C * C;
+  u16* fKt = reinterpret_cast<u16*>(smem + LP::O_KT);
+  float* Lt = reinterpret_cast<float*>(smem + LP::O_L);
+  u16* fAbh = reinterpret_cast<u16*>(smem + LP::O_L);
+  u16* fAbl = fAbh + C * C;
+  u16* fV = reinterpret_cast<u16*>(smem + LP::O_V);
+  u16* fWs = reinterpret_cast<u16*>(smem + LP::O_WS);
+  u16* fWl = reinterpret_cast<u16*>(smem + LP::O_WL);
+  float* gb = reinterpret_cast<float*>(smem + LP::O_G);
+  float* gbeta = gb + C;
+  float* ggam = gb + 2 * C;
+  float* gdec = gb + 3 * C;
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int lane = tid & 63;
+  const int g = lane >> 4, ln = lane & 15;
+  const bool sw = wave < 4;  // state wave (else operator wave)
+  const int wq = wave & 3;   // column tile of this wave within the block
+
+  // ---- work item ----------------------------------------------------------
+  const int n_cb = (args.n_roles == 2 && NP > NS) ? NP : NS;
+  const int per_rank = n_cb * args.h_v;
+  const int rank = blockIdx.x / per_rank;
+  const int rem = blockIdx.x % per_rank;
+  const int h = rem / n_cb;
+  const int cb = rem % n_cb;
+  const bool has_state = cb < NS;
+  const bool has_op = (args.n_roles == 2) && (cb < NP);
+  int seg, lo, hi;
+  if (args.mode == 0) {
+    seg = args.order[rank];
+    lo = args.cu_seqlens[seg];
+    hi = args.cu_seqlens[seg + 1];
+  } else {
+    seg = rank;
+    lo = args.tok_start[seg];
+    const int len = args.tok_len[seg];
+    hi = lo + ((len < args.w) ? len : args.w);
+  }
+  lo = (lo < 0) ? 0 : ((lo > args.n_tokens) ? args.n_tokens : lo);
+  hi = (hi < lo) ? lo : ((hi > args.n_tokens) ? args.n_tokens : hi);
+  const bool active = sw ? has_state : has_op;  // does this wave own columns?
+
+  const int hk = h / args.group;
+  const u16* kg = static_cast<const u16*>(args.k);
+  const u16* qg = static_cast<const u16*>(args.q);
+  const u16* vg = static_cast<const u16*>(args.v);
+  const long qk_stride = static_cast<long>(args.h_qk) * DK;
+  const long v_stride = static_cast<long>(args.h_v) * DV;
+  const int col0 = cb * NCOL + wq * 16;  // this wave's 16 columns (of S or P_hat)
+  const long sh = static_cast<long>(seg) * args.h_v + h;
+
+  // ---- chain state: 16 columns per wave, all d_k rows ------------------------
+  f32x4 st[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) st[dt] = zero4();
+  if (sw) {
+    if (args.mode == 1 && has_state) {
+      const float* s_in = args.S_in + sh * DK * DV;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) st[dt][i] = s_in[(dt * 16 + 4 * g + i) * DV + col0 + ln];
+    }
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) st[dt][i] = (dt * 16 + 4 * g + i == col0 + ln) ? 1.f : 0.f;
+  }
+  float log_decay = 0.f;
+
+  // ---- prefetch of one chunk's tokens into registers -------------------------
+  // threads [0, 256): K units; [256, 512): Q units; [384, 512): also V units
+  const int ku = tid & 255;
+  const bool k_thr = tid < 256 && ku < KQU;
+  const bool q_thr = tid >= 256 && ku < KQU;
+  const bool v_thr = tid >= 384;
+  const int tq = ku / (DK / 8), dq = ku % (DK / 8);
+  const int vu = tid - 384;
+  const int vtq = vu / (NCOL / 8), vdq = vu % (NCOL / 8);
+  uint4 pkq[4], pv[4];
+  float pa = 0.f, pbeta = 0.f;
+  const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
+  auto prefetch = [&](int c0) __attribute__((always_inline)) {
+    const int n = (hi - c0 < C) ? (hi - c0) : C;  // n >= 1
+    // unconditional loads from a clamped (valid) token; padded rows are zeroed
+    // by value afterwards
+    if (k_thr || q_thr) {
+      const u16* src = k_thr ? kg : qg;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int tok = 4 * tq + t;
+        const int tc = (tok < n) ? tok : n - 1;
+        const uint4 x =
+            *reinterpret_cast<const uint4*>(src + (c0 + tc) * qk_stride + hk * DK + 8 * dq);
+        pkq[t] = (tok < n) ? x : z4;
+      }
+    }
+    if (v_thr && has_state) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int tok = 4 * vtq + t;
+        const int tc = (tok < n) ? tok : n - 1;
+        const uint4 x = *reinterpret_cast<const uint4*>(vg + (c0 + tc) * v_stride + h * DV +
+                                                        cb * NCOL + 8 * vdq);
+        pv[t] = (tok < n) ? x : z4;
+      }
+    }
+    if (wave == 0) {
+      const int tc = (lane < n) ? lane : n - 1;
+      const long idx = static_cast<long>(c0 + tc) * args.h_v + h;
+      const float a = args.log_alpha[idx];
+      const float bt = args.beta[idx];
+      pa = (lane < n) ? a : 0.f;
+      pbeta = (lane < n) ? bt : 0.f;
+    }
+  };
+
+  if (lo < hi) prefetch(lo);
+
+  for (int c0 = lo; c0 < hi; c0 += C) {
+    const int n = (hi - c0 < C) ? (hi - c0) : C;
+    // an opaque copy of the thread index keeps the compiler from hoisting every
+    // loop-invariant fragment address out of the chunk loop (each would pin a
+    // register for the whole loop); they are cheap to recompute per chunk
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int lane = tid & 63;
+    const int g = lane >> 4, ln = lane & 15;
+
+    // ---- phase 0: registers -> fragment-major LDS; gates ----------------------
+    if (k_thr || q_thr) {
+      u16* dst = k_thr ? fKd : fQ;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int tok = 4 * tq + t;
+        *reinterpret_cast<uint2*>(dst + frag_index(tok, 8 * dq, KTD)) =
+            make_uint2(pkq[t].x, pkq[t].y);
+        *reinterpret_cast<uint2*>(dst + frag_index(tok, 8 * dq + 4, KTD)) =
+            make_uint2(pkq[t].z, pkq[t].w);
+      }
+    }
+    if (k_thr) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        u16x4 col;
+        col[0] = bf16_bits(pkq[0], e);
+        col[1] = bf16_bits(pkq[1], e);
+        col[2] = bf16_bits(pkq[2], e);
+        col[3] = bf16_bits(pkq[3], e);
+        *reinterpret_cast<u16x4*>(fKt + frag_index(8 * dq + e, 4 * tq, KTC)) = col;
+      }
+    }
+    if (v_thr && has_state) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        u16x4 col;
+        col[0] = bf16_bits(pv[0], e);
+        col[1] = bf16_bits(pv[1], e);
+        col[2] = bf16_bits(pv[2], e);
+        col[3] = bf16_bits(pv[3], e);
+        *reinterpret_cast<u16x4*>(fV + frag_index(8 * vdq + e, 4 * vtq, KTC)) = col;
+      }
+    }
+    if (wave == 0) {
+      float b = pa;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const float u = __shfl_up(b, off, 64);
+        if (lane >= off) b += u;
+      }
+      const float b_last = __shfl(b, 63, 64);
+      gb[lane] = b;
+      gbeta[lane] = pbeta;
+      ggam[lane] = __expf(b);
+      gdec[lane] = __expf(b_last - b);
+    }
+    __syncthreads();
+    const float b_last = gb[C - 1];
+    log_decay += b_last;
+
+    // ---- phase 1: Gram -> L^T; K Q^T tiles; (Q S0)^T ----------------------------
+    // G tile t: wave 4 + t/2 for t < 8, waves 0 and 1 for t = 8, 9.
+    // KQ tile t: wave 4 + t/2 for t < 8, waves 2 and 3 for t = 8, 9.
+    f32x4 kq[2];
+    f32x4 oq[4];
+#pragma unroll
+    for (int t = 0; t < 10; ++t) {
+      const int owner = (t < 8) ? 4 + t / 2 : t - 8;
+      if (owner != wave) continue;
+      const int ti = tri_row(t), tj = tri_col(t);
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int kb = 0; kb < KTD; ++kb)
+        acc = mma(ld_frag(fKd, frag_slot(ti, kb, KTD, lane)),
+                  ld_frag(fKd, frag_slot(tj, kb, KTD, lane)), acc);
+      // L^T[c][r] = beta_r G[r][c] for c < r
+      const int c = tj * 16 + ln;
+      float4 o4;
+      float* o = reinterpret_cast<float*>(&o4);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = ti * 16 + 4 * g + i;
+        o[i] = (c < r) ? gbeta[r] * acc[i] : 0.f;
+      }
+      *reinterpret_cast<float4*>(Lt + c * LDC + ti * 16 + 4 * g) = o4;
+    }
+#pragma unroll
+    for (int t = 0; t < 10; ++t) {
+      const int owner = (t < 8) ? 4 + t / 2 : t - 6;
+      if (owner != wave) continue;
+      // rows: key tokens (tile ti), columns: query tokens (tile tr), ti <= tr
+      const int tr = tri_row(t), ti = tri_col(t);
+      f32x4 acc = zero4();
+#pragma unroll
+      for (int kb = 0; kb < KTD; ++kb)
+        acc = mma(ld_frag(fKd, frag_slot(ti, kb, KTD, lane)),
+                  ld_frag(fQ, frag_slot(tr, kb, KTD, lane)), acc);
+      kq[(t < 8) ? (t & 1) : 0] = acc;
+    }
+    if (sw && has_state) {
+      // (Q S0)^T = S0^T Q^T: lane (g, n) holds four consecutive state columns of
+      // query token n
+      bf16x8 s0h[KTD];
+#pragma unroll
+      for (int kb = 0; kb < KTD; ++kb) s0h[kb] = pack(st[2 * kb], st[2 * kb + 1]);
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kb = 0; kb < KTD; ++kb)
+          acc = mma(s0h[kb], ld_frag(fQ, frag_slot(rt, kb, KTD, lane)), acc);
+        oq[rt] = acc;
+      }
+    }
+    __syncthreads();
+
+    // ---- phase 2: A1 = (I + L)^{-1} ------------------------------------------------
+    // (a) diagonal block wave - 4 (operator waves): lane j < 16 solves column j
+#pragma unroll
+    for (int blk = 0; blk < 4; ++blk) {
+      if (blk + 4 != wave) continue;
+      const int o = blk * 16;
+      float x[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) x[r] = (r == ln) ? 1.f : 0.f;
+#pragma unroll
+      for (int i = 0; i < 15; ++i) {
+        // column i of L below the diagonal: L^T[o+i][o+r], r > i
+        const float4* colp = reinterpret_cast<const float4*>(Lt + (o + i) * LDC + o);
+        float lc[16];
+#pragma unroll
+        for (int q4 = (i + 1) / 4; q4 < 4; ++q4) {
+          const float4 v4 = colp[q4];
+          lc[4 * q4] = v4.x;
+          lc[4 * q4 + 1] = v4.y;
+          lc[4 * q4 + 2] = v4.z;
+          lc[4 * q4 + 3] = v4.w;
+        }
+#pragma unroll
+        for (int r = i + 1; r < 16; ++r) x[r] -= lc[r] * x[i];
+      }
+      if (g == 0) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) A1[(o + r) * LDC + o + ln] = x[r];
+        float4* tp = reinterpret_cast<float4*>(A1t + (o + ln) * LDC + o);
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4)
+          tp[q4] = make_float4(x[4 * q4], x[4 * q4 + 1], x[4 * q4 + 2], x[4 * q4 + 3]);
+      }
+    }
+    __syncthreads();
+    // (b) N_ik = A_ii L_ik for i > k, written row-major into the unused
+    //     lower-left block positions (i, k) of the L^T storage
+#pragma unroll
+    for (int p = 0; p < 6; ++p) {
+      if (p != wave) continue;
+      // pairs (1,0) (2,1) (3,2) (2,0) (3,1) (3,0)
+      const int bi = 16 * ((p < 3) ? p + 1 : ((p == 5) ? 3 : p - 1));
+      const int bk = 16 * ((p < 3) ? p : ((p == 4) ? 1 : 0));
+      const float4 a = *reinterpret_cast<const float4*>(A1 + (bi + ln) * LDC + bi + 4 * g);
+      const float4 b = *reinterpret_cast<const float4*>(Lt + (bk + ln) * LDC + bi + 4 * g);
+      const f32x4 acc = mma16_f32(a, b, zero4());
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Lt[(bi + 4 * g + i) * LDC + bk + ln] = acc[i];
+    }
+    __syncthreads();
+    // (c)-(e) A_ij = -sum_{k=j}^{i-1} N_ik A_kj, one block diagonal at a time
+#pragma unroll
+    for (int dist = 1; dist < 4; ++dist) {
+#pragma unroll
+      for (int bj = 0; bj < 4 - dist; ++bj) {
+        if (bj != wave) continue;
+        const int bi = bj + dist;
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int bk = bj; bk < bi; ++bk) {
+          const float4 a =
+              *reinterpret_cast<const float4*>(Lt + (bi * 16 + ln) * LDC + bk * 16 + 4 * g);
+          const float4 b =
+              *reinterpret_cast<const float4*>(A1t + (bj * 16 + ln) * LDC + bk * 16 + 4 * g);
+          acc = mma16_f32(a, b, acc);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) A1[(bi * 16 + 4 * g + i) * LDC + bj * 16 + ln] = -acc[i];
+        *reinterpret_cast<float4*>(A1t + (bj * 16 + ln) * LDC + bi * 16 + 4 * g) =
+            make_float4(-acc[0], -acc[1], -acc[2], -acc[3]);
+      }
+      __syncthreads();
+    }
+
+    // ---- phase 3: fragments of A1 diag(beta) (hi, lo), (A1 . Gamma) diag(beta) and
+    //               (Q K^T . Gamma) -------------------------------------------------------
+    {
+      // 512 slots of a 64 x 64 fragment matrix, one per thread
+      const int s = tid;
+      const int sl = s & 63, tile = s >> 6;
+      const int rt = tile / KTC, kt = tile % KTC;
+      const int sg = sl >> 4, r = rt * 16 + (sl & 15);
+      const int k0 = kt * 32 + 4 * sg;
+      const float4 a0 = *reinterpret_cast<const float4*>(A1 + r * LDC + k0);
+      const float4 a1 = *reinterpret_cast<const float4*>(A1 + r * LDC + k0 + 16);
+      const float4 b0 = *reinterpret_cast<const float4*>(gbeta + k0);
+      const float4 b1 = *reinterpret_cast<const float4*>(gbeta + k0 + 16);
+      const float4 e0 = *reinterpret_cast<const float4*>(gb + k0);
+      const float4 e1 = *reinterpret_cast<const float4*>(gb + k0 + 16);
+      const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+      const float ev[8] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
+      const float br = gb[r];
+      bf16x8 hh, ll, gg;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int i = k0 + ((j < 4) ? j : 12 + j);
+        const bool keep = (i <= r);
+        const float ab = keep ? av[j] * bv[j] : 0.f;
+        hh[j] = static_cast<__bf16>(ab);
+        ll[j] = static_cast<__bf16>(ab - static_cast<float>(hh[j]));
+        gg[j] = static_cast<__bf16>(keep ? ab * __expf(br - ev[j]) : 0.f);
+      }
+      st_frag(fAbh, s * 8, hh);
+      st_frag(fAbl, s * 8, ll);
+      st_frag(fAgb, s * 8, gg);
+    }
+    // (Q K^T . Gamma) as A-operand fragments over key tokens for query rows
+#pragma unroll
+    for (int t = 0; t < 10; ++t) {
+      const int owner = (t < 8) ? 4 + t / 2 : t - 6;
+      if (owner != wave) continue;
+      const int tr = tri_row(t), ti = tri_col(t);
+      const int r = tr * 16 + ln;
+      const float br = gb[r];
+      const f32x4 a = kq[(t < 8) ? (t & 1) : 0];
+      u16x4 val;
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int i = ti * 16 + 4 * g + i4;
+        val[i4] = bf16_of((i <= r) ? a[i4] * __expf(br - gb[i]) : 0.f);
+      }
+      *reinterpret_cast<u16x4*>(fQK + frag_slot(tr, ti >> 1, KTC, lane) + (ti & 1) * 4) = val;
+    }
+    // zero halves (key tile > query tile): (1,0) (2,0) (3,0) (2,1) (3,1) (3,2)
+#pragma unroll
+    for (int t = 0; t < 6; ++t) {
+      if (t != wave) continue;
+      const int ti = (t < 3) ? t + 1 : ((t == 5) ? 3 : t - 1);
+      const int tr = (t < 3) ? 0 : ((t == 5) ? 2 : 1);
+      *reinterpret_cast<uint2*>(fQK + frag_slot(tr, ti >> 1, KTC, lane) + (ti & 1) * 4) =
+          make_uint2(0u, 0u);
+    }
+    __syncthreads();
+    // the next chunk's tokens load while phases 4 and 5 compute
+    if (c0 + C < hi) prefetch(c0 + C);
+
+    // ---- phase 4: W^T tiles -> fragments (gamma W, W hi, W lo); U ---------------------
+    // job (rt, kb): query-token tile rt, d_k tile pair kb; job j goes to wave j % 8
+#pragma unroll
+    for (int j = 0; j < 4 * KTD; ++j) {
+      if ((j & 7) != wave) continue;
+      const int rt = j / KTD, kb = j % KTD;
+      f32x4 w2[2];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const int dt = 2 * kb + half;
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kt = 0; kt < KTC; ++kt) {
+          const bf16x8 a = ld_frag(fKt, frag_slot(dt, kt, KTC, lane));
+          acc = mma(a, ld_frag(fAbh, frag_slot(rt, kt, KTC, lane)), acc);
+          acc = mma(a, ld_frag(fAbl, frag_slot(rt, kt, KTC, lane)), acc);
+        }
+        w2[half] = acc;
+      }
+      const float gam = ggam[rt * 16 + ln];
+      bf16x8 hh, ll;
+      pack_split(w2[0], w2[1], hh, ll);
+      st_frag(fWh, frag_slot(rt, kb, KTD, lane), hh);
+      st_frag(fWl, frag_slot(rt, kb, KTD, lane), ll);
+      st_frag(fWs, frag_slot(rt, kb, KTD, lane), pack(w2[0] * gam, w2[1] * gam));
+    }
+    f32x4 u[4];
+    if (sw && has_state) {
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kt = 0; kt < KTC; ++kt)
+          acc = mma(ld_frag(fAgb, frag_slot(rt, kt, KTC, lane)),
+                    ld_frag(fV, frag_slot(wq, kt, KTC, lane)), acc);
+        u[rt] = acc;
+      }
+    }
+    __syncthreads();
+
+    // ---- phase 5: chain update -----------------------------------------------------------
+    if (sw && has_state) {
+      bf16x8 s0h[KTD];
+#pragma unroll
+      for (int kb = 0; kb < KTD; ++kb) s0h[kb] = pack(st[2 * kb], st[2 * kb + 1]);
+      // Vn = U - W' S0
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kb = 0; kb < KTD; ++kb)
+          acc = mma(ld_frag(fWs, frag_slot(rt, kb, KTD, lane)), s0h[kb], acc);
+        u[rt] -= acc;
+      }
+      bf16x8 vnf[KTC];
+#pragma unroll
+      for (int kt = 0; kt < KTC; ++kt) vnf[kt] = pack(u[2 * kt], u[2 * kt + 1]);
+      // O^T = (Q S0)^T diag(gamma) + Vn^T (Q K^T . Gamma)^T; lane (g, n) holds
+      // O[token rt*16 + n][col0 + 4g .. col0 + 4g + 3]
+      u16* og = static_cast<u16*>(args.o);
+      const long orow0 = (args.mode == 0) ? static_cast<long>(c0)
+                                          : static_cast<long>(seg) * args.w + (c0 - lo);
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        f32x4 acc = oq[rt] * ggam[rt * 16 + ln];
+#pragma unroll
+        for (int kt = 0; kt < KTC; ++kt)
+          if (2 * kt <= rt) acc = mma(vnf[kt], ld_frag(fQK, frag_slot(rt, kt, KTC, lane)), acc);
+        const int r = rt * 16 + ln;
+        if (og != nullptr && r < n) {
+          u16x4 o4;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) o4[i] = bf16_of(acc[i]);
+          *reinterpret_cast<u16x4*>(og + (orow0 + r) * v_stride + h * DV + col0 + 4 * g) = o4;
+        }
+      }
+      // S <- gamma_last S0 + K^T diag(exp(b_last - b)) Vn
+#pragma unroll
+      for (int kt = 0; kt < KTC; ++kt) {
+        const float4 d0 = *reinterpret_cast<const float4*>(gdec + kt * 32 + 4 * g);
+        const float4 d1 = *reinterpret_cast<const float4*>(gdec + kt * 32 + 16 + 4 * g);
+        f32x4 x0 = u[2 * kt], x1 = u[2 * kt + 1];
+        x0[0] *= d0.x;
+        x0[1] *= d0.y;
+        x0[2] *= d0.z;
+        x0[3] *= d0.w;
+        x1[0] *= d1.x;
+        x1[1] *= d1.y;
+        x1[2] *= d1.z;
+        x1[3] *= d1.w;
+        vnf[kt] = pack(x0, x1);
+      }
+      const float g_last = __expf(b_last);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        f32x4 acc = st[dt] * g_last;
+#pragma unroll
+        for (int kt = 0; kt < KTC; ++kt)
+          acc = mma(ld_frag(fKt, frag_slot(dt, kt, KTC, lane)), vnf[kt], acc);
+        st[dt] = acc;
+      }
+    } else if (!sw && has_op) {
+      // X = W P0 (three passes);  P <- P0 - K^T X (two passes, K exact)
+      bf16x8 p0h[KTD], p0l[KTD];
+#pragma unroll
+      for (int kb = 0; kb < KTD; ++kb) pack_split(st[2 * kb], st[2 * kb + 1], p0h[kb], p0l[kb]);
+      f32x4 x[4];
+#pragma unroll
+      for (int rt = 0; rt < 4; ++rt) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kb = 0; kb < KTD; ++kb) {
+          const bf16x8 wh = ld_frag(fWh, frag_slot(rt, kb, KTD, lane));
+          const bf16x8 wl = ld_frag(fWl, frag_slot(rt, kb, KTD, lane));
+          acc = mma(wh, p0h[kb], acc);
+          acc = mma(wh, p0l[kb], acc);
+          acc = mma(wl, p0h[kb], acc);
+        }
+        x[rt] = -acc;
+      }
+      bf16x8 xh[KTC], xl[KTC];
+#pragma unroll
+      for (int kt = 0; kt < KTC; ++kt) pack_split(x[2 * kt], x[2 * kt + 1], xh[kt], xl[kt]);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        f32x4 acc = st[dt];
+#pragma unroll
+        for (int kt = 0; kt < KTC; ++kt) {
+          const bf16x8 a = ld_frag(fKt, frag_slot(dt, kt, KTC, lane));
+          acc = mma(a, xh[kt], acc);
+          acc = mma(a, xl[kt], acc);
+        }
+        st[dt] = acc;
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- results ------------------------------------------------------------------------
+  if (!active) return;
+  if (sw) {
+    if (args.S_out != nullptr) {
+      float* so = args.S_out + sh * DK * DV;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) so[(dt * 16 + 4 * g + i) * DV + col0 + ln] = st[dt][i];
+    }
+    if (args.log_decay != nullptr && cb == 0 && tid == 0) args.log_decay[sh] = log_decay;
+  } else {
+    float* po = args.P_hat + sh * DK * DK;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) po[(dt * 16 + 4 * g + i) * DK + col0 + ln] = st[dt][i];
+  }
+}
+
+template <int DK, int DV>
+hipError_t launch_t(const ScanArgs& a, int n_items, hipStream_t s) {
+  constexpr int bytes = Lds<DK>::TOTAL;
+  // one-time (thread-safe static initialisation) opt-in to more than 64 KiB of LDS
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&scan_bf16_kernel<DK, DV>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((scan_bf16_kernel<DK, DV>), dim3(n_items), dim3(kThreads), bytes, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int scan_bf16_items_per_head(int d_k, int d_v, int with_operator) {
+  const int ns = d_v / NCOL, np = d_k / NCOL;
+  return (with_operator && np > ns) ? np : ns;
+}
+
+hipError_t launch_scan_bf16(const ScanArgs& a, int d_k, int d_v, int n_items, hipStream_t s) {
+  if (n_items <= 0) return hipSuccess;
+  if (d_k == 64 && d_v == 64) return launch_t<64, 64>(a, n_items, s);
+  if (d_k == 64 && d_v == 128) return launch_t<64, 128>(a, n_items, s);
+  if (d_k == 128 && d_v == 64) return launch_t<128, 64>(a, n_items, s);
+  return launch_t<128, 128>(a, n_items, s);
+}
+
+}  // namespace hypic
