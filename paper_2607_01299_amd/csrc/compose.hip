@@ -1,9 +1,9 @@
 // Segment composition, Eq. (6), for gfx950.
 //
-// One workgroup (4 waves) per (request, v-head).  The running state S
+// One workgroup of d_k / 16 waves per (request, v-head).  The running state S
 // (d_k x d_v, float32) stays on chip for the whole request: each wave owns a
-// band of d_k / 4 rows as matrix-core accumulators, and a transposed copy of
-// the full state sits in LDS as the shared B operand.  Per listed segment i
+// band of 16 rows as matrix-core accumulators, and a transposed copy of the
+// full state sits in LDS as the shared B operand.  Per listed segment i
 // every wave streams its rows of P_hat_i and S_seg_i straight from HBM into
 // registers (each byte of the pool tuple is read once) and computes
 //     S[band] <- exp(log_decay_i) * (P_hat_i[band, :] @ S) + S_seg_i[band]
@@ -20,13 +20,10 @@ namespace hypic {
 
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = 4;
-
 template <int DK, int DV, int P>
-__global__ __launch_bounds__(kThreads) void compose_kernel(ComposeArgs args) {
-  constexpr int RW = DK / kWaves;  // rows per wave
-  constexpr int MT = RW / 16;
+__global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
+  constexpr int RW = 16;           // rows per wave
+  constexpr int MT = 1;
   constexpr int NT = DV / 16;
   constexpr int LDT = DK + 4;      // transposed state row stride (floats)
   __shared__ float st_t[DV * LDT];  // st_t[n * LDT + k] = S[k][n]
@@ -61,10 +58,45 @@ __global__ __launch_bounds__(kThreads) void compose_kernel(ComposeArgs args) {
   publish();
   __syncthreads();
 
+  // The pool tuple of step j + 1 is loaded into registers while step j
+  // computes (software pipelining), so the HBM latency hides behind the
+  // matrix-core work and the barriers.
   const int j0 = args.req_offsets[req], j1 = args.req_offsets[req + 1];
+  float nP[MT][DK / 32][8];
+  f32x4 nS[MT][NT];
+  float nE = 0.f;
+  auto load_step = [&](int j) __attribute__((always_inline)) {
+    const long sh = static_cast<long>(args.seg_ids[j]) * args.h_v + h;
+    const float* Pi = args.P_hat + sh * DK * DK;
+    const float* Si = args.S_seg + sh * state_sz;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int kb = 0; kb < DK / 32; ++kb) frag_kcontig(Pi, DK, row0 + mt * 16 + ln, kb * 32, g, nP[mt][kb]);
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          nS[mt][nt][i] = Si[(row0 + mt * 16 + 4 * g + i) * DV + nt * 16 + ln];
+    nE = __expf(args.log_decay[sh]);
+  };
+  if (j0 < j1) load_step(j0);
   for (int j = j0; j < j1; ++j) {
-    const long seg = args.seg_ids[j];
-    const long sh = seg * args.h_v + h;
+    float cP[MT][DK / 32][8];
+    f32x4 cS[MT][NT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+      for (int kb = 0; kb < DK / 32; ++kb)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cP[mt][kb][e] = nP[mt][kb][e];
+#pragma unroll
+      for (int nt = 0; nt < NT; ++nt) cS[mt][nt] = nS[mt][nt];
+    }
+    const float e = nE;
+    if (j + 1 < j1) load_step(j + 1);
     if (args.S_incoming != nullptr) {
       float* dst = args.S_incoming + (static_cast<long>(j) * args.h_v + h) * state_sz;
 #pragma unroll
@@ -75,35 +107,25 @@ __global__ __launch_bounds__(kThreads) void compose_kernel(ComposeArgs args) {
           for (int i = 0; i < 4; ++i)
             dst[(row0 + mt * 16 + 4 * g + i) * DV + nt * 16 + ln] = s[mt][nt][i];
     }
-    const float* Pi = args.P_hat + sh * DK * DK;
-    const float* Si = args.S_seg + sh * state_sz;
     f32x4 prod[MT][NT];
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) prod[mt][nt] = zero4();
 #pragma unroll
-    for (int kb = 0; kb < DK; kb += 32) {
-      float fa[MT][8];
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) frag_kcontig(Pi, DK, row0 + mt * 16 + ln, kb, g, fa[mt]);
+    for (int kb = 0; kb < DK / 32; ++kb) {
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt) {
         float fb[8];
-        frag_kcontig(st_t, LDT, nt * 16 + ln, kb, g, fb);
+        frag_kcontig(st_t, LDT, nt * 16 + ln, kb * 32, g, fb);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) mma_blk<P>(prod[mt][nt], fa[mt], fb);
+        for (int mt = 0; mt < MT; ++mt) mma_blk<P>(prod[mt][nt], cP[mt][kb], fb);
       }
     }
-    const float e = __expf(args.log_decay[sh]);
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          s[mt][nt][i] = e * prod[mt][nt][i] +
-                         Si[(row0 + mt * 16 + 4 * g + i) * DV + nt * 16 + ln];
+      for (int nt = 0; nt < NT; ++nt) s[mt][nt] = prod[mt][nt] * e + cS[mt][nt];
     __syncthreads();  // every wave has read the old state
     publish();
     __syncthreads();
@@ -122,10 +144,11 @@ __global__ __launch_bounds__(kThreads) void compose_kernel(ComposeArgs args) {
 template <int DK, int DV>
 hipError_t launch_compose_d(const ComposeArgs& a, int f32, int n_req, hipStream_t s) {
   const dim3 grid(static_cast<unsigned>(n_req) * a.h_v);
+  const dim3 block(DK * 4);  // one wave per 16 state rows
   if (f32)
-    hipLaunchKernelGGL((compose_kernel<DK, DV, P_F32>), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((compose_kernel<DK, DV, P_F32>), grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL((compose_kernel<DK, DV, P_SPLIT>), grid, dim3(kThreads), 0, s, a);
+    hipLaunchKernelGGL((compose_kernel<DK, DV, P_SPLIT>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 

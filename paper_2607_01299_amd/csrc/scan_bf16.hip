@@ -128,8 +128,8 @@ struct Lds {
   static constexpr int O_Q = O_KD + RA;     // Q over d -> A1^T -> (QK . Gamma), (A1 . Gamma) beta
   static constexpr int O_KT = O_Q + RA;     // K over tokens
   static constexpr int O_L = O_KT + FK;     // L^T (f32) + N blocks -> A1 beta hi / lo
-  static constexpr int O_V = O_L + F32M;    // V (64 columns) over tokens
-  static constexpr int O_WS = O_V + NCOL * C * 2;  // gamma W (state path)
+  static constexpr int O_V = O_L + F32M;    // V (up to 128 columns) over tokens
+  static constexpr int O_WS = O_V + 2 * NCOL * C * 2;  // gamma W (state path)
   static constexpr int O_WL = O_WS + FK;           // W lo (operator path)
   static constexpr int O_G = O_WL + FK;            // gates
   static constexpr int TOTAL = O_G + 4 * C * 4;
@@ -171,18 +171,25 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63;
   const int g = lane >> 4, ln = lane & 15;
-  const bool sw = wave < 4;  // state wave (else operator wave)
-  const int wq = wave & 3;   // column tile of this wave within the block
+  // With the operator requested, waves 0-3 carry 64 state columns and waves
+  // 4-7 the same 64 operator columns.  Without it, all 8 waves carry state
+  // columns (128 per workgroup).
+  const bool with_op = args.n_roles == 2;
+  const bool sw = !with_op || wave < 4;  // state wave (else operator wave)
+  const int wq = with_op ? (wave & 3) : wave;  // column tile within the block
+  const int span = with_op ? NCOL : 2 * NCOL;  // state columns per workgroup
 
   // ---- work item ----------------------------------------------------------
-  const int n_cb = (args.n_roles == 2 && NP > NS) ? NP : NS;
+  const int n_cb = with_op ? ((NP > NS) ? NP : NS) : (DV + span - 1) / span;
   const int per_rank = n_cb * args.h_v;
   const int rank = blockIdx.x / per_rank;
   const int rem = blockIdx.x % per_rank;
   const int h = rem / n_cb;
   const int cb = rem % n_cb;
-  const bool has_state = cb < NS;
-  const bool has_op = (args.n_roles == 2) && (cb < NP);
+  const int col0 = cb * span + wq * 16;  // this wave's 16 columns (of S or P_hat)
+  const bool has_state = cb * span < DV;           // the block holds state columns
+  const bool has_op = with_op && (cb < NP);
+  const bool wave_cols = sw ? (col0 < DV) : has_op;  // does this wave own columns?
   int seg, lo, hi;
   if (args.mode == 0) {
     seg = args.order[rank];
@@ -196,7 +203,6 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   }
   lo = (lo < 0) ? 0 : ((lo > args.n_tokens) ? args.n_tokens : lo);
   hi = (hi < lo) ? lo : ((hi > args.n_tokens) ? args.n_tokens : hi);
-  const bool active = sw ? has_state : has_op;  // does this wave own columns?
 
   const int hk = h / args.group;
   const u16* kg = static_cast<const u16*>(args.k);
@@ -204,7 +210,6 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   const u16* vg = static_cast<const u16*>(args.v);
   const long qk_stride = static_cast<long>(args.h_qk) * DK;
   const long v_stride = static_cast<long>(args.h_v) * DV;
-  const int col0 = cb * NCOL + wq * 16;  // this wave's 16 columns (of S or P_hat)
   const long sh = static_cast<long>(seg) * args.h_v + h;
 
   // ---- chain state: 16 columns per wave, all d_k rows ------------------------
@@ -212,7 +217,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) st[dt] = zero4();
   if (sw) {
-    if (args.mode == 1 && has_state) {
+    if (args.mode == 1 && wave_cols) {
       const float* s_in = args.S_in + sh * DK * DV;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
@@ -228,14 +233,17 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   float log_decay = 0.f;
 
   // ---- prefetch of one chunk's tokens into registers -------------------------
-  // threads [0, 256): K units; [256, 512): Q units; [384, 512): also V units
+  // threads [0, 256): K units; [256, 512): Q units; the last VU threads also
+  // load the block's V columns (4 tokens x 8 columns per unit)
+  const int vcols = (DV - cb * span < span) ? DV - cb * span : span;  // V columns to load
+  const int VU = 16 * (vcols / 8);
   const int ku = tid & 255;
   const bool k_thr = tid < 256 && ku < KQU;
   const bool q_thr = tid >= 256 && ku < KQU;
-  const bool v_thr = tid >= 384;
+  const bool v_thr = has_state && tid >= kThreads - VU;
   const int tq = ku / (DK / 8), dq = ku % (DK / 8);
-  const int vu = tid - 384;
-  const int vtq = vu / (NCOL / 8), vdq = vu % (NCOL / 8);
+  const int vu = tid - (kThreads - VU);
+  const int vtq = vu / (vcols / 8), vdq = vu % (vcols / 8);
   uint4 pkq[4], pv[4];
   float pa = 0.f, pbeta = 0.f;
   const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
@@ -254,13 +262,13 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
         pkq[t] = (tok < n) ? x : z4;
       }
     }
-    if (v_thr && has_state) {
+    if (v_thr) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int tok = 4 * vtq + t;
         const int tc = (tok < n) ? tok : n - 1;
         const uint4 x = *reinterpret_cast<const uint4*>(vg + (c0 + tc) * v_stride + h * DV +
-                                                        cb * NCOL + 8 * vdq);
+                                                        cb * span + 8 * vdq);
         pv[t] = (tok < n) ? x : z4;
       }
     }
@@ -309,7 +317,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
         *reinterpret_cast<u16x4*>(fKt + frag_index(8 * dq + e, 4 * tq, KTC)) = col;
       }
     }
-    if (v_thr && has_state) {
+    if (v_thr) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         u16x4 col;
@@ -376,7 +384,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
                   ld_frag(fQ, frag_slot(tr, kb, KTD, lane)), acc);
       kq[(t < 8) ? (t & 1) : 0] = acc;
     }
-    if (sw && has_state) {
+    if (sw && wave_cols) {
       // (Q S0)^T = S0^T Q^T: lane (g, n) holds four consecutive state columns of
       // query token n
       bf16x8 s0h[KTD];
@@ -557,7 +565,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       st_frag(fWs, frag_slot(rt, kb, KTD, lane), pack(w2[0] * gam, w2[1] * gam));
     }
     f32x4 u[4];
-    if (sw && has_state) {
+    if (sw && wave_cols) {
 #pragma unroll
       for (int rt = 0; rt < 4; ++rt) {
         f32x4 acc = zero4();
@@ -571,7 +579,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     __syncthreads();
 
     // ---- phase 5: chain update -----------------------------------------------------------
-    if (sw && has_state) {
+    if (sw && wave_cols) {
       bf16x8 s0h[KTD];
 #pragma unroll
       for (int kb = 0; kb < KTD; ++kb) s0h[kb] = pack(st[2 * kb], st[2 * kb + 1]);
@@ -669,7 +677,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   }
 
   // ---- results ------------------------------------------------------------------------
-  if (!active) return;
+  if (!wave_cols) return;
   if (sw) {
     if (args.S_out != nullptr) {
       float* so = args.S_out + sh * DK * DV;
@@ -704,7 +712,8 @@ hipError_t launch_t(const ScanArgs& a, int n_items, hipStream_t s) {
 
 int scan_bf16_items_per_head(int d_k, int d_v, int with_operator) {
   const int ns = d_v / NCOL, np = d_k / NCOL;
-  return (with_operator && np > ns) ? np : ns;
+  if (!with_operator) return (d_v + 2 * NCOL - 1) / (2 * NCOL);
+  return (np > ns) ? np : ns;
 }
 
 hipError_t launch_scan_bf16(const ScanArgs& a, int d_k, int d_v, int n_items, hipStream_t s) {

@@ -310,3 +310,35 @@ def test_error_leaves_outputs_untouched(hy):
     assert torch.all(out == 7.0)
     with pytest.raises(hy.HypicError):
         hy.compose_segments(P, g, S, ids, offs)
+
+
+@pytest.mark.parametrize("dk,dv,heads", [(128, 128, (2, 4)), (128, 64, (1, 2)), (64, 128, (1, 1))])
+def test_build_without_operator(hy, dk, dv, heads):
+    """Without the operator every wave carries state columns; o and S_seg must
+    not change."""
+    lens = [150, 64, 1, 77]
+    _say("build without operator bf16 dk=%d dv=%d heads=%s" % (dk, dv, heads))
+    w = W.segment_workload(2, lengths=lens, heads=heads, d=dk)
+    if dk != dv:
+        rng = np.random.default_rng(11)
+        w.update(W.draw_tokens(rng, int(sum(lens)), heads[0], heads[1], dk, dv, W.BF16))
+    d = _dev(w)
+    cu = w["cu_seqlens"]
+    res = hy.build_segment(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], cu,
+                           want_operator=False)
+    full = hy.build_segment(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], cu)
+    torch.cuda.synchronize()
+    assert res["P_hat"] is None
+    ref = oracle.build_segments(w["q"], w["k"], w["v"], w["beta"], w["log_alpha"], cu,
+                                want_operator=False)
+    worst = 0.0
+    for s in range(len(lens)):
+        lo, hi = int(cu[s]), int(cu[s + 1])
+        for h in range(heads[1]):
+            worst = max(worst, rel(_np(res["o"][lo:hi, h]), ref["o"][lo:hi, h]),
+                        rel(_np(res["S_seg"][s, h]), ref["S_seg"][s, h]))
+    print("no-operator build max rel err %.2e" % worst, flush=True)
+    assert worst <= TOL[W.BF16]
+    # same arithmetic for the state with or without the operator columns
+    assert torch.equal(res["S_seg"], full["S_seg"])
+    assert torch.equal(res["o"], full["o"])
