@@ -110,6 +110,15 @@ __device__ __forceinline__ void frag_from_acc(const f32x4& lo, const f32x4& hi,
   }
 }
 
+// Workgroup barrier for hand-offs through LDS only: waits for this wave's own
+// LDS traffic, then meets the other waves.  Unlike __syncthreads() it does not
+// drain outstanding global loads and stores, so register prefetches and result
+// stores stay in flight across it.  Only for kernels in which no wave reads
+// global memory that another wave of the same launch writes.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 __device__ __forceinline__ f32x4 zero4() {
   f32x4 z = {0.f, 0.f, 0.f, 0.f};
   return z;

@@ -56,15 +56,6 @@ typedef u16 u16x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ int frag_slot(int rt, int kt, int KT, int lane) {
   return ((rt * KT + kt) * 64 + lane) * 8;
 }
-// element index of (row, k): lane (g, row % 16) with g = (k % 16) / 4,
-// slot j = 4 * ((k % 32) / 16) + k % 4
-__device__ __forceinline__ int frag_index(int row, int k, int KT) {
-  const int kk = k & 31;
-  const int g = (kk & 15) >> 2;
-  const int j = ((kk >> 4) << 2) | (kk & 3);
-  return (((row >> 4) * KT + (k >> 5)) * 64 + g * 16 + (row & 15)) * 8 + j;
-}
-
 __device__ __forceinline__ bf16x8 ld_frag(const u16* base, int slot) {
   return *reinterpret_cast<const bf16x8*>(base + slot);
 }
@@ -105,10 +96,6 @@ __device__ __forceinline__ f32x4 mma16_f32(const float4& a, const float4& b, f32
   return c;
 }
 
-__device__ __forceinline__ u16 bf16_bits(uint4 v, int e) {
-  const uint32_t w = (e < 2) ? v.x : (e < 4) ? v.y : (e < 6) ? v.z : v.w;
-  return static_cast<u16>((e & 1) ? (w >> 16) : (w & 0xffffu));
-}
 __device__ __forceinline__ u16 bf16_of(float x) {
   __bf16 h = static_cast<__bf16>(x);
   return *reinterpret_cast<u16*>(&h);
@@ -145,7 +132,6 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   constexpr int DT = DK / 16;   // d_k row tiles of the state
   constexpr int NS = DV / NCOL;
   constexpr int NP = DK / NCOL;
-  constexpr int KQU = 16 * (DK / 8);  // (4-token, 8-d) load units of K (and of Q)
 
   extern __shared__ __align__(16) unsigned char smem[];
   u16* fKd = reinterpret_cast<u16*>(smem + LP::O_KD);
@@ -171,6 +157,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63;
   const int g = lane >> 4, ln = lane & 15;
+  const int lane0 = lane, g0 = g, ln0 = ln;  // for the prefetch (outside the chunk loop)
   // With the operator requested, waves 0-3 carry 64 state columns and waves
   // 4-7 the same 64 operator columns.  Without it, all 8 waves carry state
   // columns (128 per workgroup).
@@ -233,52 +220,47 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   float log_decay = 0.f;
 
   // ---- prefetch of one chunk's tokens into registers -------------------------
-  // threads [0, 256): K units; [256, 512): Q units; the last VU threads also
-  // load the block's V columns (4 tokens x 8 columns per unit)
+  // Tokens are loaded as matrix-core A-operand fragments straight from HBM:
+  // lane (g, m) of fragment (token tile tt, column block kb) holds the 8
+  // columns kb*32 + kap(g, 0..7) of token tt*16 + m (two 8-byte loads).
+  // A "pair job" loads the two token tiles 2*kt, 2*kt + 1 of one column block.
+  //   K: pair job (kb, kt) on wave kb + KTD*kt      (waves [0, 2*KTD))
+  //   Q: pair job (kb, kt) on wave 8 - 2*KTD + ...  (waves [8 - 2*KTD, 8))
+  //   V: pair job (vb, kt) on wave vb + NVB*kt over this block's V columns
   const int vcols = (DV - cb * span < span) ? DV - cb * span : span;  // V columns to load
-  const int VU = 16 * (vcols / 8);
-  const int ku = tid & 255;
-  const bool k_thr = tid < 256 && ku < KQU;
-  const bool q_thr = tid >= 256 && ku < KQU;
-  const bool v_thr = has_state && tid >= kThreads - VU;
-  const int tq = ku / (DK / 8), dq = ku % (DK / 8);
-  const int vu = tid - (kThreads - VU);
-  const int vtq = vu / (vcols / 8), vdq = vu % (vcols / 8);
-  uint4 pkq[4], pv[4];
+  const int NVB = has_state ? vcols / 32 : 0;
+  const bool k_job = wave < 2 * KTD;
+  const int kjb = wave % KTD, kjt = wave / KTD;
+  const bool q_job = wave >= 8 - 2 * KTD;
+  const int qjb = (wave - (8 - 2 * KTD)) % KTD, qjt = (wave - (8 - 2 * KTD)) / KTD;
+  const bool v_job = NVB > 0 && wave < 2 * NVB;
+  const int vjb = (NVB > 0) ? wave % NVB : 0, vjt = (NVB > 0) ? wave / NVB : 0;
+  // Raw loads only: every use of the loaded words (the tail mask included)
+  // waits until phase 0 of the next chunk, so the loads stay in flight while
+  // phases 4 and 5 compute.  Element [2t + h] holds half h of token tile 2kt + t.
+  uint2 pk[4], pq[4], pv[4];
   float pa = 0.f, pbeta = 0.f;
-  const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
+  auto load_pair = [&](uint2 (&dst)[4], const u16* base, long rs, int col, int kt, int c0,
+                       int n) __attribute__((always_inline)) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int tok = (2 * kt + t) * 16 + ln0;
+      const int tc = (tok < n) ? tok : n - 1;  // clamped (valid) token; zeroed on use
+      const u16* p = base + (c0 + tc) * rs + col + 4 * g0;
+      dst[2 * t] = *reinterpret_cast<const uint2*>(p);
+      dst[2 * t + 1] = *reinterpret_cast<const uint2*>(p + 16);
+    }
+  };
   auto prefetch = [&](int c0) __attribute__((always_inline)) {
     const int n = (hi - c0 < C) ? (hi - c0) : C;  // n >= 1
-    // unconditional loads from a clamped (valid) token; padded rows are zeroed
-    // by value afterwards
-    if (k_thr || q_thr) {
-      const u16* src = k_thr ? kg : qg;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int tok = 4 * tq + t;
-        const int tc = (tok < n) ? tok : n - 1;
-        const uint4 x =
-            *reinterpret_cast<const uint4*>(src + (c0 + tc) * qk_stride + hk * DK + 8 * dq);
-        pkq[t] = (tok < n) ? x : z4;
-      }
-    }
-    if (v_thr) {
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int tok = 4 * vtq + t;
-        const int tc = (tok < n) ? tok : n - 1;
-        const uint4 x = *reinterpret_cast<const uint4*>(vg + (c0 + tc) * v_stride + h * DV +
-                                                        cb * span + 8 * vdq);
-        pv[t] = (tok < n) ? x : z4;
-      }
-    }
+    if (k_job) load_pair(pk, kg + hk * DK, qk_stride, kjb * 32, kjt, c0, n);
+    if (q_job) load_pair(pq, qg + hk * DK, qk_stride, qjb * 32, qjt, c0, n);
+    if (v_job) load_pair(pv, vg + h * DV + cb * span, v_stride, vjb * 32, vjt, c0, n);
     if (wave == 0) {
-      const int tc = (lane < n) ? lane : n - 1;
+      const int tc = (lane0 < n) ? lane0 : n - 1;
       const long idx = static_cast<long>(c0 + tc) * args.h_v + h;
-      const float a = args.log_alpha[idx];
-      const float bt = args.beta[idx];
-      pa = (lane < n) ? a : 0.f;
-      pbeta = (lane < n) ? bt : 0.f;
+      pa = args.log_alpha[idx];
+      pbeta = args.beta[idx];
     }
   };
 
@@ -294,42 +276,50 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     const int lane = tid & 63;
     const int g = lane >> 4, ln = lane & 15;
 
-    // ---- phase 0: registers -> fragment-major LDS; gates ----------------------
-    if (k_thr || q_thr) {
-      u16* dst = k_thr ? fKd : fQ;
+    // ---- phase 0: fragments -> LDS (lane-contiguous); transposed copies of K and
+    //      V by an exact identity product on the matrix cores; gates ----------------
+    {
+      // identity selector B operands: I[k][n] = (k == half*16 + n) over one
+      // 32-wide block, so (X I)[m][n] = X[m][half*16 + n] exactly
+      bf16x8 eye[2];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int tok = 4 * tq + t;
-        *reinterpret_cast<uint2*>(dst + frag_index(tok, 8 * dq, KTD)) =
-            make_uint2(pkq[t].x, pkq[t].y);
-        *reinterpret_cast<uint2*>(dst + frag_index(tok, 8 * dq + 4, KTD)) =
-            make_uint2(pkq[t].z, pkq[t].w);
+      for (int j = 0; j < 8; ++j) {
+        eye[0][j] = static_cast<__bf16>((j < 4 && 4 * g + j == ln) ? 1.f : 0.f);
+        eye[1][j] = static_cast<__bf16>((j >= 4 && 4 * g + j - 4 == ln) ? 1.f : 0.f);
       }
-    }
-    if (k_thr) {
+      // fragment t of a prefetched pair, with tokens past the chunk's end zeroed
+      auto take = [&](const uint2 (&src)[4], int kt, int t) __attribute__((always_inline)) {
+        const uint32_t keep = ((2 * kt + t) * 16 + ln < n) ? 0xffffffffu : 0u;
+        const uint2 lo2 = src[2 * t], hi2 = src[2 * t + 1];
+        return __builtin_bit_cast(
+            bf16x8, make_uint4(lo2.x & keep, lo2.y & keep, hi2.x & keep, hi2.y & keep));
+      };
+      auto transpose_pair = [&](bf16x8 f0, bf16x8 f1, u16* dst, int row_tile0, int kt)
+          __attribute__((always_inline)) {
+        // f0, f1: A fragments of token tiles 2kt, 2kt+1 over a 32-column block
+        // whose two 16-column halves become row tiles row_tile0 and row_tile0 + 1
+        // of the token-contraction fragments
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        u16x4 col;
-        col[0] = bf16_bits(pkq[0], e);
-        col[1] = bf16_bits(pkq[1], e);
-        col[2] = bf16_bits(pkq[2], e);
-        col[3] = bf16_bits(pkq[3], e);
-        *reinterpret_cast<u16x4*>(fKt + frag_index(8 * dq + e, 4 * tq, KTC)) = col;
+        for (int half = 0; half < 2; ++half) {
+          const f32x4 c_lo = mma(f0, eye[half], zero4());
+          const f32x4 c_hi = mma(f1, eye[half], zero4());
+          st_frag(dst, frag_slot(row_tile0 + half, kt, KTC, lane), pack(c_lo, c_hi));
+        }
+      };
+      if (k_job) {
+        const bf16x8 f0 = take(pk, kjt, 0), f1 = take(pk, kjt, 1);
+        st_frag(fKd, frag_slot(2 * kjt, kjb, KTD, lane), f0);
+        st_frag(fKd, frag_slot(2 * kjt + 1, kjb, KTD, lane), f1);
+        transpose_pair(f0, f1, fKt, 2 * kjb, kjt);
       }
-    }
-    if (v_thr) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        u16x4 col;
-        col[0] = bf16_bits(pv[0], e);
-        col[1] = bf16_bits(pv[1], e);
-        col[2] = bf16_bits(pv[2], e);
-        col[3] = bf16_bits(pv[3], e);
-        *reinterpret_cast<u16x4*>(fV + frag_index(8 * vdq + e, 4 * vtq, KTC)) = col;
+      if (q_job) {
+        st_frag(fQ, frag_slot(2 * qjt, qjb, KTD, lane), take(pq, qjt, 0));
+        st_frag(fQ, frag_slot(2 * qjt + 1, qjb, KTD, lane), take(pq, qjt, 1));
       }
+      if (v_job) transpose_pair(take(pv, vjt, 0), take(pv, vjt, 1), fV, 2 * vjb, vjt);
     }
     if (wave == 0) {
-      float b = pa;
+      float b = (lane < n) ? pa : 0.f;
 #pragma unroll
       for (int off = 1; off < 64; off <<= 1) {
         const float u = __shfl_up(b, off, 64);
@@ -337,11 +327,11 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       }
       const float b_last = __shfl(b, 63, 64);
       gb[lane] = b;
-      gbeta[lane] = pbeta;
+      gbeta[lane] = (lane < n) ? pbeta : 0.f;
       ggam[lane] = __expf(b);
       gdec[lane] = __expf(b_last - b);
     }
-    __syncthreads();
+    lds_barrier();
     const float b_last = gb[C - 1];
     log_decay += b_last;
 
@@ -399,7 +389,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
         oq[rt] = acc;
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- phase 2: A1 = (I + L)^{-1} ------------------------------------------------
     // (a) diagonal block wave - 4 (operator waves): lane j < 16 solves column j
@@ -410,21 +400,25 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       float x[16];
 #pragma unroll
       for (int r = 0; r < 16; ++r) x[r] = (r == ln) ? 1.f : 0.f;
+      // column i of L below the diagonal is L^T[o+i][o+r], r > i; columns are
+      // loaded two steps ahead so the LDS latency overlaps the substitution
+      float4 cbuf[3][4];
+      auto load_col = [&](int i, float4 (&dst)[4]) __attribute__((always_inline)) {
+        const float4* colp = reinterpret_cast<const float4*>(Lt + (o + i) * LDC + o);
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) dst[q4] = colp[q4];
+      };
+      load_col(0, cbuf[0]);
+      load_col(1, cbuf[1]);
 #pragma unroll
       for (int i = 0; i < 15; ++i) {
-        // column i of L below the diagonal: L^T[o+i][o+r], r > i
-        const float4* colp = reinterpret_cast<const float4*>(Lt + (o + i) * LDC + o);
-        float lc[16];
+        if (i + 2 < 15) load_col(i + 2, cbuf[(i + 2) % 3]);
 #pragma unroll
-        for (int q4 = (i + 1) / 4; q4 < 4; ++q4) {
-          const float4 v4 = colp[q4];
-          lc[4 * q4] = v4.x;
-          lc[4 * q4 + 1] = v4.y;
-          lc[4 * q4 + 2] = v4.z;
-          lc[4 * q4 + 3] = v4.w;
+        for (int r = i + 1; r < 16; ++r) {
+          const float4 q = cbuf[i % 3][r >> 2];
+          const float lr = ((r & 3) == 0) ? q.x : ((r & 3) == 1) ? q.y : ((r & 3) == 2) ? q.z : q.w;
+          x[r] -= lr * x[i];
         }
-#pragma unroll
-        for (int r = i + 1; r < 16; ++r) x[r] -= lc[r] * x[i];
       }
       if (g == 0) {
 #pragma unroll
@@ -435,7 +429,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
           tp[q4] = make_float4(x[4 * q4], x[4 * q4 + 1], x[4 * q4 + 2], x[4 * q4 + 3]);
       }
     }
-    __syncthreads();
+    lds_barrier();
     // (b) N_ik = A_ii L_ik for i > k, written row-major into the unused
     //     lower-left block positions (i, k) of the L^T storage
 #pragma unroll
@@ -450,7 +444,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) Lt[(bi + 4 * g + i) * LDC + bk + ln] = acc[i];
     }
-    __syncthreads();
+    lds_barrier();
     // (c)-(e) A_ij = -sum_{k=j}^{i-1} N_ik A_kj, one block diagonal at a time
 #pragma unroll
     for (int dist = 1; dist < 4; ++dist) {
@@ -472,7 +466,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
         *reinterpret_cast<float4*>(A1t + (bj * 16 + ln) * LDC + bi * 16 + 4 * g) =
             make_float4(-acc[0], -acc[1], -acc[2], -acc[3]);
       }
-      __syncthreads();
+      lds_barrier();
     }
 
     // ---- phase 3: fragments of A1 diag(beta) (hi, lo), (A1 . Gamma) diag(beta) and
@@ -534,7 +528,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       *reinterpret_cast<uint2*>(fQK + frag_slot(tr, ti >> 1, KTC, lane) + (ti & 1) * 4) =
           make_uint2(0u, 0u);
     }
-    __syncthreads();
+    lds_barrier();
     // the next chunk's tokens load while phases 4 and 5 compute
     if (c0 + C < hi) prefetch(c0 + C);
 
@@ -576,7 +570,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
         u[rt] = acc;
       }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- phase 5: chain update -----------------------------------------------------------
     if (sw && wave_cols) {
@@ -673,7 +667,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
         st[dt] = acc;
       }
     }
-    __syncthreads();
+    lds_barrier();
   }
 
   // ---- results ------------------------------------------------------------------------
