@@ -22,9 +22,12 @@
 // * Gates are exponentiated once per chunk (b = prefix sum of log alpha,
 //   gamma = exp(b), exp(b_last - b)); every decay factor is exp of a
 //   non-positive number.
-// * The inverse: 16 x 16 diagonal blocks by column-parallel substitution, then
-//   the off-diagonal blocks A_ij = -sum_k N_ik A_kj with N_ik = A_ii L_ik on
-//   float32 matrix cores, one block diagonal at a time.
+// * The inverse: the four 16 x 16 diagonal blocks by column-parallel
+//   substitution in one wave (one 16-lane row per block, coefficients shared
+//   by DPP row broadcasts), overlapping the other waves' Gram and K Q^T tiles;
+//   then the off-diagonal blocks
+//   A_ij = -sum_k N_ik A_kj with N_ik = A_ii L_ik on float32 matrix cores, one
+//   block diagonal at a time.
 // * The next chunk's q, k, v, beta, log alpha are loaded into registers while
 //   the current chunk computes.
 // * Precision: W is formed in two bf16 passes (A1 diag(beta) split hi + lo, K
@@ -47,6 +50,7 @@ constexpr int C = 64;        // tokens per chunk
 constexpr int NCOL = 64;     // state / operator columns per workgroup
 constexpr int KTC = C / 32;  // 32-wide contraction blocks over the chunk's tokens
 constexpr int LDC = C + 4;   // row stride (floats) of the float32 chunk x chunk matrices
+constexpr int LDD = 20;      // row stride (floats) of the staged diagonal blocks of A1
 
 typedef unsigned short u16;
 typedef u16 u16x4 __attribute__((ext_vector_type(4)));
@@ -101,6 +105,24 @@ __device__ __forceinline__ u16 bf16_of(float x) {
   return *reinterpret_cast<u16*>(&h);
 }
 
+// Step I of the column-parallel unit-lower substitution on 16-lane rows: lane
+// 16b + c holds column c of the solution (x) and column c of -L (lcol); the
+// coefficient -L[r][I] comes from lane I of the same row (DPP row_newbcast:I).
+template <int I>
+__device__ __forceinline__ void unit_lower_solve_step(float (&x)[16], const float (&lcol)[16]) {
+  if constexpr (I < 15) {
+    float nl[16];
+#pragma unroll
+    for (int r = I + 1; r < 16; ++r)
+      nl[r] = __builtin_bit_cast(
+          float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, lcol[r]), 0x150 + I, 0xF, 0xF,
+                                          false));
+#pragma unroll
+    for (int r = I + 1; r < 16; ++r) x[r] = __builtin_fmaf(nl[r], x[I], x[r]);
+    unit_lower_solve_step<I + 1>(x, lcol);
+  }
+}
+
 // lower-triangle tile t in 0..9 -> (row tile, column tile) with column <= row
 __device__ __forceinline__ int tri_row(int t) { return (t < 1) ? 0 : (t < 3) ? 1 : (t < 6) ? 2 : 3; }
 __device__ __forceinline__ int tri_col(int t) { return t - tri_row(t) * (tri_row(t) + 1) / 2; }
@@ -122,6 +144,7 @@ struct Lds {
   static constexpr int TOTAL = O_G + 4 * C * 4;
   static_assert(2 * C * C * 2 <= F32M, "A1 beta hi + lo fit the L region");
   static_assert(2 * C * C * 2 <= RA, "QK and (A1 . Gamma) beta fit the Q region");
+  static_assert(C * LDD * 4 <= FK, "staged diagonal blocks fit the W lo region");
   static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
@@ -152,6 +175,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   float* gbeta = gb + C;
   float* ggam = gb + 2 * C;
   float* gdec = gb + 3 * C;
+  float* Dg = reinterpret_cast<float*>(smem + LP::O_WL);  // diagonal blocks of A1 (phase 1-2)
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -335,36 +359,72 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     const float b_last = gb[C - 1];
     log_decay += b_last;
 
-    // ---- phase 1: Gram -> L^T; K Q^T tiles; (Q S0)^T ----------------------------
-    // G tile t: wave 4 + t/2 for t < 8, waves 0 and 1 for t = 8, 9.
-    // KQ tile t: wave 4 + t/2 for t < 8, waves 2 and 3 for t = 8, 9.
-    f32x4 kq[2];
+    // ---- phase 1: Gram tiles; diagonal blocks of A1 = (I + L)^{-1}; K Q^T; (Q S0)^T --
+    // Wave 4 forms the four diagonal Gram tiles, parks L_bb^T in the diagonal
+    // blocks of the L^T storage, reads column c of L_bb back into lane 16b + c and
+    // inverts all four blocks at once by unit-lower substitution, one lane per
+    // column: the coefficient L[r][i] reaches every lane of row b by a DPP row
+    // broadcast from lane i.  Off-diagonal Gram tiles (as L^T) go to waves 0-3,
+    // K Q^T tiles to waves 5-7.
+    f32x4 kq[4];
     f32x4 oq[4];
+    float xd[16];  // wave 4, lane 16b + c: column c of the inverse diagonal block b
+    if (wave == 4) {
 #pragma unroll
-    for (int t = 0; t < 10; ++t) {
-      const int owner = (t < 8) ? 4 + t / 2 : t - 8;
-      if (owner != wave) continue;
-      const int ti = tri_row(t), tj = tri_col(t);
+      for (int bd = 0; bd < 4; ++bd) {
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kb = 0; kb < KTD; ++kb) {
+          const bf16x8 f = ld_frag(fKd, frag_slot(bd, kb, KTD, lane));
+          acc = mma(f, f, acc);
+        }
+        // lane (g, n) holds G[r][n], r = 4g + s; -L^T[n][r] = -beta_r G[r][n] for n < r
+        const float4 bb = *reinterpret_cast<const float4*>(gbeta + bd * 16 + 4 * g);
+        const float bv[4] = {bb.x, bb.y, bb.z, bb.w};
+        float4 o4;
+        float* o = reinterpret_cast<float*>(&o4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = (ln < 4 * g + i) ? -bv[i] * acc[i] : 0.f;
+        *reinterpret_cast<float4*>(Lt + (bd * 16 + ln) * LDC + bd * 16 + 4 * g) = o4;
+      }
+      // LDS operations of one wave complete in issue order: no barrier needed
+      const int ob = (lane >> 4) * 16;
+      float lcol[16];  // -L[r][ln] of block lane / 16
+      const float4* colp = reinterpret_cast<const float4*>(Lt + (ob + ln) * LDC + ob);
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float4 t4 = colp[q4];
+        lcol[4 * q4] = t4.x;
+        lcol[4 * q4 + 1] = t4.y;
+        lcol[4 * q4 + 2] = t4.z;
+        lcol[4 * q4 + 3] = t4.w;
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) xd[r] = (r == ln) ? 1.f : 0.f;
+      unit_lower_solve_step<0>(xd, lcol);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) Dg[(ob + r) * LDD + ln] = xd[r];
+    }
+    // off-diagonal Gram tiles (1,0) (2,0) (2,1) (3,0) (3,1) (3,2)
+#pragma unroll
+    for (int j = 0; j < 6; ++j) {
+      if ((j & 3) != wave) continue;
+      const int ti = (j < 1) ? 1 : (j < 3) ? 2 : 3;
+      const int tj = (j < 1) ? 0 : (j < 3) ? j - 1 : j - 3;
       f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < KTD; ++kb)
         acc = mma(ld_frag(fKd, frag_slot(ti, kb, KTD, lane)),
                   ld_frag(fKd, frag_slot(tj, kb, KTD, lane)), acc);
-      // L^T[c][r] = beta_r G[r][c] for c < r
+      // L^T[c][r] = beta_r G[r][c]  (c < r throughout an off-diagonal tile)
       const int c = tj * 16 + ln;
-      float4 o4;
-      float* o = reinterpret_cast<float*>(&o4);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = ti * 16 + 4 * g + i;
-        o[i] = (c < r) ? gbeta[r] * acc[i] : 0.f;
-      }
-      *reinterpret_cast<float4*>(Lt + c * LDC + ti * 16 + 4 * g) = o4;
+      const float4 bb = *reinterpret_cast<const float4*>(gbeta + ti * 16 + 4 * g);
+      *reinterpret_cast<float4*>(Lt + c * LDC + ti * 16 + 4 * g) =
+          make_float4(bb.x * acc[0], bb.y * acc[1], bb.z * acc[2], bb.w * acc[3]);
     }
 #pragma unroll
     for (int t = 0; t < 10; ++t) {
-      const int owner = (t < 8) ? 4 + t / 2 : t - 6;
-      if (owner != wave) continue;
+      if (5 + t % 3 != wave) continue;
       // rows: key tokens (tile ti), columns: query tokens (tile tr), ti <= tr
       const int tr = tri_row(t), ti = tri_col(t);
       f32x4 acc = zero4();
@@ -372,7 +432,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       for (int kb = 0; kb < KTD; ++kb)
         acc = mma(ld_frag(fKd, frag_slot(ti, kb, KTD, lane)),
                   ld_frag(fQ, frag_slot(tr, kb, KTD, lane)), acc);
-      kq[(t < 8) ? (t & 1) : 0] = acc;
+      kq[t / 3] = acc;
     }
     if (sw && wave_cols) {
       // (Q S0)^T = S0^T Q^T: lane (g, n) holds four consecutive state columns of
@@ -391,45 +451,17 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     }
     lds_barrier();
 
-    // ---- phase 2: A1 = (I + L)^{-1} ------------------------------------------------
-    // (a) diagonal block wave - 4 (operator waves): lane j < 16 solves column j
+    // ---- phase 2: the rest of A1 -------------------------------------------------------
+    // (a) the diagonal blocks move from their staging copy into A1 and A1^T
+    if (wave == 4) {
+      const int o = (lane >> 4) * 16;
 #pragma unroll
-    for (int blk = 0; blk < 4; ++blk) {
-      if (blk + 4 != wave) continue;
-      const int o = blk * 16;
-      float x[16];
+      for (int r = 0; r < 16; ++r) A1[(o + r) * LDC + o + ln] = xd[r];
+      float4* tp = reinterpret_cast<float4*>(A1t + (o + ln) * LDC + o);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) x[r] = (r == ln) ? 1.f : 0.f;
-      // column i of L below the diagonal is L^T[o+i][o+r], r > i; columns are
-      // loaded two steps ahead so the LDS latency overlaps the substitution
-      float4 cbuf[3][4];
-      auto load_col = [&](int i, float4 (&dst)[4]) __attribute__((always_inline)) {
-        const float4* colp = reinterpret_cast<const float4*>(Lt + (o + i) * LDC + o);
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) dst[q4] = colp[q4];
-      };
-      load_col(0, cbuf[0]);
-      load_col(1, cbuf[1]);
-#pragma unroll
-      for (int i = 0; i < 15; ++i) {
-        if (i + 2 < 15) load_col(i + 2, cbuf[(i + 2) % 3]);
-#pragma unroll
-        for (int r = i + 1; r < 16; ++r) {
-          const float4 q = cbuf[i % 3][r >> 2];
-          const float lr = ((r & 3) == 0) ? q.x : ((r & 3) == 1) ? q.y : ((r & 3) == 2) ? q.z : q.w;
-          x[r] -= lr * x[i];
-        }
-      }
-      if (g == 0) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) A1[(o + r) * LDC + o + ln] = x[r];
-        float4* tp = reinterpret_cast<float4*>(A1t + (o + ln) * LDC + o);
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4)
-          tp[q4] = make_float4(x[4 * q4], x[4 * q4 + 1], x[4 * q4 + 2], x[4 * q4 + 3]);
-      }
+      for (int q4 = 0; q4 < 4; ++q4)
+        tp[q4] = make_float4(xd[4 * q4], xd[4 * q4 + 1], xd[4 * q4 + 2], xd[4 * q4 + 3]);
     }
-    lds_barrier();
     // (b) N_ik = A_ii L_ik for i > k, written row-major into the unused
     //     lower-left block positions (i, k) of the L^T storage
 #pragma unroll
@@ -438,7 +470,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       // pairs (1,0) (2,1) (3,2) (2,0) (3,1) (3,0)
       const int bi = 16 * ((p < 3) ? p + 1 : ((p == 5) ? 3 : p - 1));
       const int bk = 16 * ((p < 3) ? p : ((p == 4) ? 1 : 0));
-      const float4 a = *reinterpret_cast<const float4*>(A1 + (bi + ln) * LDC + bi + 4 * g);
+      const float4 a = *reinterpret_cast<const float4*>(Dg + (bi + ln) * LDD + 4 * g);
       const float4 b = *reinterpret_cast<const float4*>(Lt + (bk + ln) * LDC + bi + 4 * g);
       const f32x4 acc = mma16_f32(a, b, zero4());
 #pragma unroll
@@ -505,12 +537,11 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     // (Q K^T . Gamma) as A-operand fragments over key tokens for query rows
 #pragma unroll
     for (int t = 0; t < 10; ++t) {
-      const int owner = (t < 8) ? 4 + t / 2 : t - 6;
-      if (owner != wave) continue;
+      if (5 + t % 3 != wave) continue;
       const int tr = tri_row(t), ti = tri_col(t);
       const int r = tr * 16 + ln;
       const float br = gb[r];
-      const f32x4 a = kq[(t < 8) ? (t & 1) : 0];
+      const f32x4 a = kq[t / 3];
       u16x4 val;
 #pragma unroll
       for (int i4 = 0; i4 < 4; ++i4) {
