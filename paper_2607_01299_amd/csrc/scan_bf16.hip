@@ -54,6 +54,7 @@ constexpr int LDD = 20;      // row stride (floats) of the staged diagonal block
 
 typedef unsigned short u16;
 typedef u16 u16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 // ---- fragment-major layout -------------------------------------------------
 // logical R x K matrix (contraction over K), KT = K / 32 blocks per row tile.
@@ -137,8 +138,7 @@ struct Lds {
   static constexpr int O_Q = O_KD + RA;     // Q over d -> A1^T -> (QK . Gamma), (A1 . Gamma) beta
   static constexpr int O_KT = O_Q + RA;     // K over tokens
   static constexpr int O_L = O_KT + FK;     // L^T (f32) + N blocks -> A1 beta hi / lo
-  static constexpr int O_V = O_L + F32M;    // V (up to 128 columns) over tokens
-  static constexpr int O_WS = O_V + 2 * NCOL * C * 2;  // gamma W (state path)
+  static constexpr int O_WS = O_L + F32M;   // gamma W (state path)
   static constexpr int O_WL = O_WS + FK;           // W lo (operator path)
   static constexpr int O_G = O_WL + FK;            // gates
   static constexpr int TOTAL = O_G + 4 * C * 4;
@@ -168,7 +168,6 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   float* Lt = reinterpret_cast<float*>(smem + LP::O_L);
   u16* fAbh = reinterpret_cast<u16*>(smem + LP::O_L);
   u16* fAbl = fAbh + C * C;
-  u16* fV = reinterpret_cast<u16*>(smem + LP::O_V);
   u16* fWs = reinterpret_cast<u16*>(smem + LP::O_WS);
   u16* fWl = reinterpret_cast<u16*>(smem + LP::O_WL);
   float* gb = reinterpret_cast<float*>(smem + LP::O_G);
@@ -250,19 +249,18 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   // A "pair job" loads the two token tiles 2*kt, 2*kt + 1 of one column block.
   //   K: pair job (kb, kt) on wave kb + KTD*kt      (waves [0, 2*KTD))
   //   Q: pair job (kb, kt) on wave 8 - 2*KTD + ...  (waves [8 - 2*KTD, 8))
-  //   V: pair job (vb, kt) on wave vb + NVB*kt over this block's V columns
-  const int vcols = (DV - cb * span < span) ? DV - cb * span : span;  // V columns to load
-  const int NVB = has_state ? vcols / 32 : 0;
+  //   V: every state wave loads its own 16 columns, lane (g, m) of token tile tt
+  //      holding columns col0 + 4g .. col0 + 4g + 3 of token tt*16 + m
   const bool k_job = wave < 2 * KTD;
   const int kjb = wave % KTD, kjt = wave / KTD;
   const bool q_job = wave >= 8 - 2 * KTD;
   const int qjb = (wave - (8 - 2 * KTD)) % KTD, qjt = (wave - (8 - 2 * KTD)) / KTD;
-  const bool v_job = NVB > 0 && wave < 2 * NVB;
-  const int vjb = (NVB > 0) ? wave % NVB : 0, vjt = (NVB > 0) ? wave / NVB : 0;
+  const bool v_job = sw && wave_cols;
   // Raw loads only: every use of the loaded words (the tail mask included)
   // waits until phase 0 of the next chunk, so the loads stay in flight while
   // phases 4 and 5 compute.  Element [2t + h] holds half h of token tile 2kt + t.
   uint2 pk[4], pq[4], pv[4];
+  bf16x8 vB[KTC];  // state waves: this chunk's V columns as B fragments (phase 0 -> 4)
   float pa = 0.f, pbeta = 0.f;
   auto load_pair = [&](uint2 (&dst)[4], const u16* base, long rs, int col, int kt, int c0,
                        int n) __attribute__((always_inline)) {
@@ -279,7 +277,15 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     const int n = (hi - c0 < C) ? (hi - c0) : C;  // n >= 1
     if (k_job) load_pair(pk, kg + hk * DK, qk_stride, kjb * 32, kjt, c0, n);
     if (q_job) load_pair(pq, qg + hk * DK, qk_stride, qjb * 32, qjt, c0, n);
-    if (v_job) load_pair(pv, vg + h * DV + cb * span, v_stride, vjb * 32, vjt, c0, n);
+    if (v_job) {
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        const int tok = tt * 16 + ln0;
+        const int tc = (tok < n) ? tok : n - 1;
+        pv[tt] = *reinterpret_cast<const uint2*>(vg + (c0 + tc) * v_stride + h * DV + col0 +
+                                                 4 * g0);
+      }
+    }
     if (wave == 0) {
       const int tc = (lane0 < n) ? lane0 : n - 1;
       const long idx = static_cast<long>(c0 + tc) * args.h_v + h;
@@ -340,7 +346,24 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
         st_frag(fQ, frag_slot(2 * qjt, qjb, KTD, lane), take(pq, qjt, 0));
         st_frag(fQ, frag_slot(2 * qjt + 1, qjb, KTD, lane), take(pq, qjt, 1));
       }
-      if (v_job) transpose_pair(take(pv, vjt, 0), take(pv, vjt, 1), fV, 2 * vjb, vjt);
+      if (v_job) {
+        // this wave's V columns as token-contraction B fragments, by exact
+        // 16x16x16 identity products: (V_tt I)[m][n] lands in lane (g, n) as
+        // rows 4g .. 4g+3, i.e. tokens along the contraction
+        s16x4 eye16;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) eye16[j] = (4 * g + j == ln) ? short(0x3F80) : short(0);
+        f32x4 vt[4];
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt) {
+          const uint32_t keep = (tt * 16 + ln < n) ? 0xffffffffu : 0u;
+          const uint2 w2 = make_uint2(pv[tt].x & keep, pv[tt].y & keep);
+          vt[tt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, w2),
+                                                             eye16, zero4(), 0, 0, 0);
+        }
+        vB[0] = pack(vt[0], vt[1]);
+        vB[1] = pack(vt[2], vt[3]);
+      }
     }
     if (wave == 0) {
       float b = (lane < n) ? pa : 0.f;
@@ -597,7 +620,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
 #pragma unroll
         for (int kt = 0; kt < KTC; ++kt)
           acc = mma(ld_frag(fAgb, frag_slot(rt, kt, KTC, lane)),
-                    ld_frag(fV, frag_slot(wq, kt, KTC, lane)), acc);
+                    vB[kt], acc);
         u[rt] = acc;
       }
     }
