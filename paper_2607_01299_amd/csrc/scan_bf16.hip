@@ -124,6 +124,17 @@ __device__ __forceinline__ void unit_lower_solve_step(float (&x)[16], const floa
   }
 }
 
+// Row order of the d_k dimension inside the kernel.  q and k are loaded 16
+// contiguous bytes per lane (lane (g, m) of a 32-column block holds columns
+// 8g .. 8g+7), which makes a matrix-core slot (g, j) carry column 8g + j.  The
+// transposed K tiles, and with them the state and operator rows, are laid out
+// so that packing row tiles (2kb, 2kb+1) from accumulators gives exactly that
+// slot order: row m of d_k tile dt is d = d_perm(dt, m).  Rows are mapped back
+// to their true index only where a state or operator enters or leaves HBM.
+__device__ __forceinline__ int d_perm(int dt, int m) {
+  return 32 * (dt >> 1) + 8 * (m >> 2) + 4 * (dt & 1) + (m & 3);
+}
+
 // lower-triangle tile t in 0..9 -> (row tile, column tile) with column <= row
 __device__ __forceinline__ int tri_row(int t) { return (t < 1) ? 0 : (t < 3) ? 1 : (t < 6) ? 2 : 3; }
 __device__ __forceinline__ int tri_col(int t) { return t - tri_row(t) * (tri_row(t) + 1) / 2; }
@@ -232,20 +243,20 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) st[dt][i] = s_in[(dt * 16 + 4 * g + i) * DV + col0 + ln];
+        for (int i = 0; i < 4; ++i) st[dt][i] = s_in[d_perm(dt, 4 * g + i) * DV + col0 + ln];
     }
   } else {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) st[dt][i] = (dt * 16 + 4 * g + i == col0 + ln) ? 1.f : 0.f;
+      for (int i = 0; i < 4; ++i) st[dt][i] = (d_perm(dt, 4 * g + i) == col0 + ln) ? 1.f : 0.f;
   }
   float log_decay = 0.f;
 
   // ---- prefetch of one chunk's tokens into registers -------------------------
   // Tokens are loaded as matrix-core A-operand fragments straight from HBM:
   // lane (g, m) of fragment (token tile tt, column block kb) holds the 8
-  // columns kb*32 + kap(g, 0..7) of token tt*16 + m (two 8-byte loads).
+  // columns kb*32 + 8g .. kb*32 + 8g + 7 of token tt*16 + m (one 16-byte load).
   // A "pair job" loads the two token tiles 2*kt, 2*kt + 1 of one column block.
   //   K: pair job (kb, kt) on wave kb + KTD*kt      (waves [0, 2*KTD))
   //   Q: pair job (kb, kt) on wave 8 - 2*KTD + ...  (waves [8 - 2*KTD, 8))
@@ -259,18 +270,17 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   // Raw loads only: every use of the loaded words (the tail mask included)
   // waits until phase 0 of the next chunk, so the loads stay in flight while
   // phases 4 and 5 compute.  Element [2t + h] holds half h of token tile 2kt + t.
-  uint2 pk[4], pq[4], pv[4];
+  uint4 pk[2], pq[2];
+  uint2 pv[4];
   bf16x8 vB[KTC];  // state waves: this chunk's V columns as B fragments (phase 0 -> 4)
   float pa = 0.f, pbeta = 0.f;
-  auto load_pair = [&](uint2 (&dst)[4], const u16* base, long rs, int col, int kt, int c0,
+  auto load_pair = [&](uint4 (&dst)[2], const u16* base, long rs, int col, int kt, int c0,
                        int n) __attribute__((always_inline)) {
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int tok = (2 * kt + t) * 16 + ln0;
       const int tc = (tok < n) ? tok : n - 1;  // clamped (valid) token; zeroed on use
-      const u16* p = base + (c0 + tc) * rs + col + 4 * g0;
-      dst[2 * t] = *reinterpret_cast<const uint2*>(p);
-      dst[2 * t + 1] = *reinterpret_cast<const uint2*>(p + 16);
+      dst[t] = *reinterpret_cast<const uint4*>(base + (c0 + tc) * rs + col + 8 * g0);
     }
   };
   auto prefetch = [&](int c0) __attribute__((always_inline)) {
@@ -309,20 +319,21 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     // ---- phase 0: fragments -> LDS (lane-contiguous); transposed copies of K and
     //      V by an exact identity product on the matrix cores; gates ----------------
     {
-      // identity selector B operands: I[k][n] = (k == half*16 + n) over one
-      // 32-wide block, so (X I)[m][n] = X[m][half*16 + n] exactly
+      // selector B operands: slot (g', j') of lane (g', n) holds column
+      // 8g' + j' of the loaded 32-column block, so eye[half] = 1 exactly where
+      // 8g' + j' = d_perm(half, n) and (X eye[half])[m][n] = X[m][d_perm(half, n)]
       bf16x8 eye[2];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        eye[0][j] = static_cast<__bf16>((j < 4 && 4 * g + j == ln) ? 1.f : 0.f);
-        eye[1][j] = static_cast<__bf16>((j >= 4 && 4 * g + j - 4 == ln) ? 1.f : 0.f);
+        eye[0][j] = static_cast<__bf16>((g == (ln >> 2) && j == (ln & 3)) ? 1.f : 0.f);
+        eye[1][j] = static_cast<__bf16>((g == (ln >> 2) && j == 4 + (ln & 3)) ? 1.f : 0.f);
       }
       // fragment t of a prefetched pair, with tokens past the chunk's end zeroed
-      auto take = [&](const uint2 (&src)[4], int kt, int t) __attribute__((always_inline)) {
+      auto take = [&](const uint4 (&src)[2], int kt, int t) __attribute__((always_inline)) {
         const uint32_t keep = ((2 * kt + t) * 16 + ln < n) ? 0xffffffffu : 0u;
-        const uint2 lo2 = src[2 * t], hi2 = src[2 * t + 1];
-        return __builtin_bit_cast(
-            bf16x8, make_uint4(lo2.x & keep, lo2.y & keep, hi2.x & keep, hi2.y & keep));
+        const uint4 w = src[t];
+        return __builtin_bit_cast(bf16x8,
+                                  make_uint4(w.x & keep, w.y & keep, w.z & keep, w.w & keep));
       };
       auto transpose_pair = [&](bf16x8 f0, bf16x8 f1, u16* dst, int row_tile0, int kt)
           __attribute__((always_inline)) {
@@ -583,34 +594,43 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
           make_uint2(0u, 0u);
     }
     lds_barrier();
-    // the next chunk's tokens load while phases 4 and 5 compute
-    if (c0 + C < hi) prefetch(c0 + C);
 
     // ---- phase 4: W^T tiles -> fragments (gamma W, W hi, W lo); U ---------------------
-    // job (rt, kb): query-token tile rt, d_k tile pair kb; job j goes to wave j % 8
-#pragma unroll
-    for (int j = 0; j < 4 * KTD; ++j) {
-      if ((j & 7) != wave) continue;
-      const int rt = j / KTD, kb = j % KTD;
-      f32x4 w2[2];
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int dt = 2 * kb + half;
-        f32x4 acc = zero4();
+    // wave (rt, dg): query-token tile rt = wave % 4, d_k tiles 4*dg .. 4*dg + 3; the
+    // A1 diag(beta) fragments of tile rt are loaded once for all four products
+    {
+      constexpr int NG = DT / 4;  // groups of four d_k tiles
+      if (wave < 4 * NG) {
+        const int rt = wave & 3, dg = wave >> 2;
+        bf16x8 ah[KTC], al[KTC];
 #pragma unroll
         for (int kt = 0; kt < KTC; ++kt) {
-          const bf16x8 a = ld_frag(fKt, frag_slot(dt, kt, KTC, lane));
-          acc = mma(a, ld_frag(fAbh, frag_slot(rt, kt, KTC, lane)), acc);
-          acc = mma(a, ld_frag(fAbl, frag_slot(rt, kt, KTC, lane)), acc);
+          ah[kt] = ld_frag(fAbh, frag_slot(rt, kt, KTC, lane));
+          al[kt] = ld_frag(fAbl, frag_slot(rt, kt, KTC, lane));
         }
-        w2[half] = acc;
+        f32x4 w4[4];
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int kt = 0; kt < KTC; ++kt) {
+            const bf16x8 a = ld_frag(fKt, frag_slot(4 * dg + d, kt, KTC, lane));
+            acc = mma(a, ah[kt], acc);
+            acc = mma(a, al[kt], acc);
+          }
+          w4[d] = acc;
+        }
+        const float gam = ggam[rt * 16 + ln];
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const int kb = 2 * dg + p;
+          bf16x8 hh, ll;
+          pack_split(w4[2 * p], w4[2 * p + 1], hh, ll);
+          st_frag(fWh, frag_slot(rt, kb, KTD, lane), hh);
+          st_frag(fWl, frag_slot(rt, kb, KTD, lane), ll);
+          st_frag(fWs, frag_slot(rt, kb, KTD, lane), pack(w4[2 * p] * gam, w4[2 * p + 1] * gam));
+        }
       }
-      const float gam = ggam[rt * 16 + ln];
-      bf16x8 hh, ll;
-      pack_split(w2[0], w2[1], hh, ll);
-      st_frag(fWh, frag_slot(rt, kb, KTD, lane), hh);
-      st_frag(fWl, frag_slot(rt, kb, KTD, lane), ll);
-      st_frag(fWs, frag_slot(rt, kb, KTD, lane), pack(w2[0] * gam, w2[1] * gam));
     }
     f32x4 u[4];
     if (sw && wave_cols) {
@@ -625,6 +645,9 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       }
     }
     lds_barrier();
+
+    // the next chunk's tokens load while phase 5 computes
+    if (c0 + C < hi) prefetch(c0 + C);
 
     // ---- phase 5: chain update -----------------------------------------------------------
     if (sw && wave_cols) {
@@ -732,7 +755,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) so[(dt * 16 + 4 * g + i) * DV + col0 + ln] = st[dt][i];
+        for (int i = 0; i < 4; ++i) so[d_perm(dt, 4 * g + i) * DV + col0 + ln] = st[dt][i];
     }
     if (args.log_decay != nullptr && cb == 0 && tid == 0) args.log_decay[sh] = log_decay;
   } else {
@@ -740,7 +763,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) po[(dt * 16 + 4 * g + i) * DK + col0 + ln] = st[dt][i];
+      for (int i = 0; i < 4; ++i) po[d_perm(dt, 4 * g + i) * DK + col0 + ln] = st[dt][i];
   }
 }
 
