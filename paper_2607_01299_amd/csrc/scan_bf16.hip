@@ -135,6 +135,11 @@ __device__ __forceinline__ int d_perm(int dt, int m) {
   return 32 * (dt >> 1) + 8 * (m >> 2) + 4 * (dt & 1) + (m & 3);
 }
 
+// owner wave and register slot of K Q^T tile t (tiles 0-3: waves 0-3; tiles
+// 4-9: two each on waves 5-7)
+__device__ __forceinline__ int kq_owner(int t) { return (t < 4) ? t : 5 + (t - 4) % 3; }
+__device__ __forceinline__ int kq_slot(int t) { return (t < 4) ? 0 : 1 + (t - 4) / 3; }
+
 // lower-triangle tile t in 0..9 -> (row tile, column tile) with column <= row
 __device__ __forceinline__ int tri_row(int t) { return (t < 1) ? 0 : (t < 3) ? 1 : (t < 6) ? 2 : 3; }
 __device__ __forceinline__ int tri_col(int t) { return t - tri_row(t) * (tri_row(t) + 1) / 2; }
@@ -399,8 +404,8 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     // inverts all four blocks at once by unit-lower substitution, one lane per
     // column: the coefficient L[r][i] reaches every lane of row b by a DPP row
     // broadcast from lane i.  Off-diagonal Gram tiles (as L^T) go to waves 0-3,
-    // K Q^T tiles to waves 5-7.
-    f32x4 kq[4];
+    // K Q^T tile t to wave t for t < 4, else to waves 5-7.
+    f32x4 kq[3];
     f32x4 oq[4];
     float xd[16];  // wave 4, lane 16b + c: column c of the inverse diagonal block b
     if (wave == 4) {
@@ -458,7 +463,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     }
 #pragma unroll
     for (int t = 0; t < 10; ++t) {
-      if (5 + t % 3 != wave) continue;
+      if (kq_owner(t) != wave) continue;
       // rows: key tokens (tile ti), columns: query tokens (tile tr), ti <= tr
       const int tr = tri_row(t), ti = tri_col(t);
       f32x4 acc = zero4();
@@ -466,7 +471,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       for (int kb = 0; kb < KTD; ++kb)
         acc = mma(ld_frag(fKd, frag_slot(ti, kb, KTD, lane)),
                   ld_frag(fQ, frag_slot(tr, kb, KTD, lane)), acc);
-      kq[t / 3] = acc;
+      kq[kq_slot(t)] = acc;
     }
     if (sw && wave_cols) {
       // (Q S0)^T = S0^T Q^T: lane (g, n) holds four consecutive state columns of
@@ -483,7 +488,13 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
         oq[rt] = acc;
       }
     }
+    // The next chunk's tokens load while this chunk computes.  Issuing the loads
+    // costs the CU's load path ~1.5k cycles, so they are issued where the waves
+    // would otherwise wait: every wave but 4 (the inverse, the longest path of
+    // this phase) here, wave 4 after the barrier.
+    if (wave != 4 && c0 + C < hi) prefetch(c0 + C);
     lds_barrier();
+    if (wave == 4 && c0 + C < hi) prefetch(c0 + C);
 
     // ---- phase 2: the rest of A1 -------------------------------------------------------
     // (a) the diagonal blocks move from their staging copy into A1 and A1^T
@@ -571,11 +582,11 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     // (Q K^T . Gamma) as A-operand fragments over key tokens for query rows
 #pragma unroll
     for (int t = 0; t < 10; ++t) {
-      if (5 + t % 3 != wave) continue;
+      if (kq_owner(t) != wave) continue;
       const int tr = tri_row(t), ti = tri_col(t);
       const int r = tr * 16 + ln;
       const float br = gb[r];
-      const f32x4 a = kq[t / 3];
+      const f32x4 a = kq[kq_slot(t)];
       u16x4 val;
 #pragma unroll
       for (int i4 = 0; i4 < 4; ++i4) {
@@ -645,9 +656,6 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       }
     }
     lds_barrier();
-
-    // the next chunk's tokens load while phase 5 computes
-    if (c0 + C < hi) prefetch(c0 + C);
 
     // ---- phase 5: chain update -----------------------------------------------------------
     if (sw && wave_cols) {
