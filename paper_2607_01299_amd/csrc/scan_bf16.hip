@@ -145,21 +145,28 @@ __device__ __forceinline__ int tri_row(int t) { return (t < 1) ? 0 : (t < 3) ? 1
 __device__ __forceinline__ int tri_col(int t) { return t - tri_row(t) * (tri_row(t) + 1) / 2; }
 
 // ---- LDS plan (bytes); regions are reused across the phases of a chunk ------
+// Phase 0 of chunk c + 1 runs in the same barrier interval as the chain update
+// of chunk c, so everything that update reads and phase 0 writes is kept
+// apart: K over tokens and the gates are double-buffered, W hi and the
+// (Q K^T . Gamma) fragments have regions of their own.
 template <int DK>
 struct Lds {
   static constexpr int FK = C * DK * 2;     // bytes of a 64 x DK bf16 fragment matrix
   static constexpr int F32M = C * LDC * 4;  // padded 64 x 64 float32 matrix
   static constexpr int RA = (FK > F32M) ? FK : F32M;
-  static constexpr int O_KD = 0;            // K over d -> A1 (f32) -> W hi
-  static constexpr int O_Q = O_KD + RA;     // Q over d -> A1^T -> (QK . Gamma), (A1 . Gamma) beta
-  static constexpr int O_KT = O_Q + RA;     // K over tokens
-  static constexpr int O_L = O_KT + FK;     // L^T (f32) + N blocks -> A1 beta hi / lo
+  static constexpr int GATES = 4 * C * 4;
+  static constexpr int O_KD = 0;            // K over d -> A1 (f32)
+  static constexpr int O_Q = O_KD + RA;     // Q over d -> A1^T -> (A1 . Gamma) beta
+  static constexpr int O_KT = O_Q + RA;     // K over tokens, two buffers
+  static constexpr int O_L = O_KT + 2 * FK;  // L^T (f32) + N blocks -> A1 beta hi / lo
   static constexpr int O_WS = O_L + F32M;   // gamma W (state path)
-  static constexpr int O_WL = O_WS + FK;           // W lo (operator path)
-  static constexpr int O_G = O_WL + FK;            // gates
-  static constexpr int TOTAL = O_G + 4 * C * 4;
+  static constexpr int O_WL = O_WS + FK;    // staged A1 diagonal blocks -> W lo (operator path)
+  static constexpr int O_WH = O_WL + FK;    // W hi (operator path)
+  static constexpr int O_QK = O_WH + FK;    // (Q K^T . Gamma)
+  static constexpr int O_G = O_QK + C * C * 2;  // gates, two buffers
+  static constexpr int TOTAL = O_G + 2 * GATES;
   static_assert(2 * C * C * 2 <= F32M, "A1 beta hi + lo fit the L region");
-  static_assert(2 * C * C * 2 <= RA, "QK and (A1 . Gamma) beta fit the Q region");
+  static_assert(C * C * 2 <= RA, "(A1 . Gamma) beta fits the Q region");
   static_assert(C * LDD * 4 <= FK, "staged diagonal blocks fit the W lo region");
   static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
@@ -175,22 +182,22 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   extern __shared__ __align__(16) unsigned char smem[];
   u16* fKd = reinterpret_cast<u16*>(smem + LP::O_KD);
   float* A1 = reinterpret_cast<float*>(smem + LP::O_KD);
-  u16* fWh = reinterpret_cast<u16*>(smem + LP::O_KD);
   u16* fQ = reinterpret_cast<u16*>(smem + LP::O_Q);
   float* A1t = reinterpret_cast<float*>(smem + LP::O_Q);
-  u16* fQK = reinterpret_cast<u16*>(smem + LP::O_Q);
-  u16* fAgb = fQK + C * C;
-  u16* fKt = reinterpret_cast<u16*>(smem + LP::O_KT);
+  u16* fAgb = reinterpret_cast<u16*>(smem + LP::O_Q);
   float* Lt = reinterpret_cast<float*>(smem + LP::O_L);
   u16* fAbh = reinterpret_cast<u16*>(smem + LP::O_L);
   u16* fAbl = fAbh + C * C;
   u16* fWs = reinterpret_cast<u16*>(smem + LP::O_WS);
   u16* fWl = reinterpret_cast<u16*>(smem + LP::O_WL);
-  float* gb = reinterpret_cast<float*>(smem + LP::O_G);
-  float* gbeta = gb + C;
-  float* ggam = gb + 2 * C;
-  float* gdec = gb + 3 * C;
+  u16* fWh = reinterpret_cast<u16*>(smem + LP::O_WH);
+  u16* fQK = reinterpret_cast<u16*>(smem + LP::O_QK);
   float* Dg = reinterpret_cast<float*>(smem + LP::O_WL);  // diagonal blocks of A1 (phase 1-2)
+  // buffer set par of the double-buffered regions
+  auto kt_buf = [&](int par) { return reinterpret_cast<u16*>(smem + LP::O_KT + par * LP::FK); };
+  auto gate_buf = [&](int par) {
+    return reinterpret_cast<float*>(smem + LP::O_G + par * LP::GATES);
+  };
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
@@ -309,7 +316,94 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     }
   };
 
-  if (lo < hi) prefetch(lo);
+  // ---- phase 0 of the chunk at c0n into buffer set par: fragments -> LDS
+  //      (lane-contiguous); transposed copies of K and V by exact identity
+  //      products on the matrix cores; gates -------------------------------------
+  auto phase0 = [&](int c0n, int par, int lane, int g, int ln) __attribute__((always_inline)) {
+    const int n = (hi - c0n < C) ? (hi - c0n) : C;
+    u16* fKt = kt_buf(par);
+    float* gb = gate_buf(par);
+    float* gbeta = gb + C;
+    float* ggam = gb + 2 * C;
+    float* gdec = gb + 3 * C;
+  {
+    // selector B operands: slot (g', j') of lane (g', n) holds column
+    // 8g' + j' of the loaded 32-column block, so eye[half] = 1 exactly where
+    // 8g' + j' = d_perm(half, n) and (X eye[half])[m][n] = X[m][d_perm(half, n)]
+    bf16x8 eye[2];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      eye[0][j] = static_cast<__bf16>((g == (ln >> 2) && j == (ln & 3)) ? 1.f : 0.f);
+      eye[1][j] = static_cast<__bf16>((g == (ln >> 2) && j == 4 + (ln & 3)) ? 1.f : 0.f);
+    }
+    // fragment t of a prefetched pair, with tokens past the chunk's end zeroed
+    auto take = [&](const uint4 (&src)[2], int kt, int t) __attribute__((always_inline)) {
+      const uint32_t keep = ((2 * kt + t) * 16 + ln < n) ? 0xffffffffu : 0u;
+      const uint4 w = src[t];
+      return __builtin_bit_cast(bf16x8,
+                                make_uint4(w.x & keep, w.y & keep, w.z & keep, w.w & keep));
+    };
+    auto transpose_pair = [&](bf16x8 f0, bf16x8 f1, u16* dst, int row_tile0, int kt)
+        __attribute__((always_inline)) {
+      // f0, f1: A fragments of token tiles 2kt, 2kt+1 over a 32-column block
+      // whose two 16-column halves become row tiles row_tile0 and row_tile0 + 1
+      // of the token-contraction fragments
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const f32x4 c_lo = mma(f0, eye[half], zero4());
+        const f32x4 c_hi = mma(f1, eye[half], zero4());
+        st_frag(dst, frag_slot(row_tile0 + half, kt, KTC, lane), pack(c_lo, c_hi));
+      }
+    };
+    if (k_job) {
+      const bf16x8 f0 = take(pk, kjt, 0), f1 = take(pk, kjt, 1);
+      st_frag(fKd, frag_slot(2 * kjt, kjb, KTD, lane), f0);
+      st_frag(fKd, frag_slot(2 * kjt + 1, kjb, KTD, lane), f1);
+      transpose_pair(f0, f1, fKt, 2 * kjb, kjt);
+    }
+    if (q_job) {
+      st_frag(fQ, frag_slot(2 * qjt, qjb, KTD, lane), take(pq, qjt, 0));
+      st_frag(fQ, frag_slot(2 * qjt + 1, qjb, KTD, lane), take(pq, qjt, 1));
+    }
+    if (v_job) {
+      // this wave's V columns as token-contraction B fragments, by exact
+      // 16x16x16 identity products: (V_tt I)[m][n] lands in lane (g, n) as
+      // rows 4g .. 4g+3, i.e. tokens along the contraction
+      s16x4 eye16;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) eye16[j] = (4 * g + j == ln) ? short(0x3F80) : short(0);
+      f32x4 vt[4];
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) {
+        const uint32_t keep = (tt * 16 + ln < n) ? 0xffffffffu : 0u;
+        const uint2 w2 = make_uint2(pv[tt].x & keep, pv[tt].y & keep);
+        vt[tt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, w2),
+                                                           eye16, zero4(), 0, 0, 0);
+      }
+      vB[0] = pack(vt[0], vt[1]);
+      vB[1] = pack(vt[2], vt[3]);
+    }
+  }
+  if (wave == 0) {
+    float b = (lane < n) ? pa : 0.f;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const float u = __shfl_up(b, off, 64);
+      if (lane >= off) b += u;
+    }
+    const float b_last = __shfl(b, 63, 64);
+    gb[lane] = b;
+    gbeta[lane] = (lane < n) ? pbeta : 0.f;
+    ggam[lane] = __expf(b);
+    gdec[lane] = __expf(b_last - b);
+  }
+  };
+
+  if (lo < hi) {
+    prefetch(lo);
+    phase0(lo, 0, lane0, g0, ln0);
+    lds_barrier();
+  }
 
   for (int c0 = lo; c0 < hi; c0 += C) {
     const int n = (hi - c0 < C) ? (hi - c0) : C;
@@ -320,81 +414,13 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     asm volatile("" : "+v"(tid));
     const int lane = tid & 63;
     const int g = lane >> 4, ln = lane & 15;
+    const int par = ((c0 - lo) / C) & 1;  // buffer set of this chunk
+    const u16* fKt = kt_buf(par);
+    const float* gb = gate_buf(par);
+    const float* gbeta = gb + C;
+    const float* ggam = gb + 2 * C;
+    const float* gdec = gb + 3 * C;
 
-    // ---- phase 0: fragments -> LDS (lane-contiguous); transposed copies of K and
-    //      V by an exact identity product on the matrix cores; gates ----------------
-    {
-      // selector B operands: slot (g', j') of lane (g', n) holds column
-      // 8g' + j' of the loaded 32-column block, so eye[half] = 1 exactly where
-      // 8g' + j' = d_perm(half, n) and (X eye[half])[m][n] = X[m][d_perm(half, n)]
-      bf16x8 eye[2];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        eye[0][j] = static_cast<__bf16>((g == (ln >> 2) && j == (ln & 3)) ? 1.f : 0.f);
-        eye[1][j] = static_cast<__bf16>((g == (ln >> 2) && j == 4 + (ln & 3)) ? 1.f : 0.f);
-      }
-      // fragment t of a prefetched pair, with tokens past the chunk's end zeroed
-      auto take = [&](const uint4 (&src)[2], int kt, int t) __attribute__((always_inline)) {
-        const uint32_t keep = ((2 * kt + t) * 16 + ln < n) ? 0xffffffffu : 0u;
-        const uint4 w = src[t];
-        return __builtin_bit_cast(bf16x8,
-                                  make_uint4(w.x & keep, w.y & keep, w.z & keep, w.w & keep));
-      };
-      auto transpose_pair = [&](bf16x8 f0, bf16x8 f1, u16* dst, int row_tile0, int kt)
-          __attribute__((always_inline)) {
-        // f0, f1: A fragments of token tiles 2kt, 2kt+1 over a 32-column block
-        // whose two 16-column halves become row tiles row_tile0 and row_tile0 + 1
-        // of the token-contraction fragments
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const f32x4 c_lo = mma(f0, eye[half], zero4());
-          const f32x4 c_hi = mma(f1, eye[half], zero4());
-          st_frag(dst, frag_slot(row_tile0 + half, kt, KTC, lane), pack(c_lo, c_hi));
-        }
-      };
-      if (k_job) {
-        const bf16x8 f0 = take(pk, kjt, 0), f1 = take(pk, kjt, 1);
-        st_frag(fKd, frag_slot(2 * kjt, kjb, KTD, lane), f0);
-        st_frag(fKd, frag_slot(2 * kjt + 1, kjb, KTD, lane), f1);
-        transpose_pair(f0, f1, fKt, 2 * kjb, kjt);
-      }
-      if (q_job) {
-        st_frag(fQ, frag_slot(2 * qjt, qjb, KTD, lane), take(pq, qjt, 0));
-        st_frag(fQ, frag_slot(2 * qjt + 1, qjb, KTD, lane), take(pq, qjt, 1));
-      }
-      if (v_job) {
-        // this wave's V columns as token-contraction B fragments, by exact
-        // 16x16x16 identity products: (V_tt I)[m][n] lands in lane (g, n) as
-        // rows 4g .. 4g+3, i.e. tokens along the contraction
-        s16x4 eye16;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) eye16[j] = (4 * g + j == ln) ? short(0x3F80) : short(0);
-        f32x4 vt[4];
-#pragma unroll
-        for (int tt = 0; tt < 4; ++tt) {
-          const uint32_t keep = (tt * 16 + ln < n) ? 0xffffffffu : 0u;
-          const uint2 w2 = make_uint2(pv[tt].x & keep, pv[tt].y & keep);
-          vt[tt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, w2),
-                                                             eye16, zero4(), 0, 0, 0);
-        }
-        vB[0] = pack(vt[0], vt[1]);
-        vB[1] = pack(vt[2], vt[3]);
-      }
-    }
-    if (wave == 0) {
-      float b = (lane < n) ? pa : 0.f;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const float u = __shfl_up(b, off, 64);
-        if (lane >= off) b += u;
-      }
-      const float b_last = __shfl(b, 63, 64);
-      gb[lane] = b;
-      gbeta[lane] = (lane < n) ? pbeta : 0.f;
-      ggam[lane] = __expf(b);
-      gdec[lane] = __expf(b_last - b);
-    }
-    lds_barrier();
     const float b_last = gb[C - 1];
     log_decay += b_last;
 
@@ -752,6 +778,8 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
         st[dt] = acc;
       }
     }
+    // phase 0 of the next chunk shares this interval with the update above
+    if (c0 + C < hi) phase0(c0 + C, par ^ 1, lane, g, ln);
     lds_barrier();
   }
 
