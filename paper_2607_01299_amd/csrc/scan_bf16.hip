@@ -135,14 +135,15 @@ __device__ __forceinline__ int d_perm(int dt, int m) {
   return 32 * (dt >> 1) + 8 * (m >> 2) + 4 * (dt & 1) + (m & 3);
 }
 
-// owner wave and register slot of K Q^T tile t (tiles 0-3: waves 0-3; tiles
-// 4-9: two each on waves 5-7)
-__device__ __forceinline__ int kq_owner(int t) { return (t < 4) ? t : 5 + (t - 4) % 3; }
-__device__ __forceinline__ int kq_slot(int t) { return (t < 4) ? 0 : 1 + (t - 4) / 3; }
-
 // lower-triangle tile t in 0..9 -> (row tile, column tile) with column <= row
 __device__ __forceinline__ int tri_row(int t) { return (t < 1) ? 0 : (t < 3) ? 1 : (t < 6) ? 2 : 3; }
 __device__ __forceinline__ int tri_col(int t) { return t - tri_row(t) * (tri_row(t) + 1) / 2; }
+
+// owner wave and register slot of K Q^T tile t (query tile tri_row(t), key tile
+// tri_col(t)): wave w holds the tiles of key tile w in slot (query - key); the
+// tile (query 3, key 0) goes to wave 3, slot 1
+__device__ __forceinline__ int kq_owner(int t) { return (t == 6) ? 3 : tri_col(t); }
+__device__ __forceinline__ int kq_slot(int t) { return (t == 6) ? 1 : tri_row(t) - tri_col(t); }
 
 // ---- LDS plan (bytes); regions are reused across the phases of a chunk ------
 // Phase 0 of chunk c + 1 runs in the same barrier interval as the chain update
@@ -429,8 +430,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     // blocks of the L^T storage, reads column c of L_bb back into lane 16b + c and
     // inverts all four blocks at once by unit-lower substitution, one lane per
     // column: the coefficient L[r][i] reaches every lane of row b by a DPP row
-    // broadcast from lane i.  Off-diagonal Gram tiles (as L^T) go to waves 0-3,
-    // K Q^T tile t to wave t for t < 4, else to waves 5-7.
+    // broadcast from lane i.
     f32x4 kq[3];
     f32x4 oq[4];
     float xd[16];  // wave 4, lane 16b + c: column c of the inverse diagonal block b
@@ -470,57 +470,76 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) Dg[(ob + r) * LDD + ln] = xd[r];
     }
-    // off-diagonal Gram tiles (1,0) (2,0) (2,1) (3,0) (3,1) (3,2)
+    // off-diagonal Gram tiles (1,0) (2,0) (2,1) (3,0) (3,1) (3,2), all on wave 5,
+    // which loads each K fragment once
+    if (wave == 5) {
+      f32x4 go[6];
 #pragma unroll
-    for (int j = 0; j < 6; ++j) {
-      if ((j & 3) != wave) continue;
-      const int ti = (j < 1) ? 1 : (j < 3) ? 2 : 3;
-      const int tj = (j < 1) ? 0 : (j < 3) ? j - 1 : j - 3;
-      f32x4 acc = zero4();
+      for (int j = 0; j < 6; ++j) go[j] = zero4();
 #pragma unroll
-      for (int kb = 0; kb < KTD; ++kb)
-        acc = mma(ld_frag(fKd, frag_slot(ti, kb, KTD, lane)),
-                  ld_frag(fKd, frag_slot(tj, kb, KTD, lane)), acc);
-      // L^T[c][r] = beta_r G[r][c]  (c < r throughout an off-diagonal tile)
-      const int c = tj * 16 + ln;
-      const float4 bb = *reinterpret_cast<const float4*>(gbeta + ti * 16 + 4 * g);
-      *reinterpret_cast<float4*>(Lt + c * LDC + ti * 16 + 4 * g) =
-          make_float4(bb.x * acc[0], bb.y * acc[1], bb.z * acc[2], bb.w * acc[3]);
+      for (int kb = 0; kb < KTD; ++kb) {
+        bf16x8 kf[4];
+#pragma unroll
+        for (int t4 = 0; t4 < 4; ++t4) kf[t4] = ld_frag(fKd, frag_slot(t4, kb, KTD, lane));
+#pragma unroll
+        for (int j = 0; j < 6; ++j) {
+          const int ti = (j < 1) ? 1 : (j < 3) ? 2 : 3;
+          const int tj = (j < 1) ? 0 : (j < 3) ? j - 1 : j - 3;
+          go[j] = mma(kf[ti], kf[tj], go[j]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 6; ++j) {
+        const int ti = (j < 1) ? 1 : (j < 3) ? 2 : 3;
+        const int tj = (j < 1) ? 0 : (j < 3) ? j - 1 : j - 3;
+        // L^T[c][r] = beta_r G[r][c]  (c < r throughout an off-diagonal tile)
+        const int c = tj * 16 + ln;
+        const float4 bb = *reinterpret_cast<const float4*>(gbeta + ti * 16 + 4 * g);
+        *reinterpret_cast<float4*>(Lt + c * LDC + ti * 16 + 4 * g) =
+            make_float4(bb.x * go[j][0], bb.y * go[j][1], bb.z * go[j][2], bb.w * go[j][3]);
+      }
     }
-#pragma unroll
-    for (int t = 0; t < 10; ++t) {
-      if (kq_owner(t) != wave) continue;
-      // rows: key tokens (tile ti), columns: query tokens (tile tr), ti <= tr
-      const int tr = tri_row(t), ti = tri_col(t);
-      f32x4 acc = zero4();
-#pragma unroll
-      for (int kb = 0; kb < KTD; ++kb)
-        acc = mma(ld_frag(fKd, frag_slot(ti, kb, KTD, lane)),
-                  ld_frag(fQ, frag_slot(tr, kb, KTD, lane)), acc);
-      kq[kq_slot(t)] = acc;
-    }
-    if (sw && wave_cols) {
-      // (Q S0)^T = S0^T Q^T: lane (g, n) holds four consecutive state columns of
-      // query token n
+    // (Q S0)^T = S0^T Q^T on every state wave (lane (g, n) holds four consecutive
+    // state columns of query token n).  Waves 0-3 also form the K Q^T tiles from
+    // the same Q fragments: wave w the tiles of key tile w, wave 3 also (0, 3).
+    {
+      const bool do_oq = sw && wave_cols;
       bf16x8 s0h[KTD];
 #pragma unroll
       for (int kb = 0; kb < KTD; ++kb) s0h[kb] = pack(st[2 * kb], st[2 * kb + 1]);
 #pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        f32x4 acc = zero4();
+      for (int rt = 0; rt < 4; ++rt) oq[rt] = zero4();
 #pragma unroll
-        for (int kb = 0; kb < KTD; ++kb)
-          acc = mma(s0h[kb], ld_frag(fQ, frag_slot(rt, kb, KTD, lane)), acc);
-        oq[rt] = acc;
+      for (int sl = 0; sl < 3; ++sl) kq[sl] = zero4();
+#pragma unroll
+      for (int w = 0; w < 5; ++w) {
+        // w < 4: wave w; w == 4: any other state wave
+        if ((w < 4) ? (w != wave) : (wave < 4 || !do_oq)) continue;
+#pragma unroll
+        for (int kb = 0; kb < KTD; ++kb) {
+          bf16x8 qf[4];
+#pragma unroll
+          for (int rt = 0; rt < 4; ++rt) qf[rt] = ld_frag(fQ, frag_slot(rt, kb, KTD, lane));
+          if (do_oq) {
+#pragma unroll
+            for (int rt = 0; rt < 4; ++rt) oq[rt] = mma(s0h[kb], qf[rt], oq[rt]);
+          }
+          if (w < 4) {
+            const bf16x8 ka = ld_frag(fKd, frag_slot(w, kb, KTD, lane));
+#pragma unroll
+            for (int sl = 0; sl < 3; ++sl)
+              if (w + sl < 4) kq[sl] = mma(ka, qf[w + sl], kq[sl]);
+            if (w == 3) kq[1] = mma(ld_frag(fKd, frag_slot(0, kb, KTD, lane)), qf[3], kq[1]);
+          }
+        }
       }
     }
     // The next chunk's tokens load while this chunk computes.  Issuing the loads
-    // costs the CU's load path ~1.5k cycles, so they are issued where the waves
-    // would otherwise wait: every wave but 4 (the inverse, the longest path of
-    // this phase) here, wave 4 after the barrier.
-    if (wave != 4 && c0 + C < hi) prefetch(c0 + C);
+    // keeps the CU's load path busy for ~1.5k cycles, so they are issued where
+    // the waves would otherwise wait: waves 0-2 here, waves 3-7 (idle while
+    // the off-diagonal blocks of A1 are merged) once the merges begin.
+    if (wave < 3 && c0 + C < hi) prefetch(c0 + C);
     lds_barrier();
-    if (wave == 4 && c0 + C < hi) prefetch(c0 + C);
 
     // ---- phase 2: the rest of A1 -------------------------------------------------------
     // (a) the diagonal blocks move from their staging copy into A1 and A1^T
@@ -549,6 +568,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     }
     lds_barrier();
     // (c)-(e) A_ij = -sum_{k=j}^{i-1} N_ik A_kj, one block diagonal at a time
+    if (wave >= 3 && c0 + C < hi) prefetch(c0 + C);
 #pragma unroll
     for (int dist = 1; dist < 4; ++dist) {
 #pragma unroll
