@@ -426,43 +426,59 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     log_decay += b_last;
 
     // ---- phase 1: Gram tiles; diagonal blocks of A1 = (I + L)^{-1}; K Q^T; (Q S0)^T --
-    // Wave 4 forms the four diagonal Gram tiles, parks L_bb^T in the diagonal
-    // blocks of the L^T storage, reads column c of L_bb back into lane 16b + c and
-    // inverts all four blocks at once by unit-lower substitution, one lane per
-    // column: the coefficient L[r][i] reaches every lane of row b by a DPP row
-    // broadcast from lane i.
+    // Wave 4 forms the four diagonal Gram tiles, gathers column c of G_bb into
+    // lane 16b + c by cross-row lane swaps (no LDS round trip) and inverts all
+    // four blocks at once by unit-lower substitution, one lane per column: the
+    // coefficient L[r][i] reaches every lane of row b by a DPP row broadcast
+    // from lane i.
     f32x4 kq[3];
     f32x4 oq[4];
     float xd[16];  // wave 4, lane 16b + c: column c of the inverse diagonal block b
     if (wave == 4) {
+      f32x4 gd[4];  // diagonal Gram tiles; lane (g, n) of tile b holds G_b[4g + i][n]
 #pragma unroll
       for (int bd = 0; bd < 4; ++bd) {
-        f32x4 acc = zero4();
+        gd[bd] = zero4();
 #pragma unroll
         for (int kb = 0; kb < KTD; ++kb) {
           const bf16x8 f = ld_frag(fKd, frag_slot(bd, kb, KTD, lane));
-          acc = mma(f, f, acc);
+          gd[bd] = mma(f, f, gd[bd]);
         }
-        // lane (g, n) holds G[r][n], r = 4g + s; -L^T[n][r] = -beta_r G[r][n] for n < r
-        const float4 bb = *reinterpret_cast<const float4*>(gbeta + bd * 16 + 4 * g);
-        const float bv[4] = {bb.x, bb.y, bb.z, bb.w};
-        float4 o4;
-        float* o = reinterpret_cast<float*>(&o4);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o[i] = (ln < 4 * g + i) ? -bv[i] * acc[i] : 0.f;
-        *reinterpret_cast<float4*>(Lt + (bd * 16 + ln) * LDC + bd * 16 + 4 * g) = o4;
       }
-      // LDS operations of one wave complete in issue order: no barrier needed
+      // exchange (tile b, lane row g) <-> (tile g, lane row b) with two rounds of
+      // row swaps: afterwards lane 16b + c of tile g holds G_b[4g + i][c], so
+      // lane 16b + c has all of column c of G_b
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int b2 = 0; b2 < 2; ++b2) {  // upper half of tile b2 <-> lower half of b2 + 2
+          const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(gd[b2][i]),
+                                                          __float_as_uint(gd[b2 + 2][i]), false,
+                                                          false);
+          // the two results are copied out one by one before any bit cast
+          const unsigned r0 = r[0], r1 = r[1];
+          gd[b2][i] = __uint_as_float(r0);
+          gd[b2 + 2][i] = __uint_as_float(r1);
+        }
+#pragma unroll
+        for (int b2 = 0; b2 < 4; b2 += 2) {  // odd rows of tile b2 <-> even rows of b2 + 1
+          const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(gd[b2][i]),
+                                                          __float_as_uint(gd[b2 + 1][i]), false,
+                                                          false);
+          const unsigned r0 = r[0], r1 = r[1];
+          gd[b2][i] = __uint_as_float(r0);
+          gd[b2 + 1][i] = __uint_as_float(r1);
+        }
+      }
       const int ob = (lane >> 4) * 16;
-      float lcol[16];  // -L[r][ln] of block lane / 16
-      const float4* colp = reinterpret_cast<const float4*>(Lt + (ob + ln) * LDC + ob);
+      float lcol[16];  // -L[r][ln] = -beta_r G[r][ln] of block lane / 16 (used for r > ln)
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4) {
-        const float4 t4 = colp[q4];
-        lcol[4 * q4] = t4.x;
-        lcol[4 * q4 + 1] = t4.y;
-        lcol[4 * q4 + 2] = t4.z;
-        lcol[4 * q4 + 3] = t4.w;
+        const float4 bb = *reinterpret_cast<const float4*>(gbeta + ob + 4 * q4);
+        lcol[4 * q4] = -bb.x * gd[q4][0];
+        lcol[4 * q4 + 1] = -bb.y * gd[q4][1];
+        lcol[4 * q4 + 2] = -bb.z * gd[q4][2];
+        lcol[4 * q4 + 3] = -bb.w * gd[q4][3];
       }
 #pragma unroll
       for (int r = 0; r < 16; ++r) xd[r] = (r == ln) ? 1.f : 0.f;
