@@ -435,6 +435,9 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     f32x4 oq[4];
     float xd[16];  // wave 4, lane 16b + c: column c of the inverse diagonal block b
     if (wave == 4) {
+      // the inverse is this phase's longest path: its instructions win issue
+      // arbitration until it is done
+      __builtin_amdgcn_s_setprio(2);
       f32x4 gd[4];  // diagonal Gram tiles; lane (g, n) of tile b holds G_b[4g + i][n]
 #pragma unroll
       for (int bd = 0; bd < 4; ++bd) {
@@ -485,6 +488,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       unit_lower_solve_step<0>(xd, lcol);
 #pragma unroll
       for (int r = 0; r < 16; ++r) Dg[(ob + r) * LDD + ln] = xd[r];
+      __builtin_amdgcn_s_setprio(0);
     }
     // off-diagonal Gram tiles (1,0) (2,0) (2,1) (3,0) (3,1) (3,2), all on wave 5,
     // which loads each K fragment once
