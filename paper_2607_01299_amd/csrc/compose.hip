@@ -1,14 +1,19 @@
 // Segment composition, Eq. (6), for gfx950.
 //
 // One workgroup of d_k / 16 waves per (request, v-head).  The running state S
-// (d_k x d_v, float32) stays on chip for the whole request: each wave owns a
-// band of 16 rows as matrix-core accumulators, and a transposed copy of the
-// full state sits in LDS as the shared B operand.  Per listed segment i
-// every wave streams its rows of P_hat_i and S_seg_i straight from HBM into
-// registers (each byte of the pool tuple is read once) and computes
-//     S[band] <- exp(log_decay_i) * (P_hat_i[band, :] @ S) + S_seg_i[band]
+// (d_k x d_v, float32) stays on chip for the whole request.  Per listed segment
+// i every wave updates its band of 16 state rows,
+//     S[band] <- exp(log_decay_i) * (P_hat_i[band, :] @ S) + S_seg_i[band],
 // which is the two-segment true splice of Eq. (4) applied in list order.
-// The state entering each segment is optionally written out for the seam.
+//
+// The product is formed transposed, S^T P_hat^T, so that the accumulator
+// layout gives each lane four consecutive columns of one state row: every
+// access to HBM (P_hat rows, S_seg, the optional prefix, S_incoming, S_out)
+// is then a 16-byte load or store per lane, 64 contiguous bytes per row per
+// instruction.  The A operand (S^T) is read from a column-major copy of the
+// state in LDS; the B operand (P_hat^T) is P_hat's own rows.  Each byte of the
+// pool tuple is read once.  The tuple of step j + 1 is loaded into registers
+// while step j computes.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -22,123 +27,103 @@ namespace {
 
 template <int DK, int DV, int P>
 __global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
-  constexpr int RW = 16;           // rows per wave
-  constexpr int MT = 1;
-  constexpr int NT = DV / 16;
-  constexpr int LDT = DK + 4;      // transposed state row stride (floats)
-  __shared__ float st_t[DV * LDT];  // st_t[n * LDT + k] = S[k][n]
+  constexpr int KB = DK / 32;     // 32-wide contraction blocks
+  constexpr int NT = DV / 16;     // 16-column tiles of the state
+  constexpr int LDT = DK + 4;     // column stride (floats) of the LDS copy
+  __shared__ float st_t[DV * LDT];  // st_t[c * LDT + d] = S[d][c]
 
   const int tid = threadIdx.x;
   const int wave = tid / 64, lane = tid % 64;
   const int g = lane / 16, ln = lane % 16;
   const int req = blockIdx.x / args.h_v;
   const int h = blockIdx.x % args.h_v;
-  const int row0 = wave * RW;
+  const int row = wave * 16 + ln;  // this lane's state row
   const long state_sz = static_cast<long>(DK) * DV;
+  const long hs = static_cast<long>(req) * args.h_v + h;
 
-  f32x4 s[MT][NT];
-  const float* pre = args.S_prefix ? args.S_prefix + (static_cast<long>(req) * args.h_v + h) * state_sz
-                                   : nullptr;
+  // s[mt][i] = S[row][16 mt + 4 g + i]
+  f32x4 s[NT];
+  if (args.S_prefix != nullptr) {
+    const float* pre = args.S_prefix + hs * state_sz + static_cast<long>(row) * DV + 4 * g;
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < NT; ++mt) s[mt] = *reinterpret_cast<const f32x4*>(pre + 16 * mt);
+  } else {
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        s[mt][nt][i] = pre ? pre[(row0 + mt * 16 + 4 * g + i) * DV + nt * 16 + ln] : 0.f;
+    for (int mt = 0; mt < NT; ++mt) s[mt] = zero4();
+  }
 
   auto publish = [&]() {
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < NT; ++mt)
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-        *reinterpret_cast<f32x4*>(&st_t[(nt * 16 + ln) * LDT + row0 + mt * 16 + 4 * g]) =
-            s[mt][nt];
+      for (int i = 0; i < 4; ++i) st_t[(16 * mt + 4 * g + i) * LDT + row] = s[mt][i];
   };
   publish();
   __syncthreads();
 
-  // The pool tuple of step j + 1 is loaded into registers while step j
-  // computes (software pipelining), so the HBM latency hides behind the
-  // matrix-core work and the barriers.
+  // pool tuple of one step: this lane's row of P_hat as B fragments (k slots
+  // kap(g, .) of each 32-block) and its four S_seg columns per tile
   const int j0 = args.req_offsets[req], j1 = args.req_offsets[req + 1];
-  float nP[MT][DK / 32][8];
-  f32x4 nS[MT][NT];
+  float nP[KB][8];
+  f32x4 nS[NT];
   float nE = 0.f;
   auto load_step = [&](int j) __attribute__((always_inline)) {
     const long sh = static_cast<long>(args.seg_ids[j]) * args.h_v + h;
-    const float* Pi = args.P_hat + sh * DK * DK;
-    const float* Si = args.S_seg + sh * state_sz;
+    const float* Pi = args.P_hat + sh * DK * DK + static_cast<long>(row) * DK + 4 * g;
+    const float* Si = args.S_seg + sh * state_sz + static_cast<long>(row) * DV + 4 * g;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int kb = 0; kb < KB; ++kb) {
+      const float4 lo = *reinterpret_cast<const float4*>(Pi + 32 * kb);
+      const float4 hi = *reinterpret_cast<const float4*>(Pi + 32 * kb + 16);
+      nP[kb][0] = lo.x; nP[kb][1] = lo.y; nP[kb][2] = lo.z; nP[kb][3] = lo.w;
+      nP[kb][4] = hi.x; nP[kb][5] = hi.y; nP[kb][6] = hi.z; nP[kb][7] = hi.w;
+    }
 #pragma unroll
-      for (int kb = 0; kb < DK / 32; ++kb) frag_kcontig(Pi, DK, row0 + mt * 16 + ln, kb * 32, g, nP[mt][kb]);
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          nS[mt][nt][i] = Si[(row0 + mt * 16 + 4 * g + i) * DV + nt * 16 + ln];
+    for (int mt = 0; mt < NT; ++mt) nS[mt] = *reinterpret_cast<const f32x4*>(Si + 16 * mt);
     nE = __expf(args.log_decay[sh]);
   };
   if (j0 < j1) load_step(j0);
   for (int j = j0; j < j1; ++j) {
-    float cP[MT][DK / 32][8];
-    f32x4 cS[MT][NT];
+    float cP[KB][8];
+    f32x4 cS[NT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
+    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-      for (int kb = 0; kb < DK / 32; ++kb)
+      for (int e = 0; e < 8; ++e) cP[kb][e] = nP[kb][e];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) cP[mt][kb][e] = nP[mt][kb][e];
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) cS[mt][nt] = nS[mt][nt];
-    }
+    for (int mt = 0; mt < NT; ++mt) cS[mt] = nS[mt];
     const float e = nE;
     if (j + 1 < j1) load_step(j + 1);
     if (args.S_incoming != nullptr) {
-      float* dst = args.S_incoming + (static_cast<long>(j) * args.h_v + h) * state_sz;
+      float* dst = args.S_incoming + (static_cast<long>(j) * args.h_v + h) * state_sz +
+                   static_cast<long>(row) * DV + 4 * g;
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            dst[(row0 + mt * 16 + 4 * g + i) * DV + nt * 16 + ln] = s[mt][nt][i];
+      for (int mt = 0; mt < NT; ++mt) *reinterpret_cast<f32x4*>(dst + 16 * mt) = s[mt];
     }
-    f32x4 prod[MT][NT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
+    for (int mt = 0; mt < NT; ++mt) {
+      f32x4 prod = zero4();
 #pragma unroll
-      for (int nt = 0; nt < NT; ++nt) prod[mt][nt] = zero4();
-#pragma unroll
-    for (int kb = 0; kb < DK / 32; ++kb) {
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) {
-        float fb[8];
-        frag_kcontig(st_t, LDT, nt * 16 + ln, kb * 32, g, fb);
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) mma_blk<P>(prod[mt][nt], cP[mt][kb], fb);
+      for (int kb = 0; kb < KB; ++kb) {
+        // A = S^T: column 16 mt + ln of the state, rows 32 kb + kap(g, .)
+        float fa[8];
+        const float* src = st_t + (16 * mt + ln) * LDT + 32 * kb + 4 * g;
+        const float4 lo = *reinterpret_cast<const float4*>(src);
+        const float4 hi = *reinterpret_cast<const float4*>(src + 16);
+        fa[0] = lo.x; fa[1] = lo.y; fa[2] = lo.z; fa[3] = lo.w;
+        fa[4] = hi.x; fa[5] = hi.y; fa[6] = hi.z; fa[7] = hi.w;
+        mma_blk<P>(prod, fa, cP[kb]);
       }
+      s[mt] = prod * e + cS[mt];
     }
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int nt = 0; nt < NT; ++nt) s[mt][nt] = prod[mt][nt] * e + cS[mt][nt];
     __syncthreads();  // every wave has read the old state
     publish();
     __syncthreads();
   }
 
-  float* out = args.S_out + (static_cast<long>(req) * args.h_v + h) * state_sz;
+  float* out = args.S_out + hs * state_sz + static_cast<long>(row) * DV + 4 * g;
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        out[(row0 + mt * 16 + 4 * g + i) * DV + nt * 16 + ln] = s[mt][nt][i];
+  for (int mt = 0; mt < NT; ++mt) *reinterpret_cast<f32x4*>(out + 16 * mt) = s[mt];
 }
 
 template <int DK, int DV>
