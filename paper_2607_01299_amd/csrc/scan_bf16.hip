@@ -46,6 +46,7 @@ namespace hypic {
 namespace {
 
 constexpr int kThreads = 512;
+constexpr int kGateWave = 1;  // loads and exponentiates the gates of each chunk
 constexpr int C = 64;        // tokens per chunk
 constexpr int NCOL = 64;     // state / operator columns per workgroup
 constexpr int KTC = C / 32;  // 32-wide contraction blocks over the chunk's tokens
@@ -215,11 +216,23 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
 
   // ---- work item ----------------------------------------------------------
   const int n_cb = with_op ? ((NP > NS) ? NP : NS) : (DV + span - 1) / span;
-  const int per_rank = n_cb * args.h_v;
-  const int rank = blockIdx.x / per_rank;
-  const int rem = blockIdx.x % per_rank;
-  const int h = rem / n_cb;
-  const int cb = rem % n_cb;
+  // Workgroups are dealt to the 8 XCDs round-robin; the n_cb column blocks of a
+  // chain are numbered so that they land on one XCD back to back and share its
+  // L2 for q and k.  Chains past the last full group of 8 keep linear order.
+  const int n_chains = static_cast<int>(gridDim.x) / n_cb;
+  const int full = (n_chains / 8) * 8 * n_cb;
+  int chain, cb;
+  if (static_cast<int>(blockIdx.x) < full) {
+    const int slot = blockIdx.x / 8;
+    chain = (slot / n_cb) * 8 + blockIdx.x % 8;
+    cb = slot % n_cb;
+  } else {
+    const int b = blockIdx.x - full;
+    chain = full / n_cb + b / n_cb;
+    cb = b % n_cb;
+  }
+  const int rank = chain / args.h_v;
+  const int h = chain % args.h_v;
   const int col0 = cb * span + wq * 16;  // this wave's 16 columns (of S or P_hat)
   const bool has_state = cb * span < DV;           // the block holds state columns
   const bool has_op = with_op && (cb < NP);
@@ -309,7 +322,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
                                                  4 * g0);
       }
     }
-    if (wave == 0) {
+    if (wave == kGateWave) {
       const int tc = (lane0 < n) ? lane0 : n - 1;
       const long idx = static_cast<long>(c0 + tc) * args.h_v + h;
       pa = args.log_alpha[idx];
@@ -385,7 +398,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       vB[1] = pack(vt[2], vt[3]);
     }
   }
-  if (wave == 0) {
+  if (wave == kGateWave) {
     float b = (lane < n) ? pa : 0.f;
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
@@ -554,6 +567,31 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
         }
       }
     }
+    // (Q K^T . Gamma) as A-operand fragments over key tokens for query rows
+#pragma unroll
+    for (int t = 0; t < 10; ++t) {
+      if (kq_owner(t) != wave) continue;
+      const int tr = tri_row(t), ti = tri_col(t);
+      const int r = tr * 16 + ln;
+      const float br = gb[r];
+      const f32x4 a = kq[kq_slot(t)];
+      u16x4 val;
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        const int i = ti * 16 + 4 * g + i4;
+        val[i4] = bf16_of((i <= r) ? a[i4] * __expf(br - gb[i]) : 0.f);
+      }
+      *reinterpret_cast<u16x4*>(fQK + frag_slot(tr, ti >> 1, KTC, lane) + (ti & 1) * 4) = val;
+    }
+    // zero halves (key tile > query tile): (1,0) (2,0) (3,0) (2,1) (3,1) (3,2)
+#pragma unroll
+    for (int t = 0; t < 6; ++t) {
+      if (((t < 4) ? t : t + 1) != wave) continue;  // waves 0-3, 5, 6
+      const int ti = (t < 3) ? t + 1 : ((t == 5) ? 3 : t - 1);
+      const int tr = (t < 3) ? 0 : ((t == 5) ? 2 : 1);
+      *reinterpret_cast<uint2*>(fQK + frag_slot(tr, ti >> 1, KTC, lane) + (ti & 1) * 4) =
+          make_uint2(0u, 0u);
+    }
     // The next chunk's tokens load while this chunk computes.  Issuing the loads
     // keeps the CU's load path busy for ~1.5k cycles, so they are issued where
     // the waves would otherwise wait: waves 0-2 here, waves 3-7 (idle while
@@ -644,31 +682,6 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       st_frag(fAbh, s * 8, hh);
       st_frag(fAbl, s * 8, ll);
       st_frag(fAgb, s * 8, gg);
-    }
-    // (Q K^T . Gamma) as A-operand fragments over key tokens for query rows
-#pragma unroll
-    for (int t = 0; t < 10; ++t) {
-      if (kq_owner(t) != wave) continue;
-      const int tr = tri_row(t), ti = tri_col(t);
-      const int r = tr * 16 + ln;
-      const float br = gb[r];
-      const f32x4 a = kq[kq_slot(t)];
-      u16x4 val;
-#pragma unroll
-      for (int i4 = 0; i4 < 4; ++i4) {
-        const int i = ti * 16 + 4 * g + i4;
-        val[i4] = bf16_of((i <= r) ? a[i4] * __expf(br - gb[i]) : 0.f);
-      }
-      *reinterpret_cast<u16x4*>(fQK + frag_slot(tr, ti >> 1, KTC, lane) + (ti & 1) * 4) = val;
-    }
-    // zero halves (key tile > query tile): (1,0) (2,0) (3,0) (2,1) (3,1) (3,2)
-#pragma unroll
-    for (int t = 0; t < 6; ++t) {
-      if (t != wave) continue;
-      const int ti = (t < 3) ? t + 1 : ((t == 5) ? 3 : t - 1);
-      const int tr = (t < 3) ? 0 : ((t == 5) ? 2 : 1);
-      *reinterpret_cast<uint2*>(fQK + frag_slot(tr, ti >> 1, KTC, lane) + (ti & 1) * 4) =
-          make_uint2(0u, 0u);
     }
     lds_barrier();
 
