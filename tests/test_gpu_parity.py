@@ -312,6 +312,20 @@ def test_error_leaves_outputs_untouched(hy):
         hy.compose_segments(P, g, S, ids, offs)
 
 
+def test_chain_count_not_a_multiple_of_eight(hy):
+    """21 chains x 2 column blocks: the first 16 chains take the XCD-grouped
+    workgroup numbering, the last 5 the linear one; both must match the oracle."""
+    lens = [97, 130, 64, 1, 200, 33, 150]
+    _say("7 segments x 3 v-heads bf16 d=128 lens=%s" % lens)
+    w = W.segment_workload(2, lengths=lens, heads=(1, 3))
+    d = _dev(w)
+    cu = w["cu_seqlens"]
+    res = hy.build_segment(d["q"], d["k"], d["v"], d["beta"], d["log_alpha"], cu)
+    torch.cuda.synchronize()
+    ref = oracle.build_segments(w["q"], w["k"], w["v"], w["beta"], w["log_alpha"], cu)
+    _check_build(res, ref, cu, _all_pairs(len(lens), 3), TOL[W.BF16], "21 chains")
+
+
 @pytest.mark.parametrize("dk,dv,heads", [(128, 128, (2, 4)), (128, 64, (1, 2)), (64, 128, (1, 1))])
 def test_build_without_operator(hy, dk, dv, heads):
     """Without the operator every wave carries state columns; o and S_seg must
