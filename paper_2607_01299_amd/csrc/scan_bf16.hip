@@ -1,39 +1,59 @@
 // Chunked gated-delta-rule scan, bf16 inputs, chunk 64: the production path
 // of the segment build and the seam rescan on gfx950.
 //
-// Same mathematics as scan.hip (per chunk: Gram matrix, unit-lower-triangular
-// inverse A1 = (I + L)^{-1}, WY factor W, then the state / operator update),
-// organised for the CDNA4 matrix cores:
+// Mathematics (per chunk of 64 tokens, incoming state S0; b = prefix sum of
+// log alpha inside the chunk, gamma = exp(b), Gamma_ri = exp(b_r - b_i)):
+//   L  = strictly-lower part of diag(beta) K K^T,   A1 = (I + L)^{-1}
+//   W  = A1 diag(beta) K,       U = (A1 . Gamma) diag(beta) V
+//   Vn = U - diag(gamma) W S0
+//   O  = diag(gamma) Q S0 + (tril(Q K^T) . Gamma) Vn
+//   S  <- gamma_last S0 + K^T diag(exp(b_last - b)) Vn
+//   P  <- P0 - K^T (W P0)                         (decay-free operator)
+// i.e. the token recurrence of Eq. (2) with the GDN transition of Tab. 1
+// applied 64 times (diag(gamma) A1 diag(gamma)^{-1} = A1 . Gamma turns the
+// decay-free UT transform into the gated one), and the identity-start operator
+// construction of Sec. 5 with the gate factored out as in Tab. 3.
 //
-// * Work split.  One workgroup of 8 waves runs one (segment, v-head, column
-//   block) chain: waves 0-3 own 16 columns each of a 64-column block of the
-//   state S (and emit those output columns), waves 4-7 own the same 64 columns
-//   of the operator P_hat.  The chunk's Gram matrix, inverse and W are computed
-//   once per workgroup and shared by both halves; each SIMD runs one state
-//   wave and one operator wave, so one's matrix-core work hides the other's
-//   latency.
-// * Operand layout.  Every matrix-core operand is staged in LDS "fragment
-//   major": a 16 x 32 (rows x contraction) tile is 64 lanes x 8 bf16 stored in
-//   lane order, so a lane reads its fragment with one 16-byte load and a wave
-//   reads 1 KiB of consecutive bytes.  Products whose result feeds another
-//   product are computed transposed where that makes the accumulator tile
-//   already be the next operand's fragment (W^T = K^T (A1 diag beta)^T,
-//   K Q^T, O^T), and states are used as operands straight from registers.
-// * Gates are exponentiated once per chunk (b = prefix sum of log alpha,
-//   gamma = exp(b), exp(b_last - b)); every decay factor is exp of a
-//   non-positive number.
-// * The inverse: the four 16 x 16 diagonal blocks by column-parallel
-//   substitution in one wave (one 16-lane row per block, coefficients shared
-//   by DPP row broadcasts), overlapping the other waves' Gram and K Q^T tiles;
-//   then the off-diagonal blocks
-//   A_ij = -sum_k N_ik A_kj with N_ik = A_ii L_ik on float32 matrix cores, one
-//   block diagonal at a time.
-// * The next chunk's q, k, v, beta, log alpha are loaded into registers while
-//   the current chunk computes.
-// * Precision: W is formed in two bf16 passes (A1 diag(beta) split hi + lo, K
-//   exact) and kept as hi + lo; the state path uses single bf16 passes (its
-//   decay keeps rounding from accumulating); the operator path, which has no
-//   decay, uses W hi + lo and splits P0 (three passes for W P0, two for K^T X).
+// Organisation on CDNA4.  One workgroup of 8 waves runs one (segment, v-head,
+// 64-column block) chain.  The waves have fixed roles and the chunk loop is
+// software-pipelined three deep, so the chunk-local work (which does not
+// depend on the state) runs ahead of the sequential state update:
+//   waves 0-1  state columns (32 each): U, Vn, outputs, S update for chunk c;
+//   waves 2-3  operator columns (32 each): X = W P0, P update for chunk c
+//              (without the operator they carry state columns too);
+//   wave 4     inverse of chunk c + 2: Gram matrix, the four diagonal 16 x 16
+//              blocks of A1 by column-parallel substitution (DPP row
+//              broadcasts), the off-diagonal blocks by split-bf16 products
+//              (three passes), all in registers; blocks are transposed by
+//              products with the identity and written straight into the
+//              split bf16 fragments of A1 diag(beta);
+//   waves 5-7  chunk c + 1: gates, K Q^T masked with Gamma and the Q
+//              fragments (wave 5, which loads K and Q once per workgroup),
+//              K^T (waves 6, 7: one d_k half each), W (hi + lo) and
+//              (A1 . Gamma) diag(beta) as matrix-core fragments.
+// Each iteration has two LDS-only barriers: the consumers' state-independent
+// products read the previous iteration's fragments before the first, their
+// K^T products follow it; the producers write K^T, Q and gates for c + 1
+// before the first barrier (double-buffered) and W, (A1 . Gamma) beta and
+// (Q K^T . Gamma) after it (single-buffered, the consumers are done with them).
+//
+// Products are v_mfma_f32_32x32x16_bf16 wherever an operand comes from LDS
+// (twice the work of a 16x16x32 product per byte of operand traffic).  Every
+// operand is stored "fragment major": a 32 x 16 operand block is 64 lanes x 8
+// bf16 in lane order, read with one 16-byte load per lane.  Within a 16-deep
+// contraction step, slot (g2, j) of lane group g2 = lane / 32 carries index
+// 8(j / 4) + 4 g2 + j % 4, which is exactly the row set a 32 x 32 accumulator
+// holds in elements 8h .. 8h+7: accumulators feed the next product as
+// operands with no data movement.  Rows of the state and the operator are kept
+// in the matching order rho (true row d = rho with bits 2 and 3 swapped), so
+// operands loaded straight from HBM (q, k rows: 16 contiguous bytes per lane)
+// meet them without shuffles; rows are mapped back only at the HBM boundary.
+//
+// Precision: q, k, v are exact in bf16.  W is formed from A1 diag(beta)
+// split into bf16 hi + lo (K exact) and kept as hi + lo; the state path uses
+// single bf16 operands (its decay keeps rounding from accumulating); the
+// operator path, which has no decay, splits its float32 operands (three
+// passes for W P0, two for K^T X).
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -46,176 +66,916 @@ namespace hypic {
 namespace {
 
 constexpr int kThreads = 512;
-constexpr int kGateWave = 1;  // loads and exponentiates the gates of each chunk
-constexpr int C = 64;        // tokens per chunk
-constexpr int NCOL = 64;     // state / operator columns per workgroup
-constexpr int KTC = C / 32;  // 32-wide contraction blocks over the chunk's tokens
-constexpr int LDC = C + 4;   // row stride (floats) of the float32 chunk x chunk matrices
-constexpr int LDD = 20;      // row stride (floats) of the staged diagonal blocks of A1
+constexpr int C = 64;     // tokens per chunk
+constexpr int NCOL = 64;  // state / operator columns per workgroup (with the operator)
+constexpr int FR = 512;   // u16 elements of one fragment (64 lanes x 8 bf16)
 
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef unsigned short u16;
 typedef u16 u16x4 __attribute__((ext_vector_type(4)));
-typedef short s16x4 __attribute__((ext_vector_type(4)));
 
-// ---- fragment-major layout -------------------------------------------------
-// logical R x K matrix (contraction over K), KT = K / 32 blocks per row tile.
-__device__ __forceinline__ int frag_slot(int rt, int kt, int KT, int lane) {
-  return ((rt * KT + kt) * 64 + lane) * 8;
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
 }
-__device__ __forceinline__ bf16x8 ld_frag(const u16* base, int slot) {
-  return *reinterpret_cast<const bf16x8*>(base + slot);
+__device__ __forceinline__ f32x16 mma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
-__device__ __forceinline__ void st_frag(u16* base, int slot, bf16x8 v) {
-  *reinterpret_cast<bf16x8*>(base + slot) = v;
-}
-
-__device__ __forceinline__ f32x4 mma(bf16x8 a, bf16x8 b, f32x4 c) {
+__device__ __forceinline__ f32x4 mma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
-
-__device__ __forceinline__ bf16x8 pack(const f32x4& lo, const f32x4& hi) {
-  bf16x8 r;
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+// 16 x 16 x 16 product of float32 operands on the bf16 matrix cores, split
+// into hi + lo terms (hi*hi + hi*lo + lo*hi): a[s] = A[r][4g + s],
+// b[s] = B[4g + s][n]; lane (g, n) of the result holds C[4g + e][n]
+__device__ __forceinline__ void split4(const f32x4& x, s16x4& hi, s16x4& lo) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    r[i] = static_cast<__bf16>(lo[i]);
-    r[4 + i] = static_cast<__bf16>(hi[i]);
+    const __bf16 h = static_cast<__bf16>(x[i]);
+    hi[i] = __builtin_bit_cast(short, h);
+    lo[i] = __builtin_bit_cast(short, static_cast<__bf16>(x[i] - static_cast<float>(h)));
   }
+}
+struct Split4 {
+  s16x4 h, l;
+};
+__device__ __forceinline__ Split4 split4(const f32x4& x) {
+  Split4 r;
+  split4(x, r.h, r.l);
   return r;
 }
-__device__ __forceinline__ void pack_split(const f32x4& lo, const f32x4& hi, bf16x8& h,
-                                           bf16x8& l) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    h[i] = static_cast<__bf16>(lo[i]);
-    h[4 + i] = static_cast<__bf16>(hi[i]);
-    l[i] = static_cast<__bf16>(lo[i] - static_cast<float>(h[i]));
-    l[4 + i] = static_cast<__bf16>(hi[i] - static_cast<float>(h[4 + i]));
-  }
-}
-
-// float32 16x16x16 product on matrix cores: a[s] = A[m][4g+s], b[s] = B[4g+s][n]
-__device__ __forceinline__ f32x4 mma16_f32(const float4& a, const float4& b, f32x4 c) {
-  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, b.x, c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, b.y, c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, b.z, c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, b.w, c, 0, 0, 0);
+__device__ __forceinline__ f32x4 mma16_x3(const Split4& a, const Split4& b, f32x4 c) {
+  c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.h, b.h, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.h, b.l, c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.l, b.h, c, 0, 0, 0);
   return c;
 }
 
-__device__ __forceinline__ u16 bf16_of(float x) {
+// elements 8h .. 8h+7 of a 32 x 32 accumulator: one 16-deep operand step
+__device__ __forceinline__ bf16x8 frag_of(const f32x16& a, int h) {
+  bf16x8 r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = static_cast<__bf16>(a[8 * h + j]);
+  return r;
+}
+__device__ __forceinline__ void split_of(const f32x16& a, int h, bf16x8& hi, bf16x8& lo) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float x = a[8 * h + j];
+    hi[j] = static_cast<__bf16>(x);
+    lo[j] = static_cast<__bf16>(x - static_cast<float>(hi[j]));
+  }
+}
+
+__device__ __forceinline__ bf16x8 ldf(const u16* base, int f, int lane) {
+  return *reinterpret_cast<const bf16x8*>(base + f * FR + lane * 8);
+}
+__device__ __forceinline__ void stf(u16* base, int f, int lane, bf16x8 v) {
+  *reinterpret_cast<bf16x8*>(base + f * FR + lane * 8) = v;
+}
+
+__device__ __forceinline__ uint4 mask4(uint4 w, bool keep) {
+  const uint32_t m = keep ? 0xffffffffu : 0u;
+  return make_uint4(w.x & m, w.y & m, w.z & m, w.w & m);
+}
+__device__ __forceinline__ bf16x8 as_bf(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
+__device__ __forceinline__ bf16x8 masked(uint4 w, bool keep) { return as_bf(mask4(w, keep)); }
+
+__device__ __forceinline__ u16 bf16_bits(float x) {
   __bf16 h = static_cast<__bf16>(x);
-  return *reinterpret_cast<u16*>(&h);
+  return __builtin_bit_cast(u16, h);
+}
+
+// true row of element (tile m, element e) held by lane group g2 of a state or
+// operator accumulator: rho = 32m + 8(e/4) + 4 g2 + e%4 with bits 2, 3 swapped
+__device__ __forceinline__ int true_row(int m, int e, int g2) {
+  const int b = e >> 2;
+  return 32 * m + 16 * (b >> 1) + 8 * g2 + 4 * (b & 1) + (e & 3);
+}
+// token (or contraction index) carried by slot j of lane group g2 in step s
+__device__ __forceinline__ int slot_idx(int s, int g2, int j) {
+  return 16 * s + 8 * (j >> 2) + 4 * g2 + (j & 3);
 }
 
 // Step I of the column-parallel unit-lower substitution on 16-lane rows: lane
 // 16b + c holds column c of the solution (x) and column c of -L (lcol); the
 // coefficient -L[r][I] comes from lane I of the same row (DPP row_newbcast:I).
+// The broadcast and the multiply-add are one instruction (v_fmac_f32 with a
+// DPP source operand).  lcol is written well before its first use as a DPP
+// source, so no extra wait states are needed beyond the one nop in front.
 template <int I>
 __device__ __forceinline__ void unit_lower_solve_step(float (&x)[16], const float (&lcol)[16]) {
   if constexpr (I < 15) {
-    float nl[16];
 #pragma unroll
     for (int r = I + 1; r < 16; ++r)
-      nl[r] = __builtin_bit_cast(
-          float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, lcol[r]), 0x150 + I, 0xF, 0xF,
-                                          false));
-#pragma unroll
-    for (int r = I + 1; r < 16; ++r) x[r] = __builtin_fmaf(nl[r], x[I], x[r]);
+      asm("v_fmac_f32_dpp %0, %1, %2 row_newbcast:%3 row_mask:0xf bank_mask:0xf"
+          : "+v"(x[r])
+          : "v"(lcol[r]), "v"(x[I]), "n"(I));
     unit_lower_solve_step<I + 1>(x, lcol);
   }
 }
 
-// Row order of the d_k dimension inside the kernel.  q and k are loaded 16
-// contiguous bytes per lane (lane (g, m) of a 32-column block holds columns
-// 8g .. 8g+7), which makes a matrix-core slot (g, j) carry column 8g + j.  The
-// transposed K tiles, and with them the state and operator rows, are laid out
-// so that packing row tiles (2kb, 2kb+1) from accumulators gives exactly that
-// slot order: row m of d_k tile dt is d = d_perm(dt, m).  Rows are mapped back
-// to their true index only where a state or operator enters or leaves HBM.
-__device__ __forceinline__ int d_perm(int dt, int m) {
-  return 32 * (dt >> 1) + 8 * (m >> 2) + 4 * (dt & 1) + (m & 3);
-}
+// index of fragment (row tile t, step s) in the 6-fragment lower-triangular
+// sets (t = 0: s = 0, 1; t = 1: s = 0..3)
+__device__ __forceinline__ int tri_idx(int t, int s) { return (t == 0) ? s : 2 + s; }
 
-// lower-triangle tile t in 0..9 -> (row tile, column tile) with column <= row
-__device__ __forceinline__ int tri_row(int t) { return (t < 1) ? 0 : (t < 3) ? 1 : (t < 6) ? 2 : 3; }
-__device__ __forceinline__ int tri_col(int t) { return t - tri_row(t) * (tri_row(t) + 1) / 2; }
-
-// owner wave and register slot of K Q^T tile t (query tile tri_row(t), key tile
-// tri_col(t)): wave w holds the tiles of key tile w in slot (query - key); the
-// tile (query 3, key 0) goes to wave 3, slot 1
-__device__ __forceinline__ int kq_owner(int t) { return (t == 6) ? 3 : tri_col(t); }
-__device__ __forceinline__ int kq_slot(int t) { return (t == 6) ? 1 : tri_row(t) - tri_col(t); }
-
-// ---- LDS plan (bytes); regions are reused across the phases of a chunk ------
-// Phase 0 of chunk c + 1 runs in the same barrier interval as the chain update
-// of chunk c, so everything that update reads and phase 0 writes is kept
-// apart: K over tokens and the gates are double-buffered, W hi and the
-// (Q K^T . Gamma) fragments have regions of their own.
+// ---- LDS plan (bytes) --------------------------------------------------------
 template <int DK>
 struct Lds {
-  static constexpr int FK = C * DK * 2;     // bytes of a 64 x DK bf16 fragment matrix
-  static constexpr int F32M = C * LDC * 4;  // padded 64 x 64 float32 matrix
-  static constexpr int RA = (FK > F32M) ? FK : F32M;
-  static constexpr int GATES = 4 * C * 4;
-  static constexpr int O_KD = 0;            // K over d -> A1 (f32)
-  static constexpr int O_Q = O_KD + RA;     // Q over d -> A1^T -> (A1 . Gamma) beta
-  static constexpr int O_KT = O_Q + RA;     // K over tokens, two buffers
-  static constexpr int O_L = O_KT + 2 * FK;  // L^T (f32) + N blocks -> A1 beta hi / lo
-  static constexpr int O_WS = O_L + F32M;   // gamma W (state path)
-  static constexpr int O_WL = O_WS + FK;    // staged A1 diagonal blocks -> W lo (operator path)
-  static constexpr int O_WH = O_WL + FK;    // W hi (operator path)
-  static constexpr int O_QK = O_WH + FK;    // (Q K^T . Gamma)
-  static constexpr int O_G = O_QK + C * C * 2;  // gates, two buffers
-  static constexpr int TOTAL = O_G + 2 * GATES;
-  static_assert(2 * C * C * 2 <= F32M, "A1 beta hi + lo fit the L region");
-  static_assert(C * C * 2 <= RA, "(A1 . Gamma) beta fits the Q region");
-  static_assert(C * LDD * 4 <= FK, "staged diagonal blocks fit the W lo region");
+  static constexpr int FB = FR * 2;            // bytes of one fragment
+  static constexpr int NKT = (DK / 32) * 4;    // K^T fragments (rho tile m, token step s)
+  static constexpr int NW = 2 * (DK / 16);     // W / Q fragments (token tile t, d step u)
+  static constexpr int O_KT = 0;                       // K^T, two buffers
+  static constexpr int O_WH = O_KT + 2 * NKT * FB;     // W hi
+  static constexpr int O_WL = O_WH + NW * FB;          // W lo (operator path)
+  static constexpr int O_Q = O_WL + NW * FB;           // Q, two buffers
+  static constexpr int O_QK = O_Q + 2 * NW * FB;       // (Q K^T . Gamma)^T, 6 fragments
+  static constexpr int O_AG = O_QK + 6 * FB;           // (A1 . Gamma) diag(beta), 6 fragments
+  static constexpr int O_AB = O_AG + 6 * FB;           // A1 diag(beta) hi + lo, two buffers
+  static constexpr int O_G = O_AB + 2 * 12 * FB;       // gates b, beta, gamma, dec; two buffers
+  static constexpr int O_BS = O_G + 2 * 4 * C * 4;     // inverse wave: beta
+  static constexpr int TOTAL = O_BS + C * 4;
   static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
-template <int DK, int DV>
-__global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
-  using LP = Lds<DK>;
-  constexpr int KTD = DK / 32;  // contraction blocks over d_k
-  constexpr int DT = DK / 16;   // d_k row tiles of the state
-  constexpr int NS = DV / NCOL;
-  constexpr int NP = DK / NCOL;
+// Shared description of the chain a workgroup runs.
+struct Chain {
+  int seg, h, hk, lo, hi, nc, cb;
+  long sh;            // seg * h_v + h
+  long qk_stride;     // elements between token rows of q, k
+  long v_stride;      // elements between token rows of v, o
+  bool with_op, need_state, need_op;
+};
 
-  extern __shared__ __align__(16) unsigned char smem[];
-  u16* fKd = reinterpret_cast<u16*>(smem + LP::O_KD);
-  float* A1 = reinterpret_cast<float*>(smem + LP::O_KD);
-  u16* fQ = reinterpret_cast<u16*>(smem + LP::O_Q);
-  float* A1t = reinterpret_cast<float*>(smem + LP::O_Q);
-  u16* fAgb = reinterpret_cast<u16*>(smem + LP::O_Q);
-  float* Lt = reinterpret_cast<float*>(smem + LP::O_L);
-  u16* fAbh = reinterpret_cast<u16*>(smem + LP::O_L);
-  u16* fAbl = fAbh + C * C;
-  u16* fWs = reinterpret_cast<u16*>(smem + LP::O_WS);
-  u16* fWl = reinterpret_cast<u16*>(smem + LP::O_WL);
-  u16* fWh = reinterpret_cast<u16*>(smem + LP::O_WH);
-  u16* fQK = reinterpret_cast<u16*>(smem + LP::O_QK);
-  float* Dg = reinterpret_cast<float*>(smem + LP::O_WL);  // diagonal blocks of A1 (phase 1-2)
-  // buffer set par of the double-buffered regions
-  auto kt_buf = [&](int par) { return reinterpret_cast<u16*>(smem + LP::O_KT + par * LP::FK); };
-  auto gate_buf = [&](int par) {
-    return reinterpret_cast<float*>(smem + LP::O_G + par * LP::GATES);
+__device__ __forceinline__ int chunk_len(const Chain& ch, int c) {
+  const int r = ch.hi - (ch.lo + c * C);
+  return (r < C) ? r : C;
+}
+
+// raw 16-byte loads of the 32x32-layout fragments of one token tile of a
+// token-major bf16 matrix: lane (g2, r) gets row 32t + r, columns 16u + 8g2 ..
+// +7 for u = 0 .. NU-1 (rows past the chunk are clamped; zeroed at use)
+template <int NU>
+__device__ __forceinline__ void load_tile32(uint4 (&dst)[NU], const u16* base, long rs, int c0,
+                                            int n, int t, int lane) {
+  const int tok = 32 * t + (lane & 31);
+  const int tc = (tok < n) ? tok : n - 1;
+  const u16* p = base + static_cast<long>(c0 + tc) * rs + 8 * (lane >> 5);
+#pragma unroll
+  for (int u = 0; u < NU; ++u) dst[u] = *reinterpret_cast<const uint4*>(p + 16 * u);
+}
+
+// =============================================================================
+// wave 4: A1 diag(beta) of chunk c + 2
+// =============================================================================
+// Exchange (tile b, 16-lane row g) <-> (tile g, 16-lane row b) of four 16 x 16
+// tiles held one f32x4 per lane: an involution on (tile, lane row) pairs, done
+// with cross-row lane swaps.
+__device__ __forceinline__ void exchange_tiles(f32x4 (&x)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+#pragma unroll
+    for (int b2 = 0; b2 < 2; ++b2) {  // upper half of tile b2 <-> lower half of b2 + 2
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x[b2][i]),
+                                                      __float_as_uint(x[b2 + 2][i]), false, false);
+      // the two results are copied out one by one before any bit cast
+      const unsigned r0 = r[0], r1 = r[1];
+      x[b2][i] = __uint_as_float(r0);
+      x[b2 + 2][i] = __uint_as_float(r1);
+    }
+#pragma unroll
+    for (int b2 = 0; b2 < 4; b2 += 2) {  // odd rows of tile b2 <-> even rows of b2 + 1
+      const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x[b2][i]),
+                                                      __float_as_uint(x[b2 + 1][i]), false, false);
+      const unsigned r0 = r[0], r1 = r[1];
+      x[b2][i] = __uint_as_float(r0);
+      x[b2 + 1][i] = __uint_as_float(r1);
+    }
+  }
+}
+
+// X^T of a 16 x 16 float32 tile in accumulator form (lane (g, n): X[4g + e][n]):
+// the tile used as an A operand is X^T, multiplied by the identity in two
+// exact bf16 passes (hi, lo)
+__device__ __forceinline__ f32x4 transpose16(const Split4& x, const s16x4& eye) {
+  f32x4 c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(x.h, eye, zero4(), 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(x.l, eye, c, 0, 0, 0);
+}
+
+template <int DK, int DV>
+__device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& ch,
+                                             unsigned char* smem, int lane) {
+  using LP = Lds<DK>;
+  constexpr int KTD = DK / 32;
+  const int g = lane >> 4, n16 = lane & 15;
+  float* bs = reinterpret_cast<float*>(smem + LP::O_BS);
+  const u16* kg = static_cast<const u16*>(args.k) + ch.hk * DK;
+
+  s16x4 eye;  // 16 x 16 identity as a B operand: lane (g, n) slot j is 1 where 4g + j == n
+#pragma unroll
+  for (int j = 0; j < 4; ++j) eye[j] = (4 * g + j == n16) ? short(0x3F80) : short(0);
+
+  // Row-form block (i, jb) of A1 (lane (g, n): A1[16i + n][16jb + 4g + e]),
+  // scaled by -beta of the column and split hi + lo, into the fragments (t, s)
+  // of -A1 diag(beta) (stored negated, so W comes out negated and the
+  // operator path needs no sign flip): lane (g2, r) of fragment (t, s) holds
+  // columns 16s + 8(j/4) + 4g2 + j%4 of row 32t + r, so this lane's four
+  // values are slots 4(g/2) .. +3 of lane 32(g%2) + 16(i%2) + n of fragment
+  // (i/2, jb).
+  auto emit = [&](u16* ab, int i, int jb, const f32x4& x, bool zero) __attribute__((always_inline)) {
+    float4 bb = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (!zero) bb = *reinterpret_cast<const float4*>(bs + 16 * jb + 4 * g);
+    const float v[4] = {-x[0] * bb.x, -x[1] * bb.y, -x[2] * bb.z, -x[3] * bb.w};
+    u16x4 hi, lo;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const __bf16 h = static_cast<__bf16>(v[e]);
+      hi[e] = __builtin_bit_cast(u16, h);
+      lo[e] = bf16_bits(v[e] - static_cast<float>(h));
+    }
+    const int off = tri_idx(i >> 1, jb) * FR + (32 * (g & 1) + 16 * (i & 1) + n16) * 8 + 4 * (g >> 1);
+    *reinterpret_cast<u16x4*>(ab + off) = hi;
+    *reinterpret_cast<u16x4*>(ab + 6 * FR + off) = lo;
   };
 
+  // 16x16x32 A fragments of K: lane (g, r) holds K[16t + r][32u + 8g .. +7]
+  uint4 kr[4][KTD];
+  float pb = 0.f;
+  auto prefetch = [&](int c) __attribute__((always_inline)) {
+    const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int tok = 16 * t + n16;
+      const int tc = (tok < n) ? tok : n - 1;
+      const u16* p = kg + static_cast<long>(c0 + tc) * ch.qk_stride + 8 * g;
+#pragma unroll
+      for (int u = 0; u < KTD; ++u) kr[t][u] = *reinterpret_cast<const uint4*>(p + 32 * u);
+    }
+    const int tc = (lane < n) ? lane : n - 1;
+    pb = args.beta[static_cast<long>(c0 + tc) * args.h_v + ch.h];
+  };
+  if (ch.nc > 0) prefetch(0);
+  // The fragments hold the blocks above the diagonal (0,1) and (2,3) too; they
+  // stay zero (per chunk only blocks on or below the diagonal are written).
+#pragma unroll
+  for (int par = 0; par < 2; ++par) {
+    u16* ab = reinterpret_cast<u16*>(smem + LP::O_AB + par * 12 * LP::FB);
+    emit(ab, 0, 1, zero4(), true);
+    emit(ab, 2, 3, zero4(), true);
+  }
+
+  for (int it = -2; it < ch.nc; ++it) {
+    const int c = it + 2;
+    const bool active = c < ch.nc;
+    f32x4 gu[6];      // upper Gram tiles (k, i), k < i: rows of L_ik once scaled by beta
+    f32x4 dc[4], dr[4];  // diagonal blocks D_b of A1: accumulator form, row form
+    if (active) {
+      const int n = chunk_len(ch, c);
+      const float beta = (lane < n) ? pb : 0.f;
+      bs[lane] = beta;
+      if (n < C) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int u = 0; u < KTD; ++u) kr[t][u] = mask4(kr[t][u], 16 * t + n16 < n);
+      }
+      f32x4 gd[4];
+#pragma unroll
+      for (int bd = 0; bd < 4; ++bd) {
+        gd[bd] = zero4();
+#pragma unroll
+        for (int u = 0; u < KTD; ++u) gd[bd] = mma16(as_bf(kr[bd][u]), as_bf(kr[bd][u]), gd[bd]);
+      }
+#pragma unroll
+      for (int p = 0; p < 6; ++p) {
+        // pairs (0,1) (0,2) (0,3) (1,2) (1,3) (2,3)
+        const int k = (p < 3) ? 0 : ((p < 5) ? 1 : 2);
+        const int i = (p < 3) ? p + 1 : ((p < 5) ? p - 1 : 3);
+        gu[p] = zero4();
+#pragma unroll
+        for (int u = 0; u < KTD; ++u) gu[p] = mma16(as_bf(kr[k][u]), as_bf(kr[i][u]), gu[p]);
+      }
+      if (c + 1 < ch.nc) prefetch(c + 1);
+      // afterwards lane 16b + c of tile q holds G_b[4q + e][c]: lane 16b + c has
+      // column c of the diagonal Gram block b
+      exchange_tiles(gd);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");  // beta visible to the wave
+      const int ob = g * 16;
+      float lcol[16];  // -L[r][c] = -beta_r G[r][c] of block g (used for r > c)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const float4 bb = *reinterpret_cast<const float4*>(bs + ob + 4 * q4);
+        lcol[4 * q4] = -bb.x * gd[q4][0];
+        lcol[4 * q4 + 1] = -bb.y * gd[q4][1];
+        lcol[4 * q4 + 2] = -bb.z * gd[q4][2];
+        lcol[4 * q4 + 3] = -bb.w * gd[q4][3];
+      }
+      float xd[16];  // lane 16b + c: column c of D_b
+#pragma unroll
+      for (int r = 0; r < 16; ++r) xd[r] = (r == n16) ? 1.f : 0.f;
+      asm volatile("s_nop 1" ::: "memory");
+      unit_lower_solve_step<0>(xd, lcol);
+      // the same exchange turns the columns into accumulator form
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
+        dc[q4] = f32x4{xd[4 * q4], xd[4 * q4 + 1], xd[4 * q4 + 2], xd[4 * q4 + 3]};
+      exchange_tiles(dc);
+#pragma unroll
+      for (int bd = 0; bd < 4; ++bd) dr[bd] = transpose16(split4(dc[bd]), eye);
+    }
+    lds_barrier();
+    if (active) {
+      u16* ab = reinterpret_cast<u16*>(smem + LP::O_AB + (c & 1) * 12 * LP::FB);
+      // L_ik as A operand: lane (g, r): beta_{16i + r} G[16i + r][16k + 4g + s];
+      // every operand is split into bf16 hi + lo once
+      auto Lr = [&](int i, int k) __attribute__((always_inline)) {
+        const int p = (k == 0) ? i - 1 : ((k == 1) ? i + 1 : 5);
+        return split4(gu[p] * bs[16 * i + n16]);
+      };
+      const Split4 L10 = Lr(1, 0), L20 = Lr(2, 0), L21 = Lr(2, 1);
+      const Split4 L30 = Lr(3, 0), L31 = Lr(3, 1), L32 = Lr(3, 2);
+      const Split4 D0 = split4(dc[0]), D1 = split4(dc[1]), D2 = split4(dc[2]);
+      const Split4 R1 = split4(dr[1]), R2 = split4(dr[2]), R3 = split4(dr[3]);
+      // A_ij = -D_i sum_{k=j}^{i-1} L_ik A_kj, one block column at a time
+      const f32x4 A10 = -mma16_x3(R1, split4(mma16_x3(L10, D0, zero4())), zero4());
+      const f32x4 A21 = -mma16_x3(R2, split4(mma16_x3(L21, D1, zero4())), zero4());
+      const f32x4 A32 = -mma16_x3(R3, split4(mma16_x3(L32, D2, zero4())), zero4());
+      const Split4 S10 = split4(A10), S21 = split4(A21);
+      const f32x4 A20 =
+          -mma16_x3(R2, split4(mma16_x3(L21, S10, mma16_x3(L20, D0, zero4()))), zero4());
+      const f32x4 A31 =
+          -mma16_x3(R3, split4(mma16_x3(L32, S21, mma16_x3(L31, D1, zero4()))), zero4());
+      const Split4 S20 = split4(A20);
+      const f32x4 A30 = -mma16_x3(
+          R3, split4(mma16_x3(L32, S20, mma16_x3(L31, S10, mma16_x3(L30, D0, zero4())))),
+          zero4());
+      // every block on or below the diagonal, in row form, into the fragments
+#pragma unroll
+      for (int bd = 0; bd < 4; ++bd) emit(ab, bd, bd, dr[bd], false);
+      emit(ab, 1, 0, transpose16(S10, eye), false);
+      emit(ab, 2, 1, transpose16(S21, eye), false);
+      emit(ab, 3, 2, transpose16(split4(A32), eye), false);
+      emit(ab, 2, 0, transpose16(S20, eye), false);
+      emit(ab, 3, 1, transpose16(split4(A31), eye), false);
+      emit(ab, 3, 0, transpose16(split4(A30), eye), false);
+    }
+    lds_barrier();
+  }
+}
+
+// =============================================================================
+// waves 5-7: the state-independent fragments of chunk c + 1
+// =============================================================================
+// W^T tiles (rho tile m, token tile t) = K^T (A1 diag beta)^T in two passes,
+// from the negated A1 diag(beta) fragments, so the tiles hold -W^T; the
+// accumulator halves are the fragments (t, u = 2m + h) of -W, kept as hi + lo.
+// Owners (wave 5, 6, 7 = 0, 1, 2) spread the tiles by cost (t = 1 costs twice
+// t = 0).
+template <int DK>
+__device__ __forceinline__ int wt_owner(int m, int t) {
+  if constexpr (DK == 128) {
+    constexpr int tab[4][2] = {{0, 1}, {0, 1}, {1, 2}, {2, 2}};
+    return tab[m][t];
+  } else {
+    constexpr int tab[2][2] = {{0, 1}, {1, 2}};
+    return tab[m][t];
+  }
+}
+
+template <int DK>
+__device__ __forceinline__ void emit_w(const Chain& ch, unsigned char* smem, int lane, int par,
+                                       int pw) {
+  using LP = Lds<DK>;
+  constexpr int NU = DK / 16;
+  constexpr int NM = DK / 32;
+  const u16* fKt = reinterpret_cast<const u16*>(smem + LP::O_KT + par * LP::NKT * LP::FB);
+  const u16* ab = reinterpret_cast<const u16*>(smem + LP::O_AB + par * 12 * LP::FB);
+  u16* fWh = reinterpret_cast<u16*>(smem + LP::O_WH);
+  u16* fWl = reinterpret_cast<u16*>(smem + LP::O_WL);
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      if (wt_owner<DK>(m, t) != pw) continue;
+      f32x16 acc = zero16();
+#pragma unroll
+      for (int s = 0; s < 2 * t + 2; ++s) {
+        const bf16x8 a = ldf(fKt, m * 4 + s, lane);
+        acc = mma32(a, ldf(ab, tri_idx(t, s), lane), acc);
+        acc = mma32(a, ldf(ab, 6 + tri_idx(t, s), lane), acc);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        bf16x8 hi, lo;
+        split_of(acc, h, hi, lo);
+        stf(fWh, t * NU + 2 * m + h, lane, hi);
+        if (ch.need_op) stf(fWl, t * NU + 2 * m + h, lane, lo);
+      }
+    }
+  }
+}
+
+// raw 16-byte loads of the 16x16x32-layout fragments of one 16-token tile of a
+// token-major bf16 matrix: lane (g, r) gets row 16t + r, columns 32u + 8g ..
+// +7 for u = 0 .. NB-1 (16 rows x 64 contiguous bytes per instruction; rows
+// past the chunk are clamped and zeroed at use)
+template <int NB>
+__device__ __forceinline__ void load_tile16(uint4 (&dst)[NB], const u16* base, long rs, int c0,
+                                            int n, int t, int lane) {
+  const int tok = 16 * t + (lane & 15);
+  const int tc = (tok < n) ? tok : n - 1;
+  const u16* p = base + static_cast<long>(c0 + tc) * rs + 8 * (lane >> 4);
+#pragma unroll
+  for (int u = 0; u < NB; ++u) dst[u] = *reinterpret_cast<const uint4*>(p + 32 * u);
+}
+
+// u16 offset of the four slots 4(g/2) .. +3 of lane 32(g%2) + 16h + n in
+// fragment f: where lane (g, n) of a 16 x 16 accumulator tile (rows 4g + e)
+// lands in a 32x32-layout operand fragment whose 16-deep step is that tile's
+// rows and whose 32-wide side holds the tile's columns at offset 16h
+__device__ __forceinline__ int scatter_off(int f, int h, int lane) {
+  const int g = lane >> 4, n = lane & 15;
+  return f * FR + (32 * (g & 1) + 16 * h + n) * 8 + 4 * (g >> 1);
+}
+__device__ __forceinline__ u16x4 pack4(float a, float b, float c, float d) {
+  u16x4 r;
+  r[0] = bf16_bits(a);
+  r[1] = bf16_bits(b);
+  r[2] = bf16_bits(c);
+  r[3] = bf16_bits(d);
+  return r;
+}
+
+// Wave 5: loads all of K and Q of the chunk (one copy per workgroup) and the
+// gates; forms K Q^T masked with Gamma, the Q fragments and its share of W.
+template <int DK, int DV>
+__device__ __forceinline__ void producer_qk_wave(const ScanArgs& args, const Chain& ch,
+                                                 unsigned char* smem, int lane) {
+  using LP = Lds<DK>;
+  constexpr int NU = DK / 16;
+  constexpr int KTD = DK / 32;
+  const int g = lane >> 4, n16 = lane & 15;
+  const u16* kg = static_cast<const u16*>(args.k) + ch.hk * DK;
+  const u16* qg = static_cast<const u16*>(args.q) + ch.hk * DK;
+  u16* fQK = reinterpret_cast<u16*>(smem + LP::O_QK);
+
+  // K Q^T tiles (k tile 1, q tile 0) and (3, 2) lie above the diagonal inside
+  // fragments that are read; they stay zero
+  *reinterpret_cast<u16x4*>(fQK + scatter_off(tri_idx(0, 1), 0, lane)) = pack4(0.f, 0.f, 0.f, 0.f);
+  *reinterpret_cast<u16x4*>(fQK + scatter_off(tri_idx(1, 3), 0, lane)) = pack4(0.f, 0.f, 0.f, 0.f);
+
+  uint4 kr[4][KTD], qr[4][KTD];
+  float pa = 0.f, pbeta = 0.f;
+  auto prefetch = [&](int c) __attribute__((always_inline)) {
+    const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      load_tile16<KTD>(kr[t], kg, ch.qk_stride, c0, n, t, lane);
+      load_tile16<KTD>(qr[t], qg, ch.qk_stride, c0, n, t, lane);
+    }
+    const int tc = (lane < n) ? lane : n - 1;
+    const long idx = static_cast<long>(c0 + tc) * args.h_v + ch.h;
+    pa = args.log_alpha[idx];
+    pbeta = args.beta[idx];
+  };
+  if (ch.nc > 0) prefetch(0);
+
+  for (int it = -2; it < ch.nc; ++it) {
+    const int p = it + 1;
+    const bool active = p >= 0 && p < ch.nc;
+    const int par = p & 1;
+    f32x4 kq[10];  // K Q^T 16 x 16 tiles (k tile tk <= q tile tq), in order of tq then tk
+    if (active) {
+      const int n = chunk_len(ch, p);
+      float* gb = reinterpret_cast<float*>(smem + LP::O_G + par * 4 * C * 4);
+      // gates: b = prefix sum of log alpha (stored in log2 units, b2 = b
+      // log2(e), so every decay factor is one exp2), beta, gamma = exp(b),
+      // exp(b_last - b)
+      {
+        float b = (lane < n) ? pa * 1.44269504088896341f : 0.f;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const float u = __shfl_up(b, off, 64);
+          if (lane >= off) b += u;
+        }
+        const float b_last = __shfl(b, 63, 64);
+        gb[lane] = b;
+        gb[C + lane] = (lane < n) ? pbeta : 0.f;
+        gb[2 * C + lane] = __builtin_amdgcn_exp2f(b);
+        gb[3 * C + lane] = __builtin_amdgcn_exp2f(b_last - b);
+      }
+      if (n < C) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int u = 0; u < KTD; ++u) {
+            kr[t][u] = mask4(kr[t][u], 16 * t + n16 < n);
+            qr[t][u] = mask4(qr[t][u], 16 * t + n16 < n);
+          }
+      }
+      if (ch.need_state) {
+        u16* fQ = reinterpret_cast<u16*>(smem + LP::O_Q + par * LP::NW * LP::FB);
+#pragma unroll
+        for (int tq = 0, i = 0; tq < 4; ++tq)
+#pragma unroll
+          for (int tk = 0; tk <= tq; ++tk, ++i) {
+            kq[i] = zero4();
+#pragma unroll
+            for (int u = 0; u < KTD; ++u) kq[i] = mma16(as_bf(kr[tk][u]), as_bf(qr[tq][u]), kq[i]);
+          }
+        // Q fragments for the consumers' (Q S0)^T: the 16 bytes of lane (g, r)
+        // of tile (t, u) are slot group g%2 of lane 16(t%2) + r of fragment
+        // (t/2, 2u + g/2)
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int u = 0; u < KTD; ++u)
+            *reinterpret_cast<uint4*>(fQ + ((t >> 1) * NU + 2 * u + (g >> 1)) * FR +
+                                      (32 * (g & 1) + 16 * (t & 1) + n16) * 8) = qr[t][u];
+      }
+    }
+    lds_barrier();
+    if (active) {
+      if (p + 1 < ch.nc) prefetch(p + 1);
+      if (ch.need_state) {
+        const float* gb = reinterpret_cast<const float*>(smem + LP::O_G + par * 4 * C * 4);
+        // (Q K^T . Gamma)^T as B fragments (key step s, query tile): the tile
+        // (tk, tq) holds (K Q^T)[16tk + 4g + e][16tq + n]; kept where key <= query,
+        // times exp(b_q - b_k)
+#pragma unroll
+        for (int tq = 0, i = 0; tq < 4; ++tq) {
+          const float bq = gb[16 * tq + n16];
+#pragma unroll
+          for (int tk = 0; tk <= tq; ++tk, ++i) {
+            const float4 bk = *reinterpret_cast<const float4*>(gb + 16 * tk + 4 * g);
+            const float bkv[4] = {bk.x, bk.y, bk.z, bk.w};
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              // computed for every slot, then selected: no divergent branch
+              const float x = kq[i][e] * __builtin_amdgcn_exp2f(bq - bkv[e]);
+              v[e] = (tk < tq || 4 * g + e <= n16) ? x : 0.f;
+            }
+            *reinterpret_cast<u16x4*>(fQK + scatter_off(tri_idx(tq >> 1, tk), tq & 1, lane)) =
+                pack4(v[0], v[1], v[2], v[3]);
+          }
+        }
+      }
+      emit_w<DK>(ch, smem, lane, par, 0);
+    }
+    lds_barrier();
+  }
+}
+
+// Waves 6, 7: load one d_k half of K (HALF = 0, 1) and form its K^T
+// fragments; then (A1 . Gamma) diag(beta) and a share of W.
+template <int DK, int DV, int HALF>
+__device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Chain& ch,
+                                                 unsigned char* smem, int lane) {
+  using LP = Lds<DK>;
+  constexpr int NH = DK / 64;  // 32-wide d_k blocks of this half
+  const int g = lane >> 4, n16 = lane & 15;
+  const int g2 = lane >> 5, n32 = lane & 31;
+  const u16* kg = static_cast<const u16*>(args.k) + ch.hk * DK + HALF * (DK / 2);
+  u16* fAG = reinterpret_cast<u16*>(smem + LP::O_AG);
+
+  // selectors for K^T over one 32-wide d block: B operand of 16x16x32, lane
+  // (g, n) slot j is 1 where 8g + j == 16h + n with bits 2, 3 swapped
+  bf16x8 esel[2];
+  {
+    const int pn = (n16 & ~12) | ((n16 & 4) << 1) | ((n16 & 8) >> 1);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        esel[h][j] = static_cast<__bf16>((8 * g + j == 16 * h + pn) ? 1.f : 0.f);
+  }
+  uint4 kr[4][NH];
+  auto prefetch = [&](int c) __attribute__((always_inline)) {
+    const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) load_tile16<NH>(kr[t], kg, ch.qk_stride, c0, n, t, lane);
+  };
+  if (ch.nc > 0) prefetch(0);
+
+  for (int it = -2; it < ch.nc; ++it) {
+    const int p = it + 1;
+    const bool active = p >= 0 && p < ch.nc;
+    const int par = p & 1;
+    if (active) {
+      const int n = chunk_len(ch, p);
+      u16* fKt = reinterpret_cast<u16*>(smem + LP::O_KT + par * LP::NKT * LP::FB);
+      if (n < C) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int u = 0; u < NH; ++u) kr[t][u] = mask4(kr[t][u], 16 * t + n16 < n);
+      }
+      // K^T: the 16 x 16 tile (token tile t, rho tile mt) is K times a 0/1
+      // selector; lane (g, n) holds K[16t + 4g + e][true row of rho 16mt + n],
+      // which are slots 4(g/2) .. +3 of lane 32(g%2) + 16(mt%2) + n of the
+      // fragment (rho tile mt/2, token step t)
+#pragma unroll
+      for (int u = 0; u < NH; ++u)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int mt = 2 * (HALF * NH + u) + h;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            const f32x4 x = mma16(as_bf(kr[t][u]), esel[h], zero4());
+            *reinterpret_cast<u16x4*>(fKt + scatter_off((mt >> 1) * 4 + t, mt & 1, lane)) =
+                pack4(x[0], x[1], x[2], x[3]);
+          }
+        }
+      if (p + 1 < ch.nc) prefetch(p + 1);
+    }
+    lds_barrier();
+    if (active) {
+      const u16* ab = reinterpret_cast<const u16*>(smem + LP::O_AB + par * 12 * LP::FB);
+      const float* gb = reinterpret_cast<const float*>(smem + LP::O_G + par * 4 * C * 4);
+      if (ch.need_state) {
+        // (A1 . Gamma) diag(beta) as A fragments (t, s): lane (g2, r) holds
+        // exp(b_r - b_i) A1[r][i] beta_i, r = 32t + r, i = slot; wave 6 the
+        // fragments 0-3, wave 7 the fragments 4, 5
+#pragma unroll
+        for (int f = (HALF == 0) ? 0 : 4; f < ((HALF == 0) ? 4 : 6); ++f) {
+          const int t = (f < 2) ? 0 : 1, s = (f < 2) ? f : f - 2;
+          const int row = 32 * t + n32;
+          const float br = gb[row];
+          const float4 b0 = *reinterpret_cast<const float4*>(gb + 16 * s + 4 * g2);
+          const float4 b1 = *reinterpret_cast<const float4*>(gb + 16 * s + 8 + 4 * g2);
+          const float bi[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+          const bf16x8 h8 = ldf(ab, f, lane), l8 = ldf(ab, 6 + f, lane);
+          bf16x8 o;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            // the fragments hold -A1 diag(beta)
+            const float x = (static_cast<float>(h8[j]) + static_cast<float>(l8[j])) *
+                            -__builtin_amdgcn_exp2f(br - bi[j]);
+            o[j] = static_cast<__bf16>((slot_idx(s, g2, j) <= row) ? x : 0.f);
+          }
+          stf(fAG, f, lane, o);
+        }
+      }
+      emit_w<DK>(ch, smem, lane, par, 1 + HALF);
+    }
+    lds_barrier();
+  }
+}
+
+// =============================================================================
+// waves 0-3: the chain update of chunk c
+// =============================================================================
+template <int DK, int DV>
+__device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch,
+                                           unsigned char* smem, int lane, int col0) {
+  using LP = Lds<DK>;
+  constexpr int NU = DK / 16;
+  constexpr int NM = DK / 32;
+  const int g2 = lane >> 5, n32 = lane & 31;
+  const u16* fWh = reinterpret_cast<const u16*>(smem + LP::O_WH);
+  const u16* fQK = reinterpret_cast<const u16*>(smem + LP::O_QK);
+  const u16* fAG = reinterpret_cast<const u16*>(smem + LP::O_AG);
+  const u16* vg = static_cast<const u16*>(args.v) + ch.h * DV + col0;
+  u16* og = static_cast<u16*>(args.o);
+
+  // state columns col0 .. col0 + 31, all d_k rows (order rho)
+  f32x16 st[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) st[m] = zero16();
+  if (args.mode == 1) {
+    const float* s_in = args.S_in + ch.sh * DK * DV + col0 + n32;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) st[m][e] = s_in[true_row(m, e, g2) * DV];
+  }
+  // identity selector for the V transposes: slot j of step u is 1 where
+  // 16u + 8g2 + j == n
+  bf16x8 isel[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      isel[u][j] = static_cast<__bf16>((16 * u + 8 * g2 + j == n32) ? 1.f : 0.f);
+
+  uint4 vr[2][2];
+  auto prefetch = [&](int c) __attribute__((always_inline)) {
+    const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+    load_tile32<2>(vr[0], vg, ch.v_stride, c0, n, 0, lane);
+    load_tile32<2>(vr[1], vg, ch.v_stride, c0, n, 1, lane);
+  };
+  if (ch.nc > 0) prefetch(0);
+  float log_decay = 0.f;
+
+  for (int it = -2; it < ch.nc; ++it) {
+    const int c = it;
+    const bool active = c >= 0;
+    const int par = c & 1;
+    const float* gb = reinterpret_cast<const float*>(smem + LP::O_G + par * 4 * C * 4);
+    bf16x8 dvn[4];
+    if (active) {
+      const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+      const float* ggam = gb + 2 * C;
+      const float* gdec = gb + 3 * C;
+      const u16* fQ = reinterpret_cast<const u16*>(smem + LP::O_Q + par * LP::NW * LP::FB);
+      // V (this wave's columns) as B fragments over tokens, by exact
+      // products with the identity: lane (g2, n) holds V[slot][col0 + n]
+      bf16x8 vB[4];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const bool keep = n == C || 32 * t + n32 < n;
+        f32x16 acc = mma32(masked(vr[t][0], keep), isel[0], zero16());
+        acc = mma32(masked(vr[t][1], keep), isel[1], acc);
+        vB[2 * t] = frag_of(acc, 0);
+        vB[2 * t + 1] = frag_of(acc, 1);
+      }
+      if (c + 1 < ch.nc) prefetch(c + 1);
+      // U = (A1 . Gamma) diag(beta) V
+      f32x16 vn[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        vn[t] = zero16();
+#pragma unroll
+        for (int s = 0; s < 2 * t + 2; ++s)
+          vn[t] = mma32(ldf(fAG, tri_idx(t, s), lane), vB[s], vn[t]);
+      }
+      // S0 as bf16 operands (step u over rho); shared by W S0 and (Q S0)^T
+      bf16x8 s0[NU];
+#pragma unroll
+      for (int u = 0; u < NU; ++u) s0[u] = frag_of(st[u >> 1], u & 1);
+      // Vn = U - diag(gamma) W S0 (the W fragments hold -W)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        f32x16 ws = zero16();
+#pragma unroll
+        for (int u = 0; u < NU; ++u) ws = mma32(ldf(fWh, t * NU + u, lane), s0[u], ws);
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const float4 gm = *reinterpret_cast<const float4*>(ggam + 32 * t + 8 * b + 4 * g2);
+          vn[t][4 * b] += gm.x * ws[4 * b];
+          vn[t][4 * b + 1] += gm.y * ws[4 * b + 1];
+          vn[t][4 * b + 2] += gm.z * ws[4 * b + 2];
+          vn[t][4 * b + 3] += gm.w * ws[4 * b + 3];
+        }
+      }
+      // O^T = (S0^T Q^T) diag(gamma) + Vn^T (Q K^T . Gamma)^T; lane (g2, n)
+      // holds O[token 32tq + n][col0 + 8b + 4g2 + i]
+      bf16x8 vA[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) vA[s] = frag_of(vn[s >> 1], s & 1);
+      const long orow0 = (args.mode == 0) ? static_cast<long>(c0)
+                                          : static_cast<long>(ch.seg) * args.w + (c0 - ch.lo);
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq) {
+        f32x16 acc = zero16();
+#pragma unroll
+        for (int u = 0; u < NU; ++u) acc = mma32(s0[u], ldf(fQ, tq * NU + u, lane), acc);
+        acc *= ggam[32 * tq + n32];
+#pragma unroll
+        for (int s = 0; s < 2 * tq + 2; ++s)
+          acc = mma32(vA[s], ldf(fQK, tri_idx(tq, s), lane), acc);
+        const int r = 32 * tq + n32;
+        if (og != nullptr && r < n) {
+          u16* dst = og + (orow0 + r) * ch.v_stride + ch.h * DV + col0 + 4 * g2;
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            u16x4 o4;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) o4[i] = bf16_bits(acc[4 * b + i]);
+            *reinterpret_cast<u16x4*>(dst + 8 * b) = o4;
+          }
+        }
+      }
+      // diag(exp(b_last - b)) Vn as B fragments over tokens
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const float4 d0 = *reinterpret_cast<const float4*>(gdec + 16 * s + 4 * g2);
+        const float4 d1 = *reinterpret_cast<const float4*>(gdec + 16 * s + 8 + 4 * g2);
+        const float dv[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+        bf16x8 f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) f[j] = static_cast<__bf16>(vn[s >> 1][8 * (s & 1) + j] * dv[j]);
+        dvn[s] = f;
+      }
+    }
+    lds_barrier();
+    if (active) {
+      const u16* fKt = reinterpret_cast<const u16*>(smem + LP::O_KT + par * LP::NKT * LP::FB);
+      const float b_last = gb[C - 1];  // log2 units
+      log_decay += b_last * 0.693147180559945309f;
+      const float g_last = __builtin_amdgcn_exp2f(b_last);
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        f32x16 acc = st[m] * g_last;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) acc = mma32(ldf(fKt, m * 4 + s, lane), dvn[s], acc);
+        st[m] = acc;
+      }
+    }
+    lds_barrier();
+  }
+
+  if (args.S_out != nullptr) {
+    float* so = args.S_out + ch.sh * DK * DV + col0 + n32;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) so[true_row(m, e, g2) * DV] = st[m][e];
+  }
+  if (args.log_decay != nullptr && ch.cb == 0 && col0 == 0 && lane == 0)
+    args.log_decay[ch.sh] = log_decay;
+}
+
+template <int DK, int DV>
+__device__ __forceinline__ void operator_wave(const ScanArgs& args, const Chain& ch,
+                                              unsigned char* smem, int lane, int col0) {
+  using LP = Lds<DK>;
+  constexpr int NU = DK / 16;
+  constexpr int NM = DK / 32;
+  const int g2 = lane >> 5, n32 = lane & 31;
+  const u16* fWh = reinterpret_cast<const u16*>(smem + LP::O_WH);
+  const u16* fWl = reinterpret_cast<const u16*>(smem + LP::O_WL);
+
+  // operator columns col0 .. col0 + 31, all d_k rows (order rho); P_hat = I
+  f32x16 st[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) st[m][e] = (true_row(m, e, g2) == col0 + n32) ? 1.f : 0.f;
+
+  for (int it = -2; it < ch.nc; ++it) {
+    const int c = it;
+    const bool active = c >= 0;
+    bf16x8 xh[4], xl[4];
+    if (active) {
+      // -X = (-W) P0 in three passes (W hi + lo, P0 hi + lo)
+      bf16x8 ph[NU], pl[NU];
+#pragma unroll
+      for (int u = 0; u < NU; ++u) split_of(st[u >> 1], u & 1, ph[u], pl[u]);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        f32x16 acc = zero16();
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+          const bf16x8 wh = ldf(fWh, t * NU + u, lane);
+          acc = mma32(wh, ph[u], acc);
+          acc = mma32(wh, pl[u], acc);
+          acc = mma32(ldf(fWl, t * NU + u, lane), ph[u], acc);
+        }
+        split_of(acc, 0, xh[2 * t], xl[2 * t]);
+        split_of(acc, 1, xh[2 * t + 1], xl[2 * t + 1]);
+      }
+    }
+    lds_barrier();
+    if (active) {
+      // P <- P0 - K^T X = P0 + K^T (-X) (K exact, X hi + lo)
+      const u16* fKt =
+          reinterpret_cast<const u16*>(smem + LP::O_KT + (c & 1) * LP::NKT * LP::FB);
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        f32x16 acc = st[m];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const bf16x8 a = ldf(fKt, m * 4 + s, lane);
+          acc = mma32(a, xh[s], acc);
+          acc = mma32(a, xl[s], acc);
+        }
+        st[m] = acc;
+      }
+    }
+    lds_barrier();
+  }
+
+  float* po = args.P_hat + ch.sh * DK * DK + col0 + n32;
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) po[true_row(m, e, g2) * DK] = st[m][e];
+}
+
+// every wave of the workgroup runs the same number of iterations and barriers
+template <int DK, int DV>
+__device__ __forceinline__ void idle_wave(const Chain& ch) {
+  for (int it = -2; it < ch.nc; ++it) {
+    lds_barrier();
+    lds_barrier();
+  }
+}
+
+template <int DK, int DV>
+__global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
+  extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int lane = tid & 63;
-  const int g = lane >> 4, ln = lane & 15;
-  const int lane0 = lane, g0 = g, ln0 = ln;  // for the prefetch (outside the chunk loop)
-  // With the operator requested, waves 0-3 carry 64 state columns and waves
-  // 4-7 the same 64 operator columns.  Without it, all 8 waves carry state
-  // columns (128 per workgroup).
-  const bool with_op = args.n_roles == 2;
-  const bool sw = !with_op || wave < 4;  // state wave (else operator wave)
-  const int wq = with_op ? (wave & 3) : wave;  // column tile within the block
-  const int span = with_op ? NCOL : 2 * NCOL;  // state columns per workgroup
 
-  // ---- work item ----------------------------------------------------------
-  const int n_cb = with_op ? ((NP > NS) ? NP : NS) : (DV + span - 1) / span;
+  Chain ch;
+  ch.with_op = args.n_roles == 2;
+  constexpr int NP = DK / NCOL, NS = DV / NCOL;
+  const int n_cb = ch.with_op ? ((NP > NS) ? NP : NS) : (DV + 2 * NCOL - 1) / (2 * NCOL);
   // Workgroups are dealt to the 8 XCDs round-robin; the n_cb column blocks of a
   // chain are numbered so that they land on one XCD back to back and share its
   // L2 for q and k.  Chains past the last full group of 8 keep linear order.
@@ -232,627 +992,55 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     cb = b % n_cb;
   }
   const int rank = chain / args.h_v;
-  const int h = chain % args.h_v;
-  const int col0 = cb * span + wq * 16;  // this wave's 16 columns (of S or P_hat)
-  const bool has_state = cb * span < DV;           // the block holds state columns
-  const bool has_op = with_op && (cb < NP);
-  const bool wave_cols = sw ? (col0 < DV) : has_op;  // does this wave own columns?
-  int seg, lo, hi;
+  ch.h = chain % args.h_v;
+  ch.cb = cb;
+  int lo, hi;
   if (args.mode == 0) {
-    seg = args.order[rank];
-    lo = args.cu_seqlens[seg];
-    hi = args.cu_seqlens[seg + 1];
+    ch.seg = args.order[rank];
+    lo = args.cu_seqlens[ch.seg];
+    hi = args.cu_seqlens[ch.seg + 1];
   } else {
-    seg = rank;
-    lo = args.tok_start[seg];
-    const int len = args.tok_len[seg];
+    ch.seg = rank;
+    lo = args.tok_start[ch.seg];
+    const int len = args.tok_len[ch.seg];
     hi = lo + ((len < args.w) ? len : args.w);
   }
   lo = (lo < 0) ? 0 : ((lo > args.n_tokens) ? args.n_tokens : lo);
   hi = (hi < lo) ? lo : ((hi > args.n_tokens) ? args.n_tokens : hi);
+  ch.lo = lo;
+  ch.hi = hi;
+  ch.nc = (hi - lo + C - 1) / C;
+  ch.hk = ch.h / args.group;
+  ch.sh = static_cast<long>(ch.seg) * args.h_v + ch.h;
+  ch.qk_stride = static_cast<long>(args.h_qk) * DK;
+  ch.v_stride = static_cast<long>(args.h_v) * DV;
+  ch.need_state = ch.with_op ? (cb * NCOL < DV) : true;
+  ch.need_op = ch.with_op && (cb * NCOL < DK);
 
-  const int hk = h / args.group;
-  const u16* kg = static_cast<const u16*>(args.k);
-  const u16* qg = static_cast<const u16*>(args.q);
-  const u16* vg = static_cast<const u16*>(args.v);
-  const long qk_stride = static_cast<long>(args.h_qk) * DK;
-  const long v_stride = static_cast<long>(args.h_v) * DV;
-  const long sh = static_cast<long>(seg) * args.h_v + h;
-
-  // ---- chain state: 16 columns per wave, all d_k rows ------------------------
-  f32x4 st[DT];
-#pragma unroll
-  for (int dt = 0; dt < DT; ++dt) st[dt] = zero4();
-  if (sw) {
-    if (args.mode == 1 && wave_cols) {
-      const float* s_in = args.S_in + sh * DK * DV;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) st[dt][i] = s_in[d_perm(dt, 4 * g + i) * DV + col0 + ln];
+  if (wave < 4) {
+    int col0;
+    bool state_role;
+    if (ch.with_op) {
+      state_role = wave < 2;
+      col0 = cb * NCOL + 32 * (wave & 1);
+    } else {
+      state_role = true;
+      col0 = cb * 2 * NCOL + 32 * wave;
     }
+    if (state_role && col0 < DV)
+      state_wave<DK, DV>(args, ch, smem, lane, col0);
+    else if (!state_role && ch.need_op)
+      operator_wave<DK, DV>(args, ch, smem, lane, col0);
+    else
+      idle_wave<DK, DV>(ch);
+  } else if (wave == 4) {
+    inverse_wave<DK, DV>(args, ch, smem, lane);
+  } else if (wave == 5) {
+    producer_qk_wave<DK, DV>(args, ch, smem, lane);
+  } else if (wave == 6) {
+    producer_kt_wave<DK, DV, 0>(args, ch, smem, lane);
   } else {
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) st[dt][i] = (d_perm(dt, 4 * g + i) == col0 + ln) ? 1.f : 0.f;
-  }
-  float log_decay = 0.f;
-
-  // ---- prefetch of one chunk's tokens into registers -------------------------
-  // Tokens are loaded as matrix-core A-operand fragments straight from HBM:
-  // lane (g, m) of fragment (token tile tt, column block kb) holds the 8
-  // columns kb*32 + 8g .. kb*32 + 8g + 7 of token tt*16 + m (one 16-byte load).
-  // A "pair job" loads the two token tiles 2*kt, 2*kt + 1 of one column block.
-  //   K: pair job (kb, kt) on wave kb + KTD*kt      (waves [0, 2*KTD))
-  //   Q: pair job (kb, kt) on wave 8 - 2*KTD + ...  (waves [8 - 2*KTD, 8))
-  //   V: every state wave loads its own 16 columns, lane (g, m) of token tile tt
-  //      holding columns col0 + 4g .. col0 + 4g + 3 of token tt*16 + m
-  const bool k_job = wave < 2 * KTD;
-  const int kjb = wave % KTD, kjt = wave / KTD;
-  const bool q_job = wave >= 8 - 2 * KTD;
-  const int qjb = (wave - (8 - 2 * KTD)) % KTD, qjt = (wave - (8 - 2 * KTD)) / KTD;
-  const bool v_job = sw && wave_cols;
-  // Raw loads only: every use of the loaded words (the tail mask included)
-  // waits until phase 0 of the next chunk, so the loads stay in flight while
-  // phases 4 and 5 compute.  Element [2t + h] holds half h of token tile 2kt + t.
-  uint4 pk[2], pq[2];
-  uint2 pv[4];
-  bf16x8 vB[KTC];  // state waves: this chunk's V columns as B fragments (phase 0 -> 4)
-  float pa = 0.f, pbeta = 0.f;
-  auto load_pair = [&](uint4 (&dst)[2], const u16* base, long rs, int col, int kt, int c0,
-                       int n) __attribute__((always_inline)) {
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      const int tok = (2 * kt + t) * 16 + ln0;
-      const int tc = (tok < n) ? tok : n - 1;  // clamped (valid) token; zeroed on use
-      dst[t] = *reinterpret_cast<const uint4*>(base + (c0 + tc) * rs + col + 8 * g0);
-    }
-  };
-  auto prefetch = [&](int c0) __attribute__((always_inline)) {
-    const int n = (hi - c0 < C) ? (hi - c0) : C;  // n >= 1
-    if (k_job) load_pair(pk, kg + hk * DK, qk_stride, kjb * 32, kjt, c0, n);
-    if (q_job) load_pair(pq, qg + hk * DK, qk_stride, qjb * 32, qjt, c0, n);
-    if (v_job) {
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt) {
-        const int tok = tt * 16 + ln0;
-        const int tc = (tok < n) ? tok : n - 1;
-        pv[tt] = *reinterpret_cast<const uint2*>(vg + (c0 + tc) * v_stride + h * DV + col0 +
-                                                 4 * g0);
-      }
-    }
-    if (wave == kGateWave) {
-      const int tc = (lane0 < n) ? lane0 : n - 1;
-      const long idx = static_cast<long>(c0 + tc) * args.h_v + h;
-      pa = args.log_alpha[idx];
-      pbeta = args.beta[idx];
-    }
-  };
-
-  // ---- phase 0 of the chunk at c0n into buffer set par: fragments -> LDS
-  //      (lane-contiguous); transposed copies of K and V by exact identity
-  //      products on the matrix cores; gates -------------------------------------
-  auto phase0 = [&](int c0n, int par, int lane, int g, int ln) __attribute__((always_inline)) {
-    const int n = (hi - c0n < C) ? (hi - c0n) : C;
-    u16* fKt = kt_buf(par);
-    float* gb = gate_buf(par);
-    float* gbeta = gb + C;
-    float* ggam = gb + 2 * C;
-    float* gdec = gb + 3 * C;
-  {
-    // selector B operands: slot (g', j') of lane (g', n) holds column
-    // 8g' + j' of the loaded 32-column block, so eye[half] = 1 exactly where
-    // 8g' + j' = d_perm(half, n) and (X eye[half])[m][n] = X[m][d_perm(half, n)]
-    bf16x8 eye[2];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      eye[0][j] = static_cast<__bf16>((g == (ln >> 2) && j == (ln & 3)) ? 1.f : 0.f);
-      eye[1][j] = static_cast<__bf16>((g == (ln >> 2) && j == 4 + (ln & 3)) ? 1.f : 0.f);
-    }
-    // fragment t of a prefetched pair, with tokens past the chunk's end zeroed
-    auto take = [&](const uint4 (&src)[2], int kt, int t) __attribute__((always_inline)) {
-      const uint32_t keep = ((2 * kt + t) * 16 + ln < n) ? 0xffffffffu : 0u;
-      const uint4 w = src[t];
-      return __builtin_bit_cast(bf16x8,
-                                make_uint4(w.x & keep, w.y & keep, w.z & keep, w.w & keep));
-    };
-    auto transpose_pair = [&](bf16x8 f0, bf16x8 f1, u16* dst, int row_tile0, int kt)
-        __attribute__((always_inline)) {
-      // f0, f1: A fragments of token tiles 2kt, 2kt+1 over a 32-column block
-      // whose two 16-column halves become row tiles row_tile0 and row_tile0 + 1
-      // of the token-contraction fragments
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const f32x4 c_lo = mma(f0, eye[half], zero4());
-        const f32x4 c_hi = mma(f1, eye[half], zero4());
-        st_frag(dst, frag_slot(row_tile0 + half, kt, KTC, lane), pack(c_lo, c_hi));
-      }
-    };
-    if (k_job) {
-      const bf16x8 f0 = take(pk, kjt, 0), f1 = take(pk, kjt, 1);
-      st_frag(fKd, frag_slot(2 * kjt, kjb, KTD, lane), f0);
-      st_frag(fKd, frag_slot(2 * kjt + 1, kjb, KTD, lane), f1);
-      transpose_pair(f0, f1, fKt, 2 * kjb, kjt);
-    }
-    if (q_job) {
-      st_frag(fQ, frag_slot(2 * qjt, qjb, KTD, lane), take(pq, qjt, 0));
-      st_frag(fQ, frag_slot(2 * qjt + 1, qjb, KTD, lane), take(pq, qjt, 1));
-    }
-    if (v_job) {
-      // this wave's V columns as token-contraction B fragments, by exact
-      // 16x16x16 identity products: (V_tt I)[m][n] lands in lane (g, n) as
-      // rows 4g .. 4g+3, i.e. tokens along the contraction
-      s16x4 eye16;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) eye16[j] = (4 * g + j == ln) ? short(0x3F80) : short(0);
-      f32x4 vt[4];
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt) {
-        const uint32_t keep = (tt * 16 + ln < n) ? 0xffffffffu : 0u;
-        const uint2 w2 = make_uint2(pv[tt].x & keep, pv[tt].y & keep);
-        vt[tt] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(s16x4, w2),
-                                                           eye16, zero4(), 0, 0, 0);
-      }
-      vB[0] = pack(vt[0], vt[1]);
-      vB[1] = pack(vt[2], vt[3]);
-    }
-  }
-  if (wave == kGateWave) {
-    float b = (lane < n) ? pa : 0.f;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const float u = __shfl_up(b, off, 64);
-      if (lane >= off) b += u;
-    }
-    const float b_last = __shfl(b, 63, 64);
-    gb[lane] = b;
-    gbeta[lane] = (lane < n) ? pbeta : 0.f;
-    ggam[lane] = __expf(b);
-    gdec[lane] = __expf(b_last - b);
-  }
-  };
-
-  if (lo < hi) {
-    prefetch(lo);
-    phase0(lo, 0, lane0, g0, ln0);
-    lds_barrier();
-  }
-
-  for (int c0 = lo; c0 < hi; c0 += C) {
-    const int n = (hi - c0 < C) ? (hi - c0) : C;
-    // an opaque copy of the thread index keeps the compiler from hoisting every
-    // loop-invariant fragment address out of the chunk loop (each would pin a
-    // register for the whole loop); they are cheap to recompute per chunk
-    int tid = threadIdx.x;
-    asm volatile("" : "+v"(tid));
-    const int lane = tid & 63;
-    const int g = lane >> 4, ln = lane & 15;
-    const int par = ((c0 - lo) / C) & 1;  // buffer set of this chunk
-    const u16* fKt = kt_buf(par);
-    const float* gb = gate_buf(par);
-    const float* gbeta = gb + C;
-    const float* ggam = gb + 2 * C;
-    const float* gdec = gb + 3 * C;
-
-    const float b_last = gb[C - 1];
-    log_decay += b_last;
-
-    // ---- phase 1: Gram tiles; diagonal blocks of A1 = (I + L)^{-1}; K Q^T; (Q S0)^T --
-    // Wave 4 forms the four diagonal Gram tiles, gathers column c of G_bb into
-    // lane 16b + c by cross-row lane swaps (no LDS round trip) and inverts all
-    // four blocks at once by unit-lower substitution, one lane per column: the
-    // coefficient L[r][i] reaches every lane of row b by a DPP row broadcast
-    // from lane i.
-    f32x4 kq[3];
-    f32x4 oq[4];
-    float xd[16];  // wave 4, lane 16b + c: column c of the inverse diagonal block b
-    if (wave == 4) {
-      // the inverse is this phase's longest path: its instructions win issue
-      // arbitration until it is done
-      __builtin_amdgcn_s_setprio(2);
-      f32x4 gd[4];  // diagonal Gram tiles; lane (g, n) of tile b holds G_b[4g + i][n]
-#pragma unroll
-      for (int bd = 0; bd < 4; ++bd) {
-        gd[bd] = zero4();
-#pragma unroll
-        for (int kb = 0; kb < KTD; ++kb) {
-          const bf16x8 f = ld_frag(fKd, frag_slot(bd, kb, KTD, lane));
-          gd[bd] = mma(f, f, gd[bd]);
-        }
-      }
-      // exchange (tile b, lane row g) <-> (tile g, lane row b) with two rounds of
-      // row swaps: afterwards lane 16b + c of tile g holds G_b[4g + i][c], so
-      // lane 16b + c has all of column c of G_b
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-#pragma unroll
-        for (int b2 = 0; b2 < 2; ++b2) {  // upper half of tile b2 <-> lower half of b2 + 2
-          const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(gd[b2][i]),
-                                                          __float_as_uint(gd[b2 + 2][i]), false,
-                                                          false);
-          // the two results are copied out one by one before any bit cast
-          const unsigned r0 = r[0], r1 = r[1];
-          gd[b2][i] = __uint_as_float(r0);
-          gd[b2 + 2][i] = __uint_as_float(r1);
-        }
-#pragma unroll
-        for (int b2 = 0; b2 < 4; b2 += 2) {  // odd rows of tile b2 <-> even rows of b2 + 1
-          const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(gd[b2][i]),
-                                                          __float_as_uint(gd[b2 + 1][i]), false,
-                                                          false);
-          const unsigned r0 = r[0], r1 = r[1];
-          gd[b2][i] = __uint_as_float(r0);
-          gd[b2 + 1][i] = __uint_as_float(r1);
-        }
-      }
-      const int ob = (lane >> 4) * 16;
-      float lcol[16];  // -L[r][ln] = -beta_r G[r][ln] of block lane / 16 (used for r > ln)
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        const float4 bb = *reinterpret_cast<const float4*>(gbeta + ob + 4 * q4);
-        lcol[4 * q4] = -bb.x * gd[q4][0];
-        lcol[4 * q4 + 1] = -bb.y * gd[q4][1];
-        lcol[4 * q4 + 2] = -bb.z * gd[q4][2];
-        lcol[4 * q4 + 3] = -bb.w * gd[q4][3];
-      }
-#pragma unroll
-      for (int r = 0; r < 16; ++r) xd[r] = (r == ln) ? 1.f : 0.f;
-      unit_lower_solve_step<0>(xd, lcol);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) Dg[(ob + r) * LDD + ln] = xd[r];
-      __builtin_amdgcn_s_setprio(0);
-    }
-    // off-diagonal Gram tiles (1,0) (2,0) (2,1) (3,0) (3,1) (3,2), all on wave 5,
-    // which loads each K fragment once
-    if (wave == 5) {
-      f32x4 go[6];
-#pragma unroll
-      for (int j = 0; j < 6; ++j) go[j] = zero4();
-#pragma unroll
-      for (int kb = 0; kb < KTD; ++kb) {
-        bf16x8 kf[4];
-#pragma unroll
-        for (int t4 = 0; t4 < 4; ++t4) kf[t4] = ld_frag(fKd, frag_slot(t4, kb, KTD, lane));
-#pragma unroll
-        for (int j = 0; j < 6; ++j) {
-          const int ti = (j < 1) ? 1 : (j < 3) ? 2 : 3;
-          const int tj = (j < 1) ? 0 : (j < 3) ? j - 1 : j - 3;
-          go[j] = mma(kf[ti], kf[tj], go[j]);
-        }
-      }
-#pragma unroll
-      for (int j = 0; j < 6; ++j) {
-        const int ti = (j < 1) ? 1 : (j < 3) ? 2 : 3;
-        const int tj = (j < 1) ? 0 : (j < 3) ? j - 1 : j - 3;
-        // L^T[c][r] = beta_r G[r][c]  (c < r throughout an off-diagonal tile)
-        const int c = tj * 16 + ln;
-        const float4 bb = *reinterpret_cast<const float4*>(gbeta + ti * 16 + 4 * g);
-        *reinterpret_cast<float4*>(Lt + c * LDC + ti * 16 + 4 * g) =
-            make_float4(bb.x * go[j][0], bb.y * go[j][1], bb.z * go[j][2], bb.w * go[j][3]);
-      }
-    }
-    // (Q S0)^T = S0^T Q^T on every state wave (lane (g, n) holds four consecutive
-    // state columns of query token n).  Waves 0-3 also form the K Q^T tiles from
-    // the same Q fragments: wave w the tiles of key tile w, wave 3 also (0, 3).
-    {
-      const bool do_oq = sw && wave_cols;
-      bf16x8 s0h[KTD];
-#pragma unroll
-      for (int kb = 0; kb < KTD; ++kb) s0h[kb] = pack(st[2 * kb], st[2 * kb + 1]);
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) oq[rt] = zero4();
-#pragma unroll
-      for (int sl = 0; sl < 3; ++sl) kq[sl] = zero4();
-#pragma unroll
-      for (int w = 0; w < 5; ++w) {
-        // w < 4: wave w; w == 4: any other state wave
-        if ((w < 4) ? (w != wave) : (wave < 4 || !do_oq)) continue;
-#pragma unroll
-        for (int kb = 0; kb < KTD; ++kb) {
-          bf16x8 qf[4];
-#pragma unroll
-          for (int rt = 0; rt < 4; ++rt) qf[rt] = ld_frag(fQ, frag_slot(rt, kb, KTD, lane));
-          if (do_oq) {
-#pragma unroll
-            for (int rt = 0; rt < 4; ++rt) oq[rt] = mma(s0h[kb], qf[rt], oq[rt]);
-          }
-          if (w < 4) {
-            const bf16x8 ka = ld_frag(fKd, frag_slot(w, kb, KTD, lane));
-#pragma unroll
-            for (int sl = 0; sl < 3; ++sl)
-              if (w + sl < 4) kq[sl] = mma(ka, qf[w + sl], kq[sl]);
-            if (w == 3) kq[1] = mma(ld_frag(fKd, frag_slot(0, kb, KTD, lane)), qf[3], kq[1]);
-          }
-        }
-      }
-    }
-    // (Q K^T . Gamma) as A-operand fragments over key tokens for query rows
-#pragma unroll
-    for (int t = 0; t < 10; ++t) {
-      if (kq_owner(t) != wave) continue;
-      const int tr = tri_row(t), ti = tri_col(t);
-      const int r = tr * 16 + ln;
-      const float br = gb[r];
-      const f32x4 a = kq[kq_slot(t)];
-      u16x4 val;
-#pragma unroll
-      for (int i4 = 0; i4 < 4; ++i4) {
-        const int i = ti * 16 + 4 * g + i4;
-        val[i4] = bf16_of((i <= r) ? a[i4] * __expf(br - gb[i]) : 0.f);
-      }
-      *reinterpret_cast<u16x4*>(fQK + frag_slot(tr, ti >> 1, KTC, lane) + (ti & 1) * 4) = val;
-    }
-    // zero halves (key tile > query tile): (1,0) (2,0) (3,0) (2,1) (3,1) (3,2)
-#pragma unroll
-    for (int t = 0; t < 6; ++t) {
-      if (((t < 4) ? t : t + 1) != wave) continue;  // waves 0-3, 5, 6
-      const int ti = (t < 3) ? t + 1 : ((t == 5) ? 3 : t - 1);
-      const int tr = (t < 3) ? 0 : ((t == 5) ? 2 : 1);
-      *reinterpret_cast<uint2*>(fQK + frag_slot(tr, ti >> 1, KTC, lane) + (ti & 1) * 4) =
-          make_uint2(0u, 0u);
-    }
-    // The next chunk's tokens load while this chunk computes.  Issuing the loads
-    // keeps the CU's load path busy for ~1.5k cycles, so they are issued where
-    // the waves would otherwise wait: waves 0-2 here, waves 3-7 (idle while
-    // the off-diagonal blocks of A1 are merged) once the merges begin.
-    if (wave < 3 && c0 + C < hi) prefetch(c0 + C);
-    lds_barrier();
-
-    // ---- phase 2: the rest of A1 -------------------------------------------------------
-    // (a) the diagonal blocks move from their staging copy into A1 and A1^T
-    if (wave == 4) {
-      const int o = (lane >> 4) * 16;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) A1[(o + r) * LDC + o + ln] = xd[r];
-      float4* tp = reinterpret_cast<float4*>(A1t + (o + ln) * LDC + o);
-#pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4)
-        tp[q4] = make_float4(xd[4 * q4], xd[4 * q4 + 1], xd[4 * q4 + 2], xd[4 * q4 + 3]);
-    }
-    // (b) N_ik = A_ii L_ik for i > k, written row-major into the unused
-    //     lower-left block positions (i, k) of the L^T storage
-#pragma unroll
-    for (int p = 0; p < 6; ++p) {
-      if (p != wave) continue;
-      // pairs (1,0) (2,1) (3,2) (2,0) (3,1) (3,0)
-      const int bi = 16 * ((p < 3) ? p + 1 : ((p == 5) ? 3 : p - 1));
-      const int bk = 16 * ((p < 3) ? p : ((p == 4) ? 1 : 0));
-      const float4 a = *reinterpret_cast<const float4*>(Dg + (bi + ln) * LDD + 4 * g);
-      const float4 b = *reinterpret_cast<const float4*>(Lt + (bk + ln) * LDC + bi + 4 * g);
-      const f32x4 acc = mma16_f32(a, b, zero4());
-#pragma unroll
-      for (int i = 0; i < 4; ++i) Lt[(bi + 4 * g + i) * LDC + bk + ln] = acc[i];
-    }
-    lds_barrier();
-    // (c)-(e) A_ij = -sum_{k=j}^{i-1} N_ik A_kj, one block diagonal at a time
-    if (wave >= 3 && c0 + C < hi) prefetch(c0 + C);
-#pragma unroll
-    for (int dist = 1; dist < 4; ++dist) {
-#pragma unroll
-      for (int bj = 0; bj < 4 - dist; ++bj) {
-        if (bj != wave) continue;
-        const int bi = bj + dist;
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int bk = bj; bk < bi; ++bk) {
-          const float4 a =
-              *reinterpret_cast<const float4*>(Lt + (bi * 16 + ln) * LDC + bk * 16 + 4 * g);
-          const float4 b =
-              *reinterpret_cast<const float4*>(A1t + (bj * 16 + ln) * LDC + bk * 16 + 4 * g);
-          acc = mma16_f32(a, b, acc);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) A1[(bi * 16 + 4 * g + i) * LDC + bj * 16 + ln] = -acc[i];
-        *reinterpret_cast<float4*>(A1t + (bj * 16 + ln) * LDC + bi * 16 + 4 * g) =
-            make_float4(-acc[0], -acc[1], -acc[2], -acc[3]);
-      }
-      lds_barrier();
-    }
-
-    // ---- phase 3: fragments of A1 diag(beta) (hi, lo), (A1 . Gamma) diag(beta) and
-    //               (Q K^T . Gamma) -------------------------------------------------------
-    {
-      // 512 slots of a 64 x 64 fragment matrix, one per thread
-      const int s = tid;
-      const int sl = s & 63, tile = s >> 6;
-      const int rt = tile / KTC, kt = tile % KTC;
-      const int sg = sl >> 4, r = rt * 16 + (sl & 15);
-      const int k0 = kt * 32 + 4 * sg;
-      const float4 a0 = *reinterpret_cast<const float4*>(A1 + r * LDC + k0);
-      const float4 a1 = *reinterpret_cast<const float4*>(A1 + r * LDC + k0 + 16);
-      const float4 b0 = *reinterpret_cast<const float4*>(gbeta + k0);
-      const float4 b1 = *reinterpret_cast<const float4*>(gbeta + k0 + 16);
-      const float4 e0 = *reinterpret_cast<const float4*>(gb + k0);
-      const float4 e1 = *reinterpret_cast<const float4*>(gb + k0 + 16);
-      const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-      const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-      const float ev[8] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
-      const float br = gb[r];
-      bf16x8 hh, ll, gg;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int i = k0 + ((j < 4) ? j : 12 + j);
-        const bool keep = (i <= r);
-        const float ab = keep ? av[j] * bv[j] : 0.f;
-        hh[j] = static_cast<__bf16>(ab);
-        ll[j] = static_cast<__bf16>(ab - static_cast<float>(hh[j]));
-        gg[j] = static_cast<__bf16>(keep ? ab * __expf(br - ev[j]) : 0.f);
-      }
-      st_frag(fAbh, s * 8, hh);
-      st_frag(fAbl, s * 8, ll);
-      st_frag(fAgb, s * 8, gg);
-    }
-    lds_barrier();
-
-    // ---- phase 4: W^T tiles -> fragments (gamma W, W hi, W lo); U ---------------------
-    // wave (rt, dg): query-token tile rt = wave % 4, d_k tiles 4*dg .. 4*dg + 3; the
-    // A1 diag(beta) fragments of tile rt are loaded once for all four products
-    {
-      constexpr int NG = DT / 4;  // groups of four d_k tiles
-      if (wave < 4 * NG) {
-        const int rt = wave & 3, dg = wave >> 2;
-        bf16x8 ah[KTC], al[KTC];
-#pragma unroll
-        for (int kt = 0; kt < KTC; ++kt) {
-          ah[kt] = ld_frag(fAbh, frag_slot(rt, kt, KTC, lane));
-          al[kt] = ld_frag(fAbl, frag_slot(rt, kt, KTC, lane));
-        }
-        f32x4 w4[4];
-#pragma unroll
-        for (int d = 0; d < 4; ++d) {
-          f32x4 acc = zero4();
-#pragma unroll
-          for (int kt = 0; kt < KTC; ++kt) {
-            const bf16x8 a = ld_frag(fKt, frag_slot(4 * dg + d, kt, KTC, lane));
-            acc = mma(a, ah[kt], acc);
-            acc = mma(a, al[kt], acc);
-          }
-          w4[d] = acc;
-        }
-        const float gam = ggam[rt * 16 + ln];
-#pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          const int kb = 2 * dg + p;
-          bf16x8 hh, ll;
-          pack_split(w4[2 * p], w4[2 * p + 1], hh, ll);
-          st_frag(fWh, frag_slot(rt, kb, KTD, lane), hh);
-          st_frag(fWl, frag_slot(rt, kb, KTD, lane), ll);
-          st_frag(fWs, frag_slot(rt, kb, KTD, lane), pack(w4[2 * p] * gam, w4[2 * p + 1] * gam));
-        }
-      }
-    }
-    f32x4 u[4];
-    if (sw && wave_cols) {
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int kt = 0; kt < KTC; ++kt)
-          acc = mma(ld_frag(fAgb, frag_slot(rt, kt, KTC, lane)),
-                    vB[kt], acc);
-        u[rt] = acc;
-      }
-    }
-    lds_barrier();
-
-    // ---- phase 5: chain update -----------------------------------------------------------
-    if (sw && wave_cols) {
-      bf16x8 s0h[KTD];
-#pragma unroll
-      for (int kb = 0; kb < KTD; ++kb) s0h[kb] = pack(st[2 * kb], st[2 * kb + 1]);
-      // Vn = U - W' S0
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int kb = 0; kb < KTD; ++kb)
-          acc = mma(ld_frag(fWs, frag_slot(rt, kb, KTD, lane)), s0h[kb], acc);
-        u[rt] -= acc;
-      }
-      bf16x8 vnf[KTC];
-#pragma unroll
-      for (int kt = 0; kt < KTC; ++kt) vnf[kt] = pack(u[2 * kt], u[2 * kt + 1]);
-      // O^T = (Q S0)^T diag(gamma) + Vn^T (Q K^T . Gamma)^T; lane (g, n) holds
-      // O[token rt*16 + n][col0 + 4g .. col0 + 4g + 3]
-      u16* og = static_cast<u16*>(args.o);
-      const long orow0 = (args.mode == 0) ? static_cast<long>(c0)
-                                          : static_cast<long>(seg) * args.w + (c0 - lo);
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        f32x4 acc = oq[rt] * ggam[rt * 16 + ln];
-#pragma unroll
-        for (int kt = 0; kt < KTC; ++kt)
-          if (2 * kt <= rt) acc = mma(vnf[kt], ld_frag(fQK, frag_slot(rt, kt, KTC, lane)), acc);
-        const int r = rt * 16 + ln;
-        if (og != nullptr && r < n) {
-          u16x4 o4;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) o4[i] = bf16_of(acc[i]);
-          *reinterpret_cast<u16x4*>(og + (orow0 + r) * v_stride + h * DV + col0 + 4 * g) = o4;
-        }
-      }
-      // S <- gamma_last S0 + K^T diag(exp(b_last - b)) Vn
-#pragma unroll
-      for (int kt = 0; kt < KTC; ++kt) {
-        const float4 d0 = *reinterpret_cast<const float4*>(gdec + kt * 32 + 4 * g);
-        const float4 d1 = *reinterpret_cast<const float4*>(gdec + kt * 32 + 16 + 4 * g);
-        f32x4 x0 = u[2 * kt], x1 = u[2 * kt + 1];
-        x0[0] *= d0.x;
-        x0[1] *= d0.y;
-        x0[2] *= d0.z;
-        x0[3] *= d0.w;
-        x1[0] *= d1.x;
-        x1[1] *= d1.y;
-        x1[2] *= d1.z;
-        x1[3] *= d1.w;
-        vnf[kt] = pack(x0, x1);
-      }
-      const float g_last = __expf(b_last);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        f32x4 acc = st[dt] * g_last;
-#pragma unroll
-        for (int kt = 0; kt < KTC; ++kt)
-          acc = mma(ld_frag(fKt, frag_slot(dt, kt, KTC, lane)), vnf[kt], acc);
-        st[dt] = acc;
-      }
-    } else if (!sw && has_op) {
-      // X = W P0 (three passes);  P <- P0 - K^T X (two passes, K exact)
-      bf16x8 p0h[KTD], p0l[KTD];
-#pragma unroll
-      for (int kb = 0; kb < KTD; ++kb) pack_split(st[2 * kb], st[2 * kb + 1], p0h[kb], p0l[kb]);
-      f32x4 x[4];
-#pragma unroll
-      for (int rt = 0; rt < 4; ++rt) {
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int kb = 0; kb < KTD; ++kb) {
-          const bf16x8 wh = ld_frag(fWh, frag_slot(rt, kb, KTD, lane));
-          const bf16x8 wl = ld_frag(fWl, frag_slot(rt, kb, KTD, lane));
-          acc = mma(wh, p0h[kb], acc);
-          acc = mma(wh, p0l[kb], acc);
-          acc = mma(wl, p0h[kb], acc);
-        }
-        x[rt] = -acc;
-      }
-      bf16x8 xh[KTC], xl[KTC];
-#pragma unroll
-      for (int kt = 0; kt < KTC; ++kt) pack_split(x[2 * kt], x[2 * kt + 1], xh[kt], xl[kt]);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        f32x4 acc = st[dt];
-#pragma unroll
-        for (int kt = 0; kt < KTC; ++kt) {
-          const bf16x8 a = ld_frag(fKt, frag_slot(dt, kt, KTC, lane));
-          acc = mma(a, xh[kt], acc);
-          acc = mma(a, xl[kt], acc);
-        }
-        st[dt] = acc;
-      }
-    }
-    // phase 0 of the next chunk shares this interval with the update above
-    if (c0 + C < hi) phase0(c0 + C, par ^ 1, lane, g, ln);
-    lds_barrier();
-  }
-
-  // ---- results ------------------------------------------------------------------------
-  if (!wave_cols) return;
-  if (sw) {
-    if (args.S_out != nullptr) {
-      float* so = args.S_out + sh * DK * DV;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) so[d_perm(dt, 4 * g + i) * DV + col0 + ln] = st[dt][i];
-    }
-    if (args.log_decay != nullptr && cb == 0 && tid == 0) args.log_decay[sh] = log_decay;
-  } else {
-    float* po = args.P_hat + sh * DK * DK;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) po[d_perm(dt, 4 * g + i) * DK + col0 + ln] = st[dt][i];
+    producer_kt_wave<DK, DV, 1>(args, ch, smem, lane);
   }
 }
 
