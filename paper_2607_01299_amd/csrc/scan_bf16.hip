@@ -21,16 +21,17 @@
 //   waves 0-1  state columns (32 each): U, Vn, outputs, S update for chunk c;
 //   waves 2-3  operator columns (32 each): X = W P0, P update for chunk c
 //              (without the operator they carry state columns too);
+//              after their update, waves 0-3 form W (hi + lo) of chunk c + 1,
+//              one 32-row d_k block each;
 //   wave 4     inverse of chunk c + 2: Gram matrix, the four diagonal 16 x 16
 //              blocks of A1 by column-parallel substitution (DPP row
-//              broadcasts), the off-diagonal blocks by split-bf16 products
-//              (three passes), all in registers; blocks are transposed by
-//              products with the identity and written straight into the
-//              split bf16 fragments of A1 diag(beta);
+//              broadcasts), the off-diagonal blocks of -A1 diag(beta) by
+//              split-bf16 products (three passes), all in registers, written
+//              as float32 matrix-core fragments;
 //   waves 5-7  chunk c + 1: gates, K Q^T masked with Gamma and the Q
-//              fragments (wave 5, which loads K and Q once per workgroup),
-//              K^T (waves 6, 7: one d_k half each), W (hi + lo) and
-//              (A1 . Gamma) diag(beta) as matrix-core fragments.
+//              fragments (wave 5, which loads K and Q once per workgroup);
+//              K^T, -A1 diag(beta) split into bf16 hi + lo, and
+//              (A1 . Gamma) diag(beta) (waves 6, 7: one half each).
 // Each iteration has two LDS-only barriers: the consumers' state-independent
 // products read the previous iteration's fragments before the first, their
 // K^T products follow it; the producers write K^T, Q and gates for c + 1
@@ -193,8 +194,10 @@ struct Lds {
   static constexpr int O_Q = O_WL + NW * FB;           // Q, two buffers
   static constexpr int O_QK = O_Q + 2 * NW * FB;       // (Q K^T . Gamma)^T, 6 fragments
   static constexpr int O_AG = O_QK + 6 * FB;           // (A1 . Gamma) diag(beta), 6 fragments
-  static constexpr int O_AB = O_AG + 6 * FB;           // A1 diag(beta) hi + lo, two buffers
-  static constexpr int O_G = O_AB + 2 * 12 * FB;       // gates b, beta, gamma, dec; two buffers
+  static constexpr int O_AB = O_AG + 6 * FB;           // -A1 diag(beta) as bf16 hi + lo
+  static constexpr int O_AF = O_AB + 12 * FB;          // -A1 diag(beta) in float32, two buffers
+  static constexpr int AFB = 6 * 2 * FB;               // bytes of one float32 buffer
+  static constexpr int O_G = O_AF + 2 * AFB;           // gates b, beta, gamma, dec; two buffers
   static constexpr int O_BS = O_G + 2 * 4 * C * 4;     // inverse wave: beta
   static constexpr int TOTAL = O_BS + C * 4;
   static_assert(TOTAL <= 160 * 1024, "LDS budget");
@@ -277,27 +280,15 @@ __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& 
 #pragma unroll
   for (int j = 0; j < 4; ++j) eye[j] = (4 * g + j == n16) ? short(0x3F80) : short(0);
 
-  // Row-form block (i, jb) of A1 (lane (g, n): A1[16i + n][16jb + 4g + e]),
-  // scaled by -beta of the column and split hi + lo, into the fragments (t, s)
-  // of -A1 diag(beta) (stored negated, so W comes out negated and the
-  // operator path needs no sign flip): lane (g2, r) of fragment (t, s) holds
-  // columns 16s + 8(j/4) + 4g2 + j%4 of row 32t + r, so this lane's four
-  // values are slots 4(g/2) .. +3 of lane 32(g%2) + 16(i%2) + n of fragment
-  // (i/2, jb).
-  auto emit = [&](u16* ab, int i, int jb, const f32x4& x, bool zero) __attribute__((always_inline)) {
-    float4 bb = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (!zero) bb = *reinterpret_cast<const float4*>(bs + 16 * jb + 4 * g);
-    const float v[4] = {-x[0] * bb.x, -x[1] * bb.y, -x[2] * bb.z, -x[3] * bb.w};
-    u16x4 hi, lo;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const __bf16 h = static_cast<__bf16>(v[e]);
-      hi[e] = __builtin_bit_cast(u16, h);
-      lo[e] = bf16_bits(v[e] - static_cast<float>(h));
-    }
-    const int off = tri_idx(i >> 1, jb) * FR + (32 * (g & 1) + 16 * (i & 1) + n16) * 8 + 4 * (g >> 1);
-    *reinterpret_cast<u16x4*>(ab + off) = hi;
-    *reinterpret_cast<u16x4*>(ab + 6 * FR + off) = lo;
+  // Row-form block (i, jb) of -A1 diag(beta) (lane (g, n): row 16i + n,
+  // columns 16jb + 4g + e) into the float32 fragments (t, s) of -A1 diag(beta):
+  // lane (g2, r) of fragment (t, s) holds columns 16s + 8(j/4) + 4g2 + j%4 of
+  // row 32t + r, so this lane's four values are slots 4(g/2) .. +3 of lane
+  // 32(g%2) + 16(i%2) + n of fragment (i/2, jb).
+  auto emit = [&](float* af, int i, int jb, const f32x4& x) __attribute__((always_inline)) {
+    const int lane_f = 32 * (g & 1) + 16 * (i & 1) + n16;
+    *reinterpret_cast<float4*>(af + (tri_idx(i >> 1, jb) * 64 + lane_f) * 8 + 4 * (g >> 1)) =
+        make_float4(x[0], x[1], x[2], x[3]);
   };
 
   // 16x16x32 A fragments of K: lane (g, r) holds K[16t + r][32u + 8g .. +7]
@@ -321,9 +312,9 @@ __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& 
   // stay zero (per chunk only blocks on or below the diagonal are written).
 #pragma unroll
   for (int par = 0; par < 2; ++par) {
-    u16* ab = reinterpret_cast<u16*>(smem + LP::O_AB + par * 12 * LP::FB);
-    emit(ab, 0, 1, zero4(), true);
-    emit(ab, 2, 3, zero4(), true);
+    float* af = reinterpret_cast<float*>(smem + LP::O_AF + par * LP::AFB);
+    emit(af, 0, 1, zero4());
+    emit(af, 2, 3, zero4());
   }
 
   for (int it = -2; it < ch.nc; ++it) {
@@ -387,7 +378,7 @@ __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& 
     }
     lds_barrier();
     if (active) {
-      u16* ab = reinterpret_cast<u16*>(smem + LP::O_AB + (c & 1) * 12 * LP::FB);
+      float* af = reinterpret_cast<float*>(smem + LP::O_AF + (c & 1) * LP::AFB);
       // L_ik as A operand: lane (g, r): beta_{16i + r} G[16i + r][16k + 4g + s];
       // every operand is split into bf16 hi + lo once
       auto Lr = [&](int i, int k) __attribute__((always_inline)) {
@@ -396,30 +387,39 @@ __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& 
       };
       const Split4 L10 = Lr(1, 0), L20 = Lr(2, 0), L21 = Lr(2, 1);
       const Split4 L30 = Lr(3, 0), L31 = Lr(3, 1), L32 = Lr(3, 2);
-      const Split4 D0 = split4(dc[0]), D1 = split4(dc[1]), D2 = split4(dc[2]);
+      // Y = -A1 diag(beta) block by block: Y_jj = D_j diag(-beta_j),
+      // Y_ij = -D_i sum_{k=j}^{i-1} L_ik Y_kj (the column scaling commutes
+      // with the recursion)
+      f32x4 yd[3];
+#pragma unroll
+      for (int j = 0; j < 3; ++j) yd[j] = dc[j] * -bs[16 * j + n16];
+      const Split4 Y0 = split4(yd[0]), Y1 = split4(yd[1]), Y2 = split4(yd[2]);
       const Split4 R1 = split4(dr[1]), R2 = split4(dr[2]), R3 = split4(dr[3]);
-      // A_ij = -D_i sum_{k=j}^{i-1} L_ik A_kj, one block column at a time
-      const f32x4 A10 = -mma16_x3(R1, split4(mma16_x3(L10, D0, zero4())), zero4());
-      const f32x4 A21 = -mma16_x3(R2, split4(mma16_x3(L21, D1, zero4())), zero4());
-      const f32x4 A32 = -mma16_x3(R3, split4(mma16_x3(L32, D2, zero4())), zero4());
-      const Split4 S10 = split4(A10), S21 = split4(A21);
-      const f32x4 A20 =
-          -mma16_x3(R2, split4(mma16_x3(L21, S10, mma16_x3(L20, D0, zero4()))), zero4());
-      const f32x4 A31 =
-          -mma16_x3(R3, split4(mma16_x3(L32, S21, mma16_x3(L31, D1, zero4()))), zero4());
-      const Split4 S20 = split4(A20);
-      const f32x4 A30 = -mma16_x3(
-          R3, split4(mma16_x3(L32, S20, mma16_x3(L31, S10, mma16_x3(L30, D0, zero4())))),
-          zero4());
+      // T_ij = sum_k L_ik Y_kj; Y_ij = -D_i T_ij in accumulator form where a later
+      // product needs it, and its row form -T_ij^T D_i^T (T as the A operand is
+      // T^T, the row form of D_i as the B operand is D_i^T) for the fragments
+      const Split4 T10 = split4(mma16_x3(L10, Y0, zero4()));
+      const Split4 T21 = split4(mma16_x3(L21, Y1, zero4()));
+      const Split4 T32 = split4(mma16_x3(L32, Y2, zero4()));
+      const Split4 Y10 = split4(-mma16_x3(R1, T10, zero4()));
+      const Split4 Y21 = split4(-mma16_x3(R2, T21, zero4()));
+      const Split4 T20 = split4(mma16_x3(L21, Y10, mma16_x3(L20, Y0, zero4())));
+      const Split4 T31 = split4(mma16_x3(L32, Y21, mma16_x3(L31, Y1, zero4())));
+      const Split4 Y20 = split4(-mma16_x3(R2, T20, zero4()));
+      const Split4 T30 =
+          split4(mma16_x3(L32, Y20, mma16_x3(L31, Y10, mma16_x3(L30, Y0, zero4()))));
       // every block on or below the diagonal, in row form, into the fragments
 #pragma unroll
-      for (int bd = 0; bd < 4; ++bd) emit(ab, bd, bd, dr[bd], false);
-      emit(ab, 1, 0, transpose16(S10, eye), false);
-      emit(ab, 2, 1, transpose16(S21, eye), false);
-      emit(ab, 3, 2, transpose16(split4(A32), eye), false);
-      emit(ab, 2, 0, transpose16(S20, eye), false);
-      emit(ab, 3, 1, transpose16(split4(A31), eye), false);
-      emit(ab, 3, 0, transpose16(split4(A30), eye), false);
+      for (int bd = 0; bd < 4; ++bd) {
+        const float4 bb = *reinterpret_cast<const float4*>(bs + 16 * bd + 4 * g);
+        emit(af, bd, bd, dr[bd] * f32x4{-bb.x, -bb.y, -bb.z, -bb.w});
+      }
+      emit(af, 1, 0, -mma16_x3(T10, R1, zero4()));
+      emit(af, 2, 1, -mma16_x3(T21, R2, zero4()));
+      emit(af, 3, 2, -mma16_x3(T32, R3, zero4()));
+      emit(af, 2, 0, -mma16_x3(T20, R2, zero4()));
+      emit(af, 3, 1, -mma16_x3(T31, R3, zero4()));
+      emit(af, 3, 0, -mma16_x3(T30, R3, zero4()));
     }
     lds_barrier();
   }
@@ -431,48 +431,37 @@ __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& 
 // W^T tiles (rho tile m, token tile t) = K^T (A1 diag beta)^T in two passes,
 // from the negated A1 diag(beta) fragments, so the tiles hold -W^T; the
 // accumulator halves are the fragments (t, u = 2m + h) of -W, kept as hi + lo.
-// Owners (wave 5, 6, 7 = 0, 1, 2) spread the tiles by cost (t = 1 costs twice
-// t = 0).
-template <int DK>
-__device__ __forceinline__ int wt_owner(int m, int t) {
-  if constexpr (DK == 128) {
-    constexpr int tab[4][2] = {{0, 1}, {0, 1}, {1, 2}, {2, 2}};
-    return tab[m][t];
-  } else {
-    constexpr int tab[2][2] = {{0, 1}, {1, 2}};
-    return tab[m][t];
-  }
-}
+// Formed after the first barrier of iteration c for chunk c + 1 by the waves
+// that share SIMDs 2 and 3 (the least loaded after that barrier): waves 2, 6,
+// 3, 7 take rho tiles 0, 1, 2, 3.
+// rho tile of W formed by consumer slot w (waves 0-3), or -1
+__device__ __forceinline__ int w_tile(int w) { return (w == 2) ? 0 : ((w == 3) ? 2 : -1); }
 
 template <int DK>
 __device__ __forceinline__ void emit_w(const Chain& ch, unsigned char* smem, int lane, int par,
-                                       int pw) {
+                                       int m) {
   using LP = Lds<DK>;
   constexpr int NU = DK / 16;
-  constexpr int NM = DK / 32;
+  if (m < 0 || m >= DK / 32) return;
   const u16* fKt = reinterpret_cast<const u16*>(smem + LP::O_KT + par * LP::NKT * LP::FB);
-  const u16* ab = reinterpret_cast<const u16*>(smem + LP::O_AB + par * 12 * LP::FB);
+  const u16* ab = reinterpret_cast<const u16*>(smem + LP::O_AB);
   u16* fWh = reinterpret_cast<u16*>(smem + LP::O_WH);
   u16* fWl = reinterpret_cast<u16*>(smem + LP::O_WL);
 #pragma unroll
-  for (int m = 0; m < NM; ++m) {
+  for (int t = 0; t < 2; ++t) {
+    f32x16 acc = zero16();
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      if (wt_owner<DK>(m, t) != pw) continue;
-      f32x16 acc = zero16();
+    for (int s = 0; s < 2 * t + 2; ++s) {
+      const bf16x8 a = ldf(fKt, m * 4 + s, lane);
+      acc = mma32(a, ldf(ab, tri_idx(t, s), lane), acc);
+      acc = mma32(a, ldf(ab, 6 + tri_idx(t, s), lane), acc);
+    }
 #pragma unroll
-      for (int s = 0; s < 2 * t + 2; ++s) {
-        const bf16x8 a = ldf(fKt, m * 4 + s, lane);
-        acc = mma32(a, ldf(ab, tri_idx(t, s), lane), acc);
-        acc = mma32(a, ldf(ab, 6 + tri_idx(t, s), lane), acc);
-      }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        bf16x8 hi, lo;
-        split_of(acc, h, hi, lo);
-        stf(fWh, t * NU + 2 * m + h, lane, hi);
-        if (ch.need_op) stf(fWl, t * NU + 2 * m + h, lane, lo);
-      }
+    for (int h = 0; h < 2; ++h) {
+      bf16x8 hi, lo;
+      split_of(acc, h, hi, lo);
+      stf(fWh, t * NU + 2 * m + h, lane, hi);
+      if (ch.need_op) stf(fWl, t * NU + 2 * m + h, lane, lo);
     }
   }
 }
@@ -623,7 +612,6 @@ __device__ __forceinline__ void producer_qk_wave(const ScanArgs& args, const Cha
           }
         }
       }
-      emit_w<DK>(ch, smem, lane, par, 0);
     }
     lds_barrier();
   }
@@ -689,11 +677,29 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
                 pack4(x[0], x[1], x[2], x[3]);
           }
         }
+      {
+        // -A1 diag(beta) of this chunk as bf16 hi + lo fragments for W: wave 6
+        // the fragments 0-3, wave 7 the fragments 4, 5
+        const float* af = reinterpret_cast<const float*>(smem + LP::O_AF + par * LP::AFB);
+        u16* ab = reinterpret_cast<u16*>(smem + LP::O_AB);
+#pragma unroll
+        for (int f = (HALF == 0) ? 0 : 4; f < ((HALF == 0) ? 4 : 6); ++f) {
+          const float4 v0 = *reinterpret_cast<const float4*>(af + (f * 64 + lane) * 8);
+          const float4 v1 = *reinterpret_cast<const float4*>(af + (f * 64 + lane) * 8 + 4);
+          f32x16 x;
+          x[0] = v0.x; x[1] = v0.y; x[2] = v0.z; x[3] = v0.w;
+          x[4] = v1.x; x[5] = v1.y; x[6] = v1.z; x[7] = v1.w;
+          bf16x8 hi, lo;
+          split_of(x, 0, hi, lo);
+          stf(ab, f, lane, hi);
+          stf(ab, 6 + f, lane, lo);
+        }
+      }
       if (p + 1 < ch.nc) prefetch(p + 1);
     }
     lds_barrier();
     if (active) {
-      const u16* ab = reinterpret_cast<const u16*>(smem + LP::O_AB + par * 12 * LP::FB);
+      const float* af = reinterpret_cast<const float*>(smem + LP::O_AF + par * LP::AFB);
       const float* gb = reinterpret_cast<const float*>(smem + LP::O_G + par * 4 * C * 4);
       if (ch.need_state) {
         // (A1 . Gamma) diag(beta) as A fragments (t, s): lane (g2, r) holds
@@ -707,19 +713,20 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
           const float4 b0 = *reinterpret_cast<const float4*>(gb + 16 * s + 4 * g2);
           const float4 b1 = *reinterpret_cast<const float4*>(gb + 16 * s + 8 + 4 * g2);
           const float bi[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-          const bf16x8 h8 = ldf(ab, f, lane), l8 = ldf(ab, 6 + f, lane);
+          const float4 v0 = *reinterpret_cast<const float4*>(af + (f * 64 + lane) * 8);
+          const float4 v1 = *reinterpret_cast<const float4*>(af + (f * 64 + lane) * 8 + 4);
+          const float av[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
           bf16x8 o;
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
             // the fragments hold -A1 diag(beta)
-            const float x = (static_cast<float>(h8[j]) + static_cast<float>(l8[j])) *
-                            -__builtin_amdgcn_exp2f(br - bi[j]);
+            const float x = av[j] * -__builtin_amdgcn_exp2f(br - bi[j]);
             o[j] = static_cast<__bf16>((slot_idx(s, g2, j) <= row) ? x : 0.f);
           }
           stf(fAG, f, lane, o);
         }
       }
-      emit_w<DK>(ch, smem, lane, par, 1 + HALF);
+      emit_w<DK>(ch, smem, lane, par, 1 + 2 * HALF);
     }
     lds_barrier();
   }
@@ -730,7 +737,7 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
 // =============================================================================
 template <int DK, int DV>
 __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch,
-                                           unsigned char* smem, int lane, int col0) {
+                                           unsigned char* smem, int lane, int col0, int wslot) {
   using LP = Lds<DK>;
   constexpr int NU = DK / 16;
   constexpr int NM = DK / 32;
@@ -875,6 +882,7 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
         st[m] = acc;
       }
     }
+    if (it + 1 >= 0 && it + 1 < ch.nc) emit_w<DK>(ch, smem, lane, (it + 1) & 1, w_tile(wslot));
     lds_barrier();
   }
 
@@ -891,7 +899,7 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
 
 template <int DK, int DV>
 __device__ __forceinline__ void operator_wave(const ScanArgs& args, const Chain& ch,
-                                              unsigned char* smem, int lane, int col0) {
+                                              unsigned char* smem, int lane, int col0, int wslot) {
   using LP = Lds<DK>;
   constexpr int NU = DK / 16;
   constexpr int NM = DK / 32;
@@ -946,6 +954,7 @@ __device__ __forceinline__ void operator_wave(const ScanArgs& args, const Chain&
         st[m] = acc;
       }
     }
+    if (it + 1 >= 0 && it + 1 < ch.nc) emit_w<DK>(ch, smem, lane, (it + 1) & 1, w_tile(wslot));
     lds_barrier();
   }
 
@@ -956,11 +965,14 @@ __device__ __forceinline__ void operator_wave(const ScanArgs& args, const Chain&
     for (int e = 0; e < 16; ++e) po[true_row(m, e, g2) * DK] = st[m][e];
 }
 
-// every wave of the workgroup runs the same number of iterations and barriers
+// every wave of the workgroup runs the same number of iterations and barriers;
+// a consumer slot without columns still forms its share of W
 template <int DK, int DV>
-__device__ __forceinline__ void idle_wave(const Chain& ch) {
+__device__ __forceinline__ void idle_wave(const Chain& ch, unsigned char* smem, int lane,
+                                          int wslot) {
   for (int it = -2; it < ch.nc; ++it) {
     lds_barrier();
+    if (it + 1 >= 0 && it + 1 < ch.nc) emit_w<DK>(ch, smem, lane, (it + 1) & 1, w_tile(wslot));
     lds_barrier();
   }
 }
@@ -1028,11 +1040,11 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       col0 = cb * 2 * NCOL + 32 * wave;
     }
     if (state_role && col0 < DV)
-      state_wave<DK, DV>(args, ch, smem, lane, col0);
+      state_wave<DK, DV>(args, ch, smem, lane, col0, wave);
     else if (!state_role && ch.need_op)
-      operator_wave<DK, DV>(args, ch, smem, lane, col0);
+      operator_wave<DK, DV>(args, ch, smem, lane, col0, wave);
     else
-      idle_wave<DK, DV>(ch);
+      idle_wave<DK, DV>(ch, smem, lane, wave);
   } else if (wave == 4) {
     inverse_wave<DK, DV>(args, ch, smem, lane);
   } else if (wave == 5) {
