@@ -1,19 +1,27 @@
 // Segment composition, Eq. (6), for gfx950.
 //
-// One workgroup of d_k / 16 waves per (request, v-head).  The running state S
-// (d_k x d_v, float32) stays on chip for the whole request.  Per listed segment
-// i every wave updates its band of 16 state rows,
-//     S[band] <- exp(log_decay_i) * (P_hat_i[band, :] @ S) + S_seg_i[band],
+// For every request r and v-head h, S starts at the prefix (or zero) and for
+// each listed segment i in order
+//     S_incoming[j] = S;   S <- exp(log_decay_i) * (P_hat_i @ S) + S_seg_i,
 // which is the two-segment true splice of Eq. (4) applied in list order.
 //
-// The product is formed transposed, S^T P_hat^T, so that the accumulator
-// layout gives each lane four consecutive columns of one state row: every
-// access to HBM (P_hat rows, S_seg, the optional prefix, S_incoming, S_out)
-// is then a 16-byte load or store per lane, 64 contiguous bytes per row per
-// instruction.  The A operand (S^T) is read from a column-major copy of the
-// state in LDS; the B operand (P_hat^T) is P_hat's own rows.  Each byte of the
-// pool tuple is read once.  The tuple of step j + 1 is loaded into registers
-// while step j computes.
+// One workgroup of d_k / 16 waves runs one (request, v-head, column block):
+// the state S (all d_k rows, NC = d_v / NCB columns) stays on chip for the
+// whole request, wave w owning rows 16w .. 16w+15.  Per listed segment:
+//   * each wave streams its 16 rows of P_hat_i from HBM (16 rows x 64
+//     contiguous bytes per load instruction), split once into bf16 hi + lo,
+//     the A operand of P_hat S;
+//   * the B operand is S itself: a wave's 16 x 16 accumulator tiles are
+//     exactly half of a 32-deep B fragment (rows 4g .. 4g+3 of column n in
+//     lane (g, n)), so publishing the state is one 8-byte LDS store of its hi
+//     and one of its lo part per tile, and every wave reads the fragments it
+//     needs with 16-byte loads;
+//   * the product runs in three bf16 passes (hi hi, hi lo, lo hi) or on the
+//     float32 matrix cores, then S <- e^g (P_hat S) + S_seg in float32.
+// The tuple of step j + 1 is loaded into registers while step j computes.
+// Small grids split the columns of each head over NCB = 4 workgroups (numbered
+// so that they land on one XCD and share its L2 for P_hat); large grids keep
+// one workgroup per head, so each byte of the pool tuple is read once.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -25,116 +33,196 @@ namespace hypic {
 
 namespace {
 
-template <int DK, int DV, int P>
+typedef unsigned short u16;
+typedef u16 u16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ u16 bf16_bits(float x) {
+  return __builtin_bit_cast(u16, static_cast<__bf16>(x));
+}
+
+template <int DK, int DV, int P, int NCB>
 __global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
-  constexpr int KB = DK / 32;     // 32-wide contraction blocks
-  constexpr int NT = DV / 16;     // 16-column tiles of the state
-  constexpr int LDT = DK + 4;     // column stride (floats) of the LDS copy
-  __shared__ float st_t[DV * LDT];  // st_t[c * LDT + d] = S[d][c]
+  constexpr int KB = DK / 32;        // 32-deep contraction blocks
+  constexpr int NC = DV / NCB;       // state columns of this workgroup
+  constexpr int NT = NC / 16;        // 16-column tiles
+  constexpr bool SPLIT = P != P_F32;
+  // B fragments of S: (kb, mt) -> 64 lanes x 8 values, as bf16 hi + lo or float32
+  constexpr int FRAG_U32 = SPLIT ? 64 * 4 * 2 : 64 * 8;  // 32-bit words per fragment
+  __shared__ __align__(16) uint32_t sb[KB * NT * FRAG_U32];
 
   const int tid = threadIdx.x;
-  const int wave = tid / 64, lane = tid % 64;
-  const int g = lane / 16, ln = lane % 16;
-  const int req = blockIdx.x / args.h_v;
-  const int h = blockIdx.x % args.h_v;
-  const int row = wave * 16 + ln;  // this lane's state row
+  const int wave = tid >> 6, lane = tid & 63;
+  const int g = lane >> 4, ln = lane & 15;
+
+  // work item: n_heads chains of NCB column blocks, the blocks of one chain
+  // numbered to land on one XCD back to back (workgroups are dealt to the 8
+  // XCDs round-robin); chains past the last full group of 8 keep linear order
+  const int n_chains = static_cast<int>(gridDim.x) / NCB;
+  const int full = (n_chains / 8) * 8 * NCB;
+  int chain, cb;
+  if (static_cast<int>(blockIdx.x) < full) {
+    const int slot = blockIdx.x / 8;
+    chain = (slot / NCB) * 8 + blockIdx.x % 8;
+    cb = slot % NCB;
+  } else {
+    const int b = blockIdx.x - full;
+    chain = full / NCB + b / NCB;
+    cb = b % NCB;
+  }
+  const int req = chain / args.h_v;
+  const int h = chain % args.h_v;
+  const int c0 = cb * NC;
   const long state_sz = static_cast<long>(DK) * DV;
   const long hs = static_cast<long>(req) * args.h_v + h;
+  const int row0 = wave * 16;  // this wave's state rows
 
-  // s[mt][i] = S[row][16 mt + 4 g + i]
+  // element (mt, i) of a state tile: S[row0 + 4g + i][c0 + 16mt + ln]
+  auto tile_ptr = [&](const float* base, int mt) __attribute__((always_inline)) {
+    return base + static_cast<long>(row0 + 4 * g) * DV + c0 + 16 * mt + ln;
+  };
+
   f32x4 s[NT];
   if (args.S_prefix != nullptr) {
-    const float* pre = args.S_prefix + hs * state_sz + static_cast<long>(row) * DV + 4 * g;
+    const float* pre = args.S_prefix + hs * state_sz;
 #pragma unroll
-    for (int mt = 0; mt < NT; ++mt) s[mt] = *reinterpret_cast<const f32x4*>(pre + 16 * mt);
+    for (int mt = 0; mt < NT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) s[mt][i] = tile_ptr(pre, mt)[i * DV];
   } else {
 #pragma unroll
     for (int mt = 0; mt < NT; ++mt) s[mt] = zero4();
   }
 
-  auto publish = [&]() {
+  // publish: tile mt of wave w fills slots 4(w % 2) .. +3 of fragment (w / 2, mt)
+  auto publish = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int mt = 0; mt < NT; ++mt)
+    for (int mt = 0; mt < NT; ++mt) {
+      uint32_t* f = sb + ((wave >> 1) * NT + mt) * FRAG_U32;
+      if constexpr (SPLIT) {
+        u16x4 hi, lo;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) st_t[(16 * mt + 4 * g + i) * LDT + row] = s[mt][i];
+        for (int i = 0; i < 4; ++i) {
+          const __bf16 hb = static_cast<__bf16>(s[mt][i]);
+          hi[i] = __builtin_bit_cast(u16, hb);
+          lo[i] = bf16_bits(s[mt][i] - static_cast<float>(hb));
+        }
+        *reinterpret_cast<u16x4*>(f + lane * 4 + 2 * (wave & 1)) = hi;
+        *reinterpret_cast<u16x4*>(f + 64 * 4 + lane * 4 + 2 * (wave & 1)) = lo;
+      } else {
+        *reinterpret_cast<float4*>(f + lane * 8 + 4 * (wave & 1)) =
+            make_float4(s[mt][0], s[mt][1], s[mt][2], s[mt][3]);
+      }
+    }
   };
   publish();
-  __syncthreads();
+  lds_barrier();  // (no wave reads what another writes to HBM: loads stay in flight)
 
-  // pool tuple of one step: this lane's row of P_hat as B fragments (k slots
-  // kap(g, .) of each 32-block) and its four S_seg columns per tile
+  // pool tuple of one step: this lane's row of P_hat as A fragments (k slots
+  // kap(g, .) of each 32-block) and the S_seg tile elements
   const int j0 = args.req_offsets[req], j1 = args.req_offsets[req + 1];
   float nP[KB][8];
   f32x4 nS[NT];
   float nE = 0.f;
   auto load_step = [&](int j) __attribute__((always_inline)) {
     const long sh = static_cast<long>(args.seg_ids[j]) * args.h_v + h;
-    const float* Pi = args.P_hat + sh * DK * DK + static_cast<long>(row) * DK + 4 * g;
-    const float* Si = args.S_seg + sh * state_sz + static_cast<long>(row) * DV + 4 * g;
+    const float* Pi = args.P_hat + sh * DK * DK + static_cast<long>(row0 + ln) * DK + 4 * g;
+    const float* Si = args.S_seg + sh * state_sz;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
-      const float4 lo = *reinterpret_cast<const float4*>(Pi + 32 * kb);
-      const float4 hi = *reinterpret_cast<const float4*>(Pi + 32 * kb + 16);
-      nP[kb][0] = lo.x; nP[kb][1] = lo.y; nP[kb][2] = lo.z; nP[kb][3] = lo.w;
-      nP[kb][4] = hi.x; nP[kb][5] = hi.y; nP[kb][6] = hi.z; nP[kb][7] = hi.w;
+      const float4 a = *reinterpret_cast<const float4*>(Pi + 32 * kb);
+      const float4 b = *reinterpret_cast<const float4*>(Pi + 32 * kb + 16);
+      nP[kb][0] = a.x; nP[kb][1] = a.y; nP[kb][2] = a.z; nP[kb][3] = a.w;
+      nP[kb][4] = b.x; nP[kb][5] = b.y; nP[kb][6] = b.z; nP[kb][7] = b.w;
     }
 #pragma unroll
-    for (int mt = 0; mt < NT; ++mt) nS[mt] = *reinterpret_cast<const f32x4*>(Si + 16 * mt);
+    for (int mt = 0; mt < NT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) nS[mt][i] = tile_ptr(Si, mt)[i * DV];
     nE = __expf(args.log_decay[sh]);
   };
   if (j0 < j1) load_step(j0);
   for (int j = j0; j < j1; ++j) {
-    float cP[KB][8];
+    // A operand of this step, split once
+    bf16x8 ah[KB], al[KB];
+    float af[KB][8];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      if constexpr (SPLIT) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          ah[kb][e] = static_cast<__bf16>(nP[kb][e]);
+          al[kb][e] = static_cast<__bf16>(nP[kb][e] - static_cast<float>(ah[kb][e]));
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) af[kb][e] = nP[kb][e];
+      }
+    }
     f32x4 cS[NT];
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) cP[kb][e] = nP[kb][e];
 #pragma unroll
     for (int mt = 0; mt < NT; ++mt) cS[mt] = nS[mt];
     const float e = nE;
     if (j + 1 < j1) load_step(j + 1);
     if (args.S_incoming != nullptr) {
-      float* dst = args.S_incoming + (static_cast<long>(j) * args.h_v + h) * state_sz +
-                   static_cast<long>(row) * DV + 4 * g;
+      float* dst = args.S_incoming + (static_cast<long>(j) * args.h_v + h) * state_sz;
 #pragma unroll
-      for (int mt = 0; mt < NT; ++mt) *reinterpret_cast<f32x4*>(dst + 16 * mt) = s[mt];
+      for (int mt = 0; mt < NT; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) const_cast<float*>(tile_ptr(dst, mt))[i * DV] = s[mt][i];
     }
 #pragma unroll
     for (int mt = 0; mt < NT; ++mt) {
-      f32x4 prod = zero4();
+      f32x4 acc = zero4();
 #pragma unroll
       for (int kb = 0; kb < KB; ++kb) {
-        // A = S^T: column 16 mt + ln of the state, rows 32 kb + kap(g, .)
-        float fa[8];
-        const float* src = st_t + (16 * mt + ln) * LDT + 32 * kb + 4 * g;
-        const float4 lo = *reinterpret_cast<const float4*>(src);
-        const float4 hi = *reinterpret_cast<const float4*>(src + 16);
-        fa[0] = lo.x; fa[1] = lo.y; fa[2] = lo.z; fa[3] = lo.w;
-        fa[4] = hi.x; fa[5] = hi.y; fa[6] = hi.z; fa[7] = hi.w;
-        mma_blk<P>(prod, fa, cP[kb]);
+        const uint32_t* f = sb + (kb * NT + mt) * FRAG_U32;
+        if constexpr (SPLIT) {
+          const bf16x8 bh = *reinterpret_cast<const bf16x8*>(f + lane * 4);
+          const bf16x8 bl = *reinterpret_cast<const bf16x8*>(f + 64 * 4 + lane * 4);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[kb], bh, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[kb], bl, acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[kb], bh, acc, 0, 0, 0);
+        } else {
+          const float4 b0 = *reinterpret_cast<const float4*>(f + lane * 8);
+          const float4 b1 = *reinterpret_cast<const float4*>(f + lane * 8 + 4);
+          const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[kb][q], bv[q], acc, 0, 0, 0);
+        }
       }
-      s[mt] = prod * e + cS[mt];
+      s[mt] = acc * e + cS[mt];
     }
-    __syncthreads();  // every wave has read the old state
+    lds_barrier();  // every wave has read the old state
     publish();
-    __syncthreads();
+    lds_barrier();
   }
 
-  float* out = args.S_out + hs * state_sz + static_cast<long>(row) * DV + 4 * g;
+  float* out = args.S_out + hs * state_sz;
 #pragma unroll
-  for (int mt = 0; mt < NT; ++mt) *reinterpret_cast<f32x4*>(out + 16 * mt) = s[mt];
+  for (int mt = 0; mt < NT; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) const_cast<float*>(tile_ptr(out, mt))[i * DV] = s[mt][i];
+}
+
+template <int DK, int DV, int P>
+hipError_t launch_compose_p(const ComposeArgs& a, int n_req, hipStream_t s) {
+  const long heads = static_cast<long>(n_req) * a.h_v;
+  const dim3 block(DK * 4);  // one wave per 16 state rows
+  // split the columns of each head over 4 workgroups while that keeps the
+  // grid within two workgroups per compute unit
+  if (heads * 4 <= 512) {
+    hipLaunchKernelGGL((compose_kernel<DK, DV, P, 4>), dim3(heads * 4), block, 0, s, a);
+  } else {
+    hipLaunchKernelGGL((compose_kernel<DK, DV, P, 1>), dim3(heads), block, 0, s, a);
+  }
+  return hipGetLastError();
 }
 
 template <int DK, int DV>
 hipError_t launch_compose_d(const ComposeArgs& a, int f32, int n_req, hipStream_t s) {
-  const dim3 grid(static_cast<unsigned>(n_req) * a.h_v);
-  const dim3 block(DK * 4);  // one wave per 16 state rows
-  if (f32)
-    hipLaunchKernelGGL((compose_kernel<DK, DV, P_F32>), grid, block, 0, s, a);
-  else
-    hipLaunchKernelGGL((compose_kernel<DK, DV, P_SPLIT>), grid, block, 0, s, a);
-  return hipGetLastError();
+  if (f32) return launch_compose_p<DK, DV, P_F32>(a, n_req, s);
+  return launch_compose_p<DK, DV, P_SPLIT>(a, n_req, s);
 }
 
 }  // namespace

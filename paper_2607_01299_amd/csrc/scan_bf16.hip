@@ -679,11 +679,11 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
         }
       {
         // -A1 diag(beta) of this chunk as bf16 hi + lo fragments for W: wave 6
-        // the fragments 0-3, wave 7 the fragments 4, 5
+        // the fragments 0-2, wave 7 the fragments 3-5
         const float* af = reinterpret_cast<const float*>(smem + LP::O_AF + par * LP::AFB);
         u16* ab = reinterpret_cast<u16*>(smem + LP::O_AB);
 #pragma unroll
-        for (int f = (HALF == 0) ? 0 : 4; f < ((HALF == 0) ? 4 : 6); ++f) {
+        for (int f = 3 * HALF; f < 3 * HALF + 3; ++f) {
           const float4 v0 = *reinterpret_cast<const float4*>(af + (f * 64 + lane) * 8);
           const float4 v1 = *reinterpret_cast<const float4*>(af + (f * 64 + lane) * 8 + 4);
           f32x16 x;
