@@ -18,7 +18,8 @@
 //     needs with 16-byte loads;
 //   * the product runs in three bf16 passes (hi hi, hi lo, lo hi) or on the
 //     float32 matrix cores, then S <- e^g (P_hat S) + S_seg in float32.
-// The tuple of step j + 1 is loaded into registers while step j computes.
+// The tuple of a later step is loaded into registers while a step computes
+// (two steps ahead on split grids, one on full-width ones).
 // Small grids split the columns of each head over NCB = 4 workgroups (numbered
 // so that they land on one XCD and share its L2 for P_hat); large grids keep
 // one workgroup per head, so each byte of the pool tuple is read once.
@@ -117,31 +118,42 @@ __global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
   publish();
   lds_barrier();  // (no wave reads what another writes to HBM: loads stay in flight)
 
-  // pool tuple of one step: this lane's row of P_hat as A fragments (k slots
-  // kap(g, .) of each 32-block) and the S_seg tile elements
+  // Pool tuple of one step: this lane's row of P_hat as A fragments (k slots
+  // kap(g, .) of each 32-block), the S_seg tile elements and exp(log_decay).
+  // LOOK register sets: the tuple of step j + LOOK is loaded while step j
+  // computes.  Split grids are latency-bound and look two steps ahead; the
+  // full-width state of an unsplit grid leaves registers for one.
+  constexpr int LOOK = (NCB > 1) ? 2 : 1;
+  struct Tuple {
+    float p[KB][8];
+    f32x4 s[NT];
+    float e;
+  };
   const int j0 = args.req_offsets[req], j1 = args.req_offsets[req + 1];
-  float nP[KB][8];
-  f32x4 nS[NT];
-  float nE = 0.f;
-  auto load_step = [&](int j) __attribute__((always_inline)) {
-    const long sh = static_cast<long>(args.seg_ids[j]) * args.h_v + h;
+  // the request's first 64 segment ids, one per lane, so that a step's tuple
+  // address does not wait for a load of its id
+  const int my_id = (j0 + lane < j1) ? args.seg_ids[j0 + lane] : 0;
+  auto load_step = [&](Tuple& t, int j) __attribute__((always_inline)) {
+    const int id = (j - j0 < 64) ? __builtin_amdgcn_readlane(my_id, j - j0) : args.seg_ids[j];
+    const long sh = static_cast<long>(id) * args.h_v + h;
     const float* Pi = args.P_hat + sh * DK * DK + static_cast<long>(row0 + ln) * DK + 4 * g;
     const float* Si = args.S_seg + sh * state_sz;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
       const float4 a = *reinterpret_cast<const float4*>(Pi + 32 * kb);
       const float4 b = *reinterpret_cast<const float4*>(Pi + 32 * kb + 16);
-      nP[kb][0] = a.x; nP[kb][1] = a.y; nP[kb][2] = a.z; nP[kb][3] = a.w;
-      nP[kb][4] = b.x; nP[kb][5] = b.y; nP[kb][6] = b.z; nP[kb][7] = b.w;
+      t.p[kb][0] = a.x; t.p[kb][1] = a.y; t.p[kb][2] = a.z; t.p[kb][3] = a.w;
+      t.p[kb][4] = b.x; t.p[kb][5] = b.y; t.p[kb][6] = b.z; t.p[kb][7] = b.w;
     }
 #pragma unroll
     for (int mt = 0; mt < NT; ++mt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) nS[mt][i] = tile_ptr(Si, mt)[i * DV];
-    nE = __expf(args.log_decay[sh]);
+      for (int i = 0; i < 4; ++i) t.s[mt][i] = tile_ptr(Si, mt)[i * DV];
+    t.e = __expf(args.log_decay[sh]);
   };
-  if (j0 < j1) load_step(j0);
-  for (int j = j0; j < j1; ++j) {
+  // one composition step with the tuple t (step j), then the load of step
+  // j + LOOK into t
+  auto step = [&](Tuple& t, int j) __attribute__((always_inline)) {
     // A operand of this step, split once
     bf16x8 ah[KB], al[KB];
     float af[KB][8];
@@ -150,19 +162,19 @@ __global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
       if constexpr (SPLIT) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          ah[kb][e] = static_cast<__bf16>(nP[kb][e]);
-          al[kb][e] = static_cast<__bf16>(nP[kb][e] - static_cast<float>(ah[kb][e]));
+          ah[kb][e] = static_cast<__bf16>(t.p[kb][e]);
+          al[kb][e] = static_cast<__bf16>(t.p[kb][e] - static_cast<float>(ah[kb][e]));
         }
       } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) af[kb][e] = nP[kb][e];
+        for (int e = 0; e < 8; ++e) af[kb][e] = t.p[kb][e];
       }
     }
     f32x4 cS[NT];
 #pragma unroll
-    for (int mt = 0; mt < NT; ++mt) cS[mt] = nS[mt];
-    const float e = nE;
-    if (j + 1 < j1) load_step(j + 1);
+    for (int mt = 0; mt < NT; ++mt) cS[mt] = t.s[mt];
+    const float e = t.e;
+    if (j + LOOK < j1) load_step(t, j + LOOK);
     if (args.S_incoming != nullptr) {
       float* dst = args.S_incoming + (static_cast<long>(j) * args.h_v + h) * state_sz;
 #pragma unroll
@@ -196,6 +208,19 @@ __global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
     lds_barrier();  // every wave has read the old state
     publish();
     lds_barrier();
+  };
+  if constexpr (LOOK == 2) {
+    Tuple ta, tb;
+    if (j0 < j1) load_step(ta, j0);
+    if (j0 + 1 < j1) load_step(tb, j0 + 1);
+    for (int j = j0; j < j1; j += 2) {
+      step(ta, j);
+      if (j + 1 < j1) step(tb, j + 1);
+    }
+  } else {
+    Tuple ta;
+    if (j0 < j1) load_step(ta, j0);
+    for (int j = j0; j < j1; ++j) step(ta, j);
   }
 
   float* out = args.S_out + hs * state_sz;
