@@ -570,9 +570,25 @@ hipError_t launch_scan(const ScanArgs& a, int bf16, int d_k, int d_v, int chunk,
   const bool fast = bf16 && chunk == 64;
   const int64_t per_head =
       fast ? scan_bf16_items_per_head(d_k, d_v, a.n_roles == 2) : a.n_roles;
+  if (fast) {
+    // Seams of at most one chunk run back to back through one workgroup's
+    // pipeline, up to 16 entries of one head per workgroup, while that still
+    // leaves two workgroups per compute unit.
+    ScanArgs b = a;
+    b.n_entries = n_chains;
+    b.group_e = 1;
+    if (a.mode == 1 && a.w <= 64) {
+      const int64_t pairs = static_cast<int64_t>(n_chains) * a.h_v;
+      const int64_t ge = pairs / 512;
+      b.group_e = static_cast<int>((ge < 1) ? 1 : ((ge > 16) ? 16 : ge));
+    }
+    const int64_t groups = (n_chains + b.group_e - 1) / b.group_e;
+    const int64_t n_items = groups * a.h_v * per_head;
+    if (n_items > 0x7fffffff) return hipErrorInvalidValue;
+    return launch_scan_bf16(b, d_k, d_v, static_cast<int>(n_items), s);
+  }
   const int64_t n_items = static_cast<int64_t>(n_chains) * a.h_v * per_head;
   if (n_items > 0x7fffffff) return hipErrorInvalidValue;
-  if (fast) return launch_scan_bf16(a, d_k, d_v, static_cast<int>(n_items), s);
   if (bf16)
     return launch_scan_d<uint16_t>(a, d_k, d_v, chunk, static_cast<int>(n_items), s);
   return launch_scan_d<float>(a, d_k, d_v, chunk, static_cast<int>(n_items), s);

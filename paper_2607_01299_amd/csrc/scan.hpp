@@ -23,6 +23,8 @@ struct ScanArgs {
   const int32_t* tok_start;  // seam: first token of each entry
   const int32_t* tok_len;    // seam: segment length of each entry
   int32_t w;                 // seam width
+  int32_t n_entries;         // seam: number of entries
+  int32_t group_e;           // seam: entries per workgroup (w <= chunk: run back to back)
   const float* S_in;         // seam: incoming states
   void* o;                   // outputs (build: [T,h_v,d_v]; seam: [n,w,h_v,d_v])
   float* S_out;              // build: S_seg; seam: S_post (may be null)

@@ -203,18 +203,36 @@ struct Lds {
   static_assert(TOTAL <= 160 * 1024, "LDS budget");
 };
 
-// Shared description of the chain a workgroup runs.
+// Shared description of the chain a workgroup runs: the chunks of one
+// segment (build) or seam entry, or, for seams of at most one chunk, the
+// seam entries e0 .. e0 + nc - 1 of one head back to back (one chunk each).
 struct Chain {
   int seg, h, hk, lo, hi, nc, cb;
   long sh;            // seg * h_v + h
   long qk_stride;     // elements between token rows of q, k
   long v_stride;      // elements between token rows of v, o
   bool with_op, need_state, need_op;
+  bool batched;       // one seam entry per chunk
+  int e0, w, n_tok;
+  const int32_t* tok_start;
+  const int32_t* tok_len;
 };
 
+__device__ __forceinline__ int chunk_start(const Chain& ch, int c) {
+  if (!ch.batched) return ch.lo + c * C;
+  const int t = ch.tok_start[ch.e0 + c];
+  return (t < 0) ? 0 : ((t >= ch.n_tok) ? ch.n_tok - 1 : t);
+}
 __device__ __forceinline__ int chunk_len(const Chain& ch, int c) {
-  const int r = ch.hi - (ch.lo + c * C);
-  return (r < C) ? r : C;
+  if (!ch.batched) {
+    const int r = ch.hi - (ch.lo + c * C);
+    return (r < C) ? r : C;
+  }
+  const int t = chunk_start(ch, c);
+  const int l = ch.tok_len[ch.e0 + c];
+  int n = (l < ch.w) ? l : ch.w;
+  n = (n > ch.n_tok - t) ? ch.n_tok - t : n;
+  return (n < 1) ? 1 : n;
 }
 
 // raw 16-byte loads of the 32x32-layout fragments of one token tile of a
@@ -295,7 +313,7 @@ __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& 
   uint4 kr[4][KTD];
   float pb = 0.f;
   auto prefetch = [&](int c) __attribute__((always_inline)) {
-    const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+    const int c0 = chunk_start(ch, c), n = chunk_len(ch, c);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const int tok = 16 * t + n16;
@@ -518,7 +536,7 @@ __device__ __forceinline__ void producer_qk_wave(const ScanArgs& args, const Cha
   uint4 kr[4][KTD], qr[4][KTD];
   float pa = 0.f, pbeta = 0.f;
   auto prefetch = [&](int c) __attribute__((always_inline)) {
-    const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+    const int c0 = chunk_start(ch, c), n = chunk_len(ch, c);
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       load_tile16<KTD>(kr[t], kg, ch.qk_stride, c0, n, t, lane);
@@ -642,7 +660,7 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
   }
   uint4 kr[4][NH];
   auto prefetch = [&](int c) __attribute__((always_inline)) {
-    const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+    const int c0 = chunk_start(ch, c), n = chunk_len(ch, c);
 #pragma unroll
     for (int t = 0; t < 4; ++t) load_tile16<NH>(kr[t], kg, ch.qk_stride, c0, n, t, lane);
   };
@@ -770,21 +788,28 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
 
   uint4 vr[2][2];
   auto prefetch = [&](int c) __attribute__((always_inline)) {
-    const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+    const int c0 = chunk_start(ch, c), n = chunk_len(ch, c);
     load_tile32<2>(vr[0], vg, ch.v_stride, c0, n, 0, lane);
     load_tile32<2>(vr[1], vg, ch.v_stride, c0, n, 1, lane);
   };
   if (ch.nc > 0) prefetch(0);
   float log_decay = 0.f;
 
+  const int lane_in = lane;
   for (int it = -2; it < ch.nc; ++it) {
+    // an opaque copy of the lane index keeps the compiler from hoisting every
+    // loop-invariant fragment address out of the chunk loop (each would pin a
+    // register); they are cheap to recompute per chunk
+    int lane = lane_in;
+    asm volatile("" : "+v"(lane));
+    const int g2 = lane >> 5, n32 = lane & 31;
     const int c = it;
     const bool active = c >= 0;
     const int par = c & 1;
     const float* gb = reinterpret_cast<const float*>(smem + LP::O_G + par * 4 * C * 4);
     bf16x8 dvn[4];
     if (active) {
-      const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+      const int c0 = chunk_start(ch, c), n = chunk_len(ch, c);
       const float* ggam = gb + 2 * C;
       const float* gdec = gb + 3 * C;
       const u16* fQ = reinterpret_cast<const u16*>(smem + LP::O_Q + par * LP::NW * LP::FB);
@@ -834,7 +859,8 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
 #pragma unroll
       for (int s = 0; s < 4; ++s) vA[s] = frag_of(vn[s >> 1], s & 1);
       const long orow0 = (args.mode == 0) ? static_cast<long>(c0)
-                                          : static_cast<long>(ch.seg) * args.w + (c0 - ch.lo);
+                         : ch.batched ? static_cast<long>(ch.e0 + c) * args.w
+                                      : static_cast<long>(ch.seg) * args.w + (c0 - ch.lo);
 #pragma unroll
       for (int tq = 0; tq < 2; ++tq) {
         f32x16 acc = zero16();
@@ -882,11 +908,37 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
         st[m] = acc;
       }
     }
+    if (active && ch.batched) {
+      // one seam entry per chunk: its state after the seam, then the state
+      // entering the next entry
+      const long eh = static_cast<long>(ch.e0 + c) * args.h_v + ch.h;
+      // an opaque copy of the row stride keeps the compiler from hoisting all
+      // 64 row offsets out of the loop (each would pin a register)
+      int dv = DV;
+      asm volatile("" : "+v"(dv));
+      __builtin_amdgcn_sched_barrier(0);
+      if (args.S_out != nullptr) {
+        float* so = args.S_out + eh * DK * DV + col0 + n32;
+#pragma unroll
+        for (int m = 0; m < NM; ++m)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) so[true_row(m, e, g2) * dv] = st[m][e];
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (c + 1 < ch.nc) {
+        const float* s_in = args.S_in + (eh + args.h_v) * DK * DV + col0 + n32;
+#pragma unroll
+        for (int m = 0; m < NM; ++m)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) st[m][e] = s_in[true_row(m, e, g2) * dv];
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if (it + 1 >= 0 && it + 1 < ch.nc) emit_w<DK>(ch, smem, lane, (it + 1) & 1, w_tile(wslot));
     lds_barrier();
   }
 
-  if (args.S_out != nullptr) {
+  if (args.S_out != nullptr && !ch.batched) {
     float* so = args.S_out + ch.sh * DK * DV + col0 + n32;
 #pragma unroll
     for (int m = 0; m < NM; ++m)
@@ -1007,10 +1059,20 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   ch.h = chain % args.h_v;
   ch.cb = cb;
   int lo, hi;
+  ch.batched = args.mode == 1 && args.w <= C;
+  ch.w = args.w;
+  ch.n_tok = args.n_tokens;
+  ch.tok_start = args.tok_start;
+  ch.tok_len = args.tok_len;
+  ch.e0 = 0;
   if (args.mode == 0) {
     ch.seg = args.order[rank];
     lo = args.cu_seqlens[ch.seg];
     hi = args.cu_seqlens[ch.seg + 1];
+  } else if (ch.batched) {
+    ch.e0 = rank * args.group_e;
+    ch.seg = ch.e0;
+    lo = hi = 0;
   } else {
     ch.seg = rank;
     lo = args.tok_start[ch.seg];
@@ -1021,7 +1083,12 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   hi = (hi < lo) ? lo : ((hi > args.n_tokens) ? args.n_tokens : hi);
   ch.lo = lo;
   ch.hi = hi;
-  ch.nc = (hi - lo + C - 1) / C;
+  if (ch.batched) {
+    const int e1 = ch.e0 + args.group_e;
+    ch.nc = ((e1 < args.n_entries) ? e1 : args.n_entries) - ch.e0;
+  } else {
+    ch.nc = (hi - lo + C - 1) / C;
+  }
   ch.hk = ch.h / args.group;
   ch.sh = static_cast<long>(ch.seg) * args.h_v + ch.h;
   ch.qk_stride = static_cast<long>(args.h_qk) * DK;
