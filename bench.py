@@ -11,8 +11,10 @@ steps, inputs resident in HBM.
 
 Also reported:
   roofline      the build scan kernel: algorithmic FLOP per launch over its
-                average duration (HIP events on the launch stream) vs the
-                dense bf16 matrix-core peak;
+                average duration (HIP events on the launch stream around
+                back-to-back builds after the timed steps; build_ms_in_step is
+                the same call bracketed inside each step) vs the dense bf16
+                matrix-core peak;
   compose_burst serve-time burst: 256 requests x U{8..64} segments of a
                 512-entry float32 pool (16 heads, 128 x 128), then a w = 64
                 seam per listed segment; compositions / s and the composition
@@ -119,15 +121,16 @@ def _worker_init(cfg):
     _CACHE[cfg] = W.segment_workload(cfg)
 
 
-def cpu_baseline(cfg, h_v, pairs_per_worker=12):
+def cpu_baseline(cfg, h_v, pairs_per_worker=100):
     import multiprocessing as mp
     workers = min(len(os.sched_getaffinity(0)), 16)
     for var in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
         os.environ[var] = "1"
     wl = W.segment_workload(cfg)
     n_seg = len(wl["cu_seqlens"]) - 1
-    pairs = [(cfg, s, h) for h in range(h_v) for s in range(n_seg)]
-    pairs = pairs[:workers * pairs_per_worker]
+    distinct = [(cfg, s, h) for h in range(h_v) for s in range(n_seg)]
+    # 10-20 s of wall time on 16 cores: the distinct pairs, cycled
+    pairs = [distinct[i % len(distinct)] for i in range(workers * pairs_per_worker)]
     ctx = mp.get_context("spawn")
     with ctx.Pool(workers, initializer=_worker_init, initargs=(cfg,)) as pool:
         pool.map(_oracle_pair, pairs[:workers])           # warm the workers
@@ -141,8 +144,9 @@ def cpu_baseline(cfg, h_v, pairs_per_worker=12):
         "cores": workers,
         "kind": "oracle",
         "sample": "%d (segment, head) builds of %d tokens (S and operator, float64 token "
-                  "recurrence) on %d processes, %.1f s; tokens/s = token-heads/s / %d heads"
-                  % (len(pairs), int(toks[0]), workers, dt, h_v),
+                  "recurrence; the workload's %d distinct pairs, cycled) on %d processes, "
+                  "%.1f s; tokens/s = token-heads/s / %d heads"
+                  % (len(pairs), int(toks[0]), len(distinct), workers, dt, h_v),
     }
 
 
@@ -180,7 +184,16 @@ def bench_segments(torch, cfg, steps, warmup, seam_w):
         pipe.seam()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    build_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    build_in_step_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    # the build kernel's average launch duration: `steps` launches back to back
+    # between one pair of events on the launch stream (amortises the markers)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        pipe.build()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    build_ms = e0.elapsed_time(e1) / steps
     T = int(w["cu_seqlens"][-1])
     h_v, d_k, d_v = w["v"].shape[1], w["d_k"], w["d_v"]
     flop = float(flop_per_token_head(d_k, d_v, w["chunk"])) * T * h_v
@@ -189,6 +202,7 @@ def bench_segments(torch, cfg, steps, warmup, seam_w):
         "ms_per_step": dt / steps * 1e3,
         "tokens": T,
         "build_ms": build_ms,
+        "build_ms_in_step": build_in_step_ms,
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": measured_traffic("scan_bf16", W.CONFIG_NAMES[cfg]),
@@ -311,6 +325,7 @@ def main():
         "config": seg["config"],
         "roofline": seg["roofline"],
         "build_ms": seg["build_ms"],
+        "build_ms_in_step": seg["build_ms_in_step"],
         "cpu_baseline": cpu,
         "compose_burst": burst,
     }

@@ -105,9 +105,11 @@ const char* hypic_status_str(int32_t status);
  *   P_hat       [n_seg, h_v, d_k, d_k] f32, or NULL to skip the operator path.
  *   log_decay   [n_seg, h_v] f32, or NULL.
  *   workspace   device scratch of at least
- *               hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg) bytes
- *               (holds the longest-first segment order; contents are not
- *               preserved across calls).
+ *               hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg) bytes; that
+ *               is 0 (workspace may be NULL) for n_seg <= 128, whose order
+ *               travels in the kernel arguments.  Otherwise it holds the
+ *               longest-first segment order, computed on the device;
+ *               contents are not preserved across calls.
  * Segments are scheduled longest first (Eq. (9) LPT order, ties by index);
  * results do not depend on the schedule.  n_seg == 0 enqueues nothing.
  */

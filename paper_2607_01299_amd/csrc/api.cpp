@@ -1,6 +1,7 @@
 // C ABI of libhypic.so: argument validation on the host, workspace sizing and
 // kernel dispatch.  Nothing is enqueued unless every check passes.
 
+#include <algorithm>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -46,7 +47,8 @@ const char* hypic_status_str(int32_t status) {
 
 size_t hypic_workspace_bytes(int32_t op, const hypic_dims* dims, int64_t n) {
   if (check_dims(dims) != HYPIC_OK || n <= 0) return 0;
-  if (op == HYPIC_OP_BUILD) return round_up(static_cast<size_t>(n) * sizeof(int32_t));
+  if (op == HYPIC_OP_BUILD && n > hypic::kInlineOrder)
+    return round_up(static_cast<size_t>(n) * sizeof(int32_t));
   return 0;
 }
 
@@ -70,14 +72,27 @@ int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k
   const int64_t n_items = static_cast<int64_t>(n_seg) * dims->h_v * 4;
   if (n_items > 0x7fffffff) return HYPIC_EINVAL;
   const size_t need = hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg);
-  if (workspace == nullptr || workspace_bytes < need) return HYPIC_EWORKSPACE;
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return HYPIC_EWORKSPACE;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  int32_t* order = static_cast<int32_t*>(workspace);
-  st = hip_status(hypic::launch_lpt_order(cu_seqlens, n_seg, order, s));
-  if (st != HYPIC_OK) return st;
-
   hypic::ScanArgs a{};
+  if (n_seg <= hypic::kInlineOrder) {
+    // Eq. (9) list order, longest first, ties by index, from the host offsets.
+    int32_t idx[hypic::kInlineOrder];
+    for (int32_t i = 0; i < n_seg; ++i) idx[i] = i;
+    std::stable_sort(idx, idx + n_seg, [&](int32_t x, int32_t y) {
+      return cu_seqlens_host[x + 1] - cu_seqlens_host[x] >
+             cu_seqlens_host[y + 1] - cu_seqlens_host[y];
+    });
+    for (int32_t i = 0; i < n_seg; ++i) a.order_inline[i] = static_cast<uint16_t>(idx[i]);
+    a.n_inline = n_seg;
+    a.order = nullptr;
+  } else {
+    int32_t* order = static_cast<int32_t*>(workspace);
+    st = hip_status(hypic::launch_lpt_order(cu_seqlens, n_seg, order, s));
+    if (st != HYPIC_OK) return st;
+    a.order = order;
+  }
   a.q = q;
   a.k = k;
   a.v = v;
@@ -90,7 +105,6 @@ int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k
   a.mode = 0;
   a.n_roles = P_hat ? 2 : 1;
   a.cu_seqlens = cu_seqlens;
-  a.order = order;
   a.o = o;
   a.S_out = S_seg;
   a.P_hat = P_hat;

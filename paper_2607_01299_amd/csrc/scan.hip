@@ -194,7 +194,7 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(ScanArgs args) {
   const int hk = h / args.group;
   int seg, lo, hi;
   if (args.mode == 0) {
-    seg = args.order[rank];
+    seg = segment_of_rank(args, rank);
     lo = args.cu_seqlens[seg];
     hi = args.cu_seqlens[seg + 1];
   } else {

@@ -6,6 +6,10 @@
 
 namespace hypic {
 
+// Builds of at most this many segments carry their longest-first order in the
+// kernel arguments; larger builds compute it on the device into the workspace.
+constexpr int kInlineOrder = 128;
+
 // Arguments of the chunked scan kernel (segment build when mode == 0, seam
 // rescan when mode == 1).  All pointers are device pointers.
 struct ScanArgs {
@@ -19,7 +23,7 @@ struct ScanArgs {
   int32_t mode;              // 0 build, 1 seam
   int32_t n_roles;           // 1: state only, 2: state and operator
   const int32_t* cu_seqlens; // build: segment offsets
-  const int32_t* order;      // build: longest-first segment order
+  const int32_t* order;      // build: longest-first segment order (n_inline == 0)
   const int32_t* tok_start;  // seam: first token of each entry
   const int32_t* tok_len;    // seam: segment length of each entry
   int32_t w;                 // seam width
@@ -30,7 +34,14 @@ struct ScanArgs {
   float* S_out;              // build: S_seg; seam: S_post (may be null)
   float* P_hat;              // build, role 1
   float* log_decay;          // build, may be null
+  int32_t n_inline;          // build: > 0 when the order is held in order_inline
+  uint16_t order_inline[kInlineOrder];
 };
+
+// Segment scheduled at position `rank` of the longest-first order.
+__device__ __forceinline__ int32_t segment_of_rank(const ScanArgs& a, int rank) {
+  return a.n_inline > 0 ? static_cast<int32_t>(a.order_inline[rank]) : a.order[rank];
+}
 
 struct ComposeArgs {
   const float* P_hat;

@@ -1066,7 +1066,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   ch.tok_len = args.tok_len;
   ch.e0 = 0;
   if (args.mode == 0) {
-    ch.seg = args.order[rank];
+    ch.seg = segment_of_rank(args, rank);
     lo = args.cu_seqlens[ch.seg];
     hi = args.cu_seqlens[ch.seg + 1];
   } else if (ch.batched) {

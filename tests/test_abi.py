@@ -55,7 +55,9 @@ def test_status_strings(lib):
 
 def test_workspace_sizes(lib):
     d = _dims()
-    assert lib.hypic_workspace_bytes(_lib.HYPIC_OP_BUILD, ctypes.byref(d), 64) >= 64 * 4
+    assert lib.hypic_workspace_bytes(_lib.HYPIC_OP_BUILD, ctypes.byref(d), 1000) >= 1000 * 4
+    # up to 128 segments carry their order in the kernel arguments
+    assert lib.hypic_workspace_bytes(_lib.HYPIC_OP_BUILD, ctypes.byref(d), 128) == 0
     assert lib.hypic_workspace_bytes(_lib.HYPIC_OP_BUILD, ctypes.byref(d), 0) == 0
     assert lib.hypic_workspace_bytes(_lib.HYPIC_OP_COMPOSE, ctypes.byref(d), 10) == 0
     bad = _dims(d_k=96)
@@ -94,8 +96,10 @@ def test_build_rejects_bad_arguments(lib):
     assert _build(lib, d, [1, 10]) == _lib.HYPIC_EINVAL            # must start at 0
     assert _build(lib, d, [0, 10, 5]) == _lib.HYPIC_EINVAL         # decreasing
     assert _build(lib, d, [0, 10], n_seg=-1) == _lib.HYPIC_EINVAL
-    assert _build(lib, d, [0, 10, 20], ws=None) == _lib.HYPIC_EWORKSPACE
-    assert _build(lib, d, [0, 10, 20], ws_bytes=4) == _lib.HYPIC_EWORKSPACE
+    # past 128 segments the order needs device workspace
+    many = np.arange(0, 10 * 130, 10)
+    assert _build(lib, d, many, ws=None) == _lib.HYPIC_EWORKSPACE
+    assert _build(lib, d, many, ws_bytes=4) == _lib.HYPIC_EWORKSPACE
     # nothing to do is not an error (and launches nothing)
     assert _build(lib, d, [0], n_seg=0) == _lib.HYPIC_OK
 

@@ -158,6 +158,22 @@ def test_ragged_build_matches_oracle(hy, dtype, dk, dv, heads, chunk):
     assert np.all(_np(res["log_decay"])[3] == 0)
 
 
+@pytest.mark.parametrize("dtype,d", [(W.BF16, 128), (W.F32, 64)])
+def test_many_segments_device_order(hy, dtype, d):
+    """Past 128 segments the longest-first order is computed on the device."""
+    rng = np.random.default_rng(11)
+    lens = [int(x) for x in rng.integers(0, 90, size=160)]
+    lens[5] = 0
+    _say("many segments dtype=%s d=%d n_seg=%d tokens=%d" % (dtype, d, len(lens), sum(lens)))
+    w = W.segment_workload(2, lengths=lens, heads=(1, 2), dtype=dtype, d=d)
+    dv = _dev(w)
+    cu = w["cu_seqlens"]
+    res = hy.build_segment(dv["q"], dv["k"], dv["v"], dv["beta"], dv["log_alpha"], cu)
+    torch.cuda.synchronize()
+    ref = oracle.build_segments(w["q"], w["k"], w["v"], w["beta"], w["log_alpha"], cu)
+    _check_build(res, ref, cu, _all_pairs(len(lens), 2), TOL[dtype], "many segments")
+
+
 def test_build_is_deterministic_and_batch_independent(hy):
     _say("determinism / batch independence bf16 d=128")
     w = W.segment_workload(2, lengths=[300, 70, 129], heads=(2, 2))
