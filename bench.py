@@ -28,6 +28,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -58,11 +59,20 @@ KERNEL_SOURCES = {
 }
 
 
+def _code_only(src):
+    """Source text without comments, blank lines or indentation."""
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    return "\n".join(ln.strip() for ln in src.splitlines() if ln.strip())
+
+
 def kernel_source_sha256(kernel):
+    """Hash of a kernel's code (comments and layout ignored), so the HBM counter
+    record stays valid across comment-only edits and lapses on any code change."""
     h = hashlib.sha256()
     for name in KERNEL_SOURCES[kernel]:
-        with open(os.path.join(CSRC, name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(CSRC, name), encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()
 
 

@@ -21,8 +21,9 @@
 //   waves 0-1  state columns (32 each): U, Vn, outputs, S update for chunk c;
 //   waves 2-3  operator columns (32 each): X = W P0, P update for chunk c
 //              (without the operator they carry state columns too);
-//              after their update, waves 0-3 form W (hi + lo) of chunk c + 1,
-//              one 32-row d_k block each;
+//              W (hi + lo) of chunk c + 1 is formed after the first barrier by
+//              the four waves on SIMDs 2 and 3 (waves 2, 6, 3, 7), one 32-row
+//              rho block of d_k each;
 //   wave 4     inverse of chunk c + 2: Gram matrix, the four diagonal 16 x 16
 //              blocks of A1 by column-parallel substitution (DPP row
 //              broadcasts), the off-diagonal blocks of -A1 diag(beta) by
@@ -32,6 +33,10 @@
 //              fragments (wave 5, which loads K and Q once per workgroup);
 //              K^T, -A1 diag(beta) split into bf16 hi + lo, and
 //              (A1 . Gamma) diag(beta) (waves 6, 7: one half each).
+// A seam of w <= 64 tokens is one chunk: up to 16 entries of one head then run
+// back to back through the same pipeline, one entry per iteration, each state
+// wave storing the finished state and loading the next entry's incoming state
+// between iterations.
 // Each iteration has two LDS-only barriers: the consumers' state-independent
 // products read the previous iteration's fragments before the first, their
 // K^T products follow it; the producers write K^T, Q and gates for c + 1
