@@ -14,3 +14,4 @@ from .gdn import (  # noqa: F401
     compose,
     seam,
 )
+from . import families  # noqa: F401,E402  (scalar / diagonal families, RoPE, conv)
