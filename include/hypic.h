@@ -177,6 +177,80 @@ int32_t hypic_seam_rescan(const hypic_dims* dims, const void* q, const void* k,
                           float* S_post, void* workspace,
                           size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Scalar and diagonal transition families (Tab. 1 rows without the delta-rule
+ * correction; Tab. 3 compressed operators), through the same three steps.
+ *
+ * Per head and token t, with u_t = k_t v_t^T and Eq. (2):
+ *   HYPIC_FAMILY_SCALAR   (RetNet, Lightning-2, Mamba2): S_t = exp(a_t) S_{t-1} + u_t
+ *   HYPIC_FAMILY_DIAGONAL (GLA):             S_t = diag(exp(g_t)) S_{t-1} + u_t
+ *   o_t = S_t^T q_t.
+ * gate holds a_t as [T, h_v] float32 (scalar) or g_t as [T, h_v, d_k] float32
+ * (diagonal), natural-log units.  The segment operator T_C of Tab. 3 is a
+ * scalar exp(sum_t a_t) or a vector exp(sum_t g_t); it is returned as its
+ * logarithm log_decay, [n, h_v] (scalar) or [n, h_v, d_k] (diagonal), which
+ * does not underflow on long segments.
+ *
+ * The diagonal family's chunked kernel refers each key's gate to the start of
+ * its 16-token tile, so every channel's gate sum over any 16 consecutive tokens
+ * must be above -80 (float32 range; e.g. per-token gates >= -5); beyond that the
+ * outputs are undefined.  The scalar family has no such limit.
+ * dims->chunk is validated but the family kernels always run chunks of 64
+ * tokens (results do not depend on the chunk size).  Other conventions as above.
+ * ------------------------------------------------------------------------ */
+typedef enum hypic_family {
+  HYPIC_FAMILY_SCALAR = 1,
+  HYPIC_FAMILY_DIAGONAL = 2
+} hypic_family;
+
+/*
+ * hypic_family_build -- zero-start prefill of n_seg independent segments of a
+ * scalar- or diagonal-family layer (Sec. 4.2 cache tuple, Tab. 3 compressed
+ * operator).
+ *   q, k [T, h_qk, d_k] dtype; v [T, h_v, d_v] dtype; gate as above.
+ *   cu_seqlens / cu_seqlens_host, o, S_seg, workspace: as in hypic_build_segment.
+ *   log_decay   [n_seg, h_v] (scalar) or [n_seg, h_v, d_k] (diagonal) f32, or NULL.
+ * A zero-length segment yields S_seg = 0 and log_decay = 0.
+ * Returns HYPIC_EUNSUPPORTED for an unknown family.
+ */
+int32_t hypic_family_build(const hypic_dims* dims, int32_t family, const void* q,
+                           const void* k, const void* v, const float* gate,
+                           const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                           int32_t n_seg, void* o, float* S_seg, float* log_decay,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * hypic_family_compose -- Eq. (6) with the compressed operators of Tab. 3: for
+ * each request r and v-head h, S = S_prefix[r, h] (zero when NULL); for each
+ * listed segment i = seg_ids[j] in order
+ *     S_incoming[j, h] = S;   S <- exp(log_decay[i, h]) . S + S_seg[i, h]
+ * (scalar: one factor; diagonal: row c of S scaled by exp(log_decay[i, h, c]));
+ * then S_out[r, h] = S.  Arguments as in hypic_compose_segments, without P_hat;
+ * S_seg, S_prefix, S_out and S_incoming must be 16-byte aligned.  The
+ * arithmetic is float32 whatever dims->dtype says.  Workspace: none.
+ */
+int32_t hypic_family_compose(const hypic_dims* dims, int32_t family, const float* log_decay,
+                             const float* S_seg, int32_t n_pool, const int32_t* seg_ids,
+                             const int32_t* seg_ids_host, const int32_t* req_offsets,
+                             const int32_t* req_offsets_host, int32_t n_req,
+                             const float* S_prefix, float* S_out, float* S_incoming,
+                             void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * hypic_family_seam -- Sec. 4.3 seam rescan for a scalar- or diagonal-family
+ * layer: entry e runs tokens [tok_start[e], tok_start[e] + min(w, tok_len[e]))
+ * through the family's recurrence from S_in[e].  Arguments and outputs as in
+ * hypic_seam_rescan with gate in place of beta and log_alpha (w may exceed 64).
+ * Workspace: none.
+ */
+int32_t hypic_family_seam(const hypic_dims* dims, int32_t family, const void* q, const void* k,
+                          const void* v, const float* gate, int32_t n_tokens,
+                          const int32_t* tok_start, const int32_t* tok_len,
+                          const int32_t* tok_start_host, const int32_t* tok_len_host,
+                          int32_t n_entries, int32_t w, const float* S_in, void* o_seam,
+                          float* S_post, void* workspace, size_t workspace_bytes,
+                          void* stream);
+
 #ifdef __cplusplus
 }
 #endif

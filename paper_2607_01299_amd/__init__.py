@@ -9,7 +9,8 @@ from ._lib import HypicError  # noqa: F401
 def __getattr__(name):
     # the torch-facing calls load torch lazily so that the generators and the
     # library loader stay importable without it
-    if name in ("build_segment", "compose_segments", "seam_rescan", "make_dims"):
+    if name in ("build_segment", "compose_segments", "seam_rescan", "make_dims",
+                "family_build", "family_compose", "family_seam"):
         from . import ops
         return getattr(ops, name)
     raise AttributeError(name)

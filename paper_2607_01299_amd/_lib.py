@@ -30,7 +30,13 @@ EXPORTS = (
     "hypic_build_segment",
     "hypic_compose_segments",
     "hypic_seam_rescan",
+    "hypic_family_build",
+    "hypic_family_compose",
+    "hypic_family_seam",
 )
+
+HYPIC_FAMILY_SCALAR = 1
+HYPIC_FAMILY_DIAGONAL = 2
 
 
 class HypicError(RuntimeError):
@@ -80,6 +86,16 @@ def load():
         ctypes.POINTER(Dims), _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _I32, _P, _P, _P,
         _P, _SZ, _P]
     lib.hypic_seam_rescan.restype = _I32
+    lib.hypic_family_build.argtypes = [
+        ctypes.POINTER(Dims), _I32, _P, _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _SZ, _P]
+    lib.hypic_family_build.restype = _I32
+    lib.hypic_family_compose.argtypes = [
+        ctypes.POINTER(Dims), _I32, _P, _P, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _SZ, _P]
+    lib.hypic_family_compose.restype = _I32
+    lib.hypic_family_seam.argtypes = [
+        ctypes.POINTER(Dims), _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _I32, _P, _P, _P,
+        _P, _SZ, _P]
+    lib.hypic_family_seam.restype = _I32
     _lib = lib
     return lib
 

@@ -164,3 +164,96 @@ def seam_rescan(q, k, v, beta, log_alpha, tok_start, tok_len, w, S_in, *, tok_st
         _ptr(st_d), _ptr(ln_d), _hptr(st_h), _hptr(ln_h), n_e, int(w), _ptr(S_in), _ptr(o_seam),
         _ptr(S_post), None, 0, _stream(dev)))
     return o_seam, S_post
+
+
+# ---------------------------------------------------------------------------
+# scalar and diagonal transition families (Tab. 1, Tab. 3)
+# ---------------------------------------------------------------------------
+
+FAMILIES = {"scalar": _lib.HYPIC_FAMILY_SCALAR, "diagonal": _lib.HYPIC_FAMILY_DIAGONAL}
+
+
+def _family_code(family):
+    if family not in FAMILIES:
+        raise HypicError(_lib.HYPIC_EUNSUPPORTED, "family must be 'scalar' or 'diagonal'")
+    return FAMILIES[family]
+
+
+def family_build(family, q, k, v, gate, cu_seqlens, cu_seqlens_dev=None, *, want_o=True):
+    """Zero-start build of every segment of a scalar- or diagonal-family layer.
+
+    gate: [T, h_v] (scalar) or [T, h_v, d_k] (diagonal) float32, natural-log
+    units.  Returns dict(o, S_seg, log_decay); log_decay is [n_seg, h_v] or
+    [n_seg, h_v, d_k].
+    """
+    lib = _lib.load()
+    code = _family_code(family)
+    for name, t in (("q", q), ("k", k), ("v", v), ("gate", gate)):
+        _contig(t, name)
+    dev = q.device
+    dims = make_dims(q, v, 64)
+    cu_h, cu_d = _index_pair(cu_seqlens, cu_seqlens_dev, dev)
+    n_seg = len(cu_h) - 1
+    T, h_v, d_v = v.shape
+    d_k = q.shape[2]
+    o = torch.empty((T, h_v, d_v), dtype=q.dtype, device=dev) if want_o else None
+    S_seg = torch.empty((n_seg, h_v, d_k, d_v), dtype=torch.float32, device=dev)
+    ld_shape = (n_seg, h_v) if family == "scalar" else (n_seg, h_v, d_k)
+    log_decay = torch.empty(ld_shape, dtype=torch.float32, device=dev)
+    ws, ws_bytes = _workspace(_lib.HYPIC_OP_BUILD, dims, n_seg, dev)
+    _lib.check(lib.hypic_family_build(
+        ctypes.byref(dims), code, _ptr(q), _ptr(k), _ptr(v), _ptr(gate), _ptr(cu_d),
+        _hptr(cu_h), n_seg, _ptr(o), _ptr(S_seg), _ptr(log_decay), _ptr(ws), ws_bytes,
+        _stream(dev)))
+    return {"o": o, "S_seg": S_seg, "log_decay": log_decay}
+
+
+def family_compose(family, log_decay, S_seg, seg_ids, req_offsets, S_prefix=None, *,
+                   seg_ids_dev=None, req_offsets_dev=None, want_incoming=True):
+    """Eq. (6) with the compressed operators of Tab. 3 for each request (CSR
+    lists).  Returns (S_out, S_incoming or None)."""
+    lib = _lib.load()
+    code = _family_code(family)
+    for name, t in (("log_decay", log_decay), ("S_seg", S_seg)):
+        _contig(t, name)
+    dev = S_seg.device
+    n_pool, h_v, d_k, d_v = S_seg.shape
+    dims = Dims(h_qk=h_v, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_lib.HYPIC_F32, chunk=64)
+    ids_h, ids_d = _index_pair(seg_ids, seg_ids_dev, dev)
+    off_h, off_d = _index_pair(req_offsets, req_offsets_dev, dev)
+    n_req = len(off_h) - 1
+    nnz = int(off_h[-1]) if len(off_h) else 0
+    S_out = torch.empty((max(n_req, 0), h_v, d_k, d_v), dtype=torch.float32, device=dev)
+    S_inc = (torch.empty((nnz, h_v, d_k, d_v), dtype=torch.float32, device=dev)
+             if want_incoming else None)
+    if S_prefix is not None:
+        _contig(S_prefix, "S_prefix")
+    _lib.check(lib.hypic_family_compose(
+        ctypes.byref(dims), code, _ptr(log_decay), _ptr(S_seg), n_pool, _ptr(ids_d),
+        _hptr(ids_h), _ptr(off_d), _hptr(off_h), n_req, _ptr(S_prefix), _ptr(S_out),
+        _ptr(S_inc), None, 0, _stream(dev)))
+    return S_out, S_inc
+
+
+def family_seam(family, q, k, v, gate, tok_start, tok_len, w, S_in, *, tok_start_dev=None,
+                tok_len_dev=None, want_post=True):
+    """Seam rescan of each entry's first min(w, tok_len) tokens from S_in for a
+    scalar- or diagonal-family layer.  Returns (o_seam, S_post or None)."""
+    lib = _lib.load()
+    code = _family_code(family)
+    for name, t in (("q", q), ("k", k), ("v", v), ("gate", gate), ("S_in", S_in)):
+        _contig(t, name)
+    dev = q.device
+    dims = make_dims(q, v, 64)
+    st_h, st_d = _index_pair(tok_start, tok_start_dev, dev)
+    ln_h, ln_d = _index_pair(tok_len, tok_len_dev, dev)
+    n_e = len(st_h)
+    T, h_v, d_v = v.shape
+    d_k = q.shape[2]
+    o_seam = torch.empty((n_e, w, h_v, d_v), dtype=q.dtype, device=dev)
+    S_post = torch.empty((n_e, h_v, d_k, d_v), dtype=torch.float32, device=dev) if want_post else None
+    _lib.check(lib.hypic_family_seam(
+        ctypes.byref(dims), code, _ptr(q), _ptr(k), _ptr(v), _ptr(gate), T, _ptr(st_d),
+        _ptr(ln_d), _hptr(st_h), _hptr(ln_h), n_e, int(w), _ptr(S_in), _ptr(o_seam),
+        _ptr(S_post), None, 0, _stream(dev)))
+    return o_seam, S_post

@@ -188,3 +188,33 @@ def pool_workload(seed=None, n_pool=512, n_req=256, n_min=8, n_max=64,
             "tok_start": tok_start, "tok_len": tok_len, "w": w,
             "h_qk": heads, "h_v": heads, "d_k": d, "d_v": d, "dtype": BF16,
             "chunk": 64, "cfg": 5, "seed": seed, "n_pool": n_pool}
+
+
+# --------------------------------------------------------------------------
+# gates of the scalar and diagonal transition families (Tab. 1)
+# --------------------------------------------------------------------------
+
+def family_gate(family, T, h_v, d_k, seed, kind="softplus"):
+    """Log-gates of the scalar ([T, h_v]) or diagonal ([T, h_v, d_k]) family,
+    float32, natural-log units, drawn from their own seeded stream.
+
+    kind: "softplus"   a = -0.05 softplus(N(0, 1)) (the GDN gate distribution,
+                       per channel for the diagonal family);
+          "logsigmoid" a = log sigmoid(N(0, 1)) (un-normalised GLA-style gates,
+                       strong decay: mean about -0.8 per token);
+          "retnet"     scalar only: RetNet's fixed per-head decays
+                       gamma_h = 1 - 2^(-5 - h), for every token.
+    """
+    rng = np.random.default_rng(seed)
+    shape = (T, h_v) if family == "scalar" else (T, h_v, d_k)
+    if kind == "retnet":
+        if family != "scalar":
+            raise ValueError("retnet gates are scalar")
+        gam = 1.0 - 2.0 ** (-5.0 - np.arange(h_v, dtype=np.float64))
+        return np.broadcast_to(np.log(gam).astype(np.float32), shape).copy()
+    x = rng.standard_normal(shape, dtype=np.float32)
+    if kind == "softplus":
+        return (-0.05 * _softplus(x)).astype(np.float32)
+    if kind == "logsigmoid":
+        return (-_softplus(-x)).astype(np.float32)
+    raise ValueError(kind)

@@ -151,3 +151,51 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_lib, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(_lib.HypicError):
         _lib.load()
+
+
+def _fbuild(lib, family, cu, gate=FAKE, dims=None):
+    cu = np.asarray(cu, dtype=np.int32)
+    d = _dims() if dims is None else dims
+    return lib.hypic_family_build(
+        ctypes.byref(d), family, FAKE, FAKE, FAKE, gate, FAKE, cu.ctypes.data_as(ctypes.c_void_p),
+        len(cu) - 1, FAKE, FAKE, FAKE, FAKE, 1 << 20, None)
+
+
+def _fcompose(lib, family, ids, offs, n_pool=8, S_out=FAKE, S_seg=FAKE):
+    ids = np.asarray(ids, dtype=np.int32)
+    offs = np.asarray(offs, dtype=np.int32)
+    return lib.hypic_family_compose(
+        ctypes.byref(_dims()), family, FAKE, S_seg, n_pool, FAKE,
+        ids.ctypes.data_as(ctypes.c_void_p), FAKE, offs.ctypes.data_as(ctypes.c_void_p),
+        len(offs) - 1, None, S_out, None, None, 0, None)
+
+
+def _fseam(lib, family, start, length, w=8, n_tokens=100, gate=FAKE):
+    st = np.asarray(start, dtype=np.int32)
+    ln = np.asarray(length, dtype=np.int32)
+    return lib.hypic_family_seam(
+        ctypes.byref(_dims()), family, FAKE, FAKE, FAKE, gate, n_tokens, FAKE, FAKE,
+        st.ctypes.data_as(ctypes.c_void_p), ln.ctypes.data_as(ctypes.c_void_p), len(st), w,
+        FAKE, FAKE, None, None, 0, None)
+
+
+@pytest.mark.parametrize("family", [_lib.HYPIC_FAMILY_SCALAR, _lib.HYPIC_FAMILY_DIAGONAL])
+def test_family_calls_reject_bad_arguments(lib, family):
+    assert _fbuild(lib, family, [0, 10, 5]) == _lib.HYPIC_EINVAL
+    assert _fbuild(lib, family, [0, 10], gate=None) == _lib.HYPIC_EINVAL
+    assert _fbuild(lib, family, [0, 10], dims=_dims(d_k=96)) == _lib.HYPIC_EUNSUPPORTED
+    assert _fbuild(lib, family, [0]) == _lib.HYPIC_OK
+    assert _fcompose(lib, family, [0, 8], [0, 2]) == _lib.HYPIC_EINVAL
+    assert _fcompose(lib, family, [0, 1], [0, 2], S_out=FAKE_ODD) == _lib.HYPIC_EINVAL
+    assert _fcompose(lib, family, [0, 1], [0, 2], S_seg=None) == _lib.HYPIC_EINVAL
+    assert _fcompose(lib, family, [], [0]) == _lib.HYPIC_OK
+    assert _fseam(lib, family, [0, 95], [10, 10]) == _lib.HYPIC_EINVAL
+    assert _fseam(lib, family, [0], [4], gate=None) == _lib.HYPIC_EINVAL
+    assert _fseam(lib, family, [], []) == _lib.HYPIC_OK
+
+
+@pytest.mark.parametrize("family", [0, 3, -1])
+def test_family_calls_reject_unknown_family(lib, family):
+    assert _fbuild(lib, family, [0, 10]) == _lib.HYPIC_EUNSUPPORTED
+    assert _fcompose(lib, family, [0], [0, 1]) == _lib.HYPIC_EUNSUPPORTED
+    assert _fseam(lib, family, [0], [4]) == _lib.HYPIC_EUNSUPPORTED
