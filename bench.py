@@ -271,6 +271,87 @@ def bench_compose_burst(torch, steps, warmup):
     }
 
 
+def family_build_bytes(family, T, h_qk, h_v, d_k, d_v, n_seg):
+    """Algorithmic HBM bytes of one family build launch: q, k, v read and o
+    written in bf16, the gates read in float32, S_seg and log_decay written."""
+    g = 1 if family == "scalar" else d_k
+    return (T * (2 * h_qk * d_k * 2 + 2 * h_v * d_v * 2 + h_v * g * 4)
+            + n_seg * h_v * (d_k * d_v * 4 + g * 4))
+
+
+def family_compose_bytes_per_head_step(family, d_k, d_v):
+    # read S_i and log_decay_i, write the incoming state
+    return 2 * 4 * d_k * d_v + 4 * (1 if family == "scalar" else d_k)
+
+
+def _events_ms(torch, stream, fn, reps):
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def bench_families(torch, steps, warmup, seam_w):
+    """Scalar and diagonal families (Tab. 1) on the bench workload: the whole
+    family step (build, composition of the batch in order, seams) and the
+    build kernel's HBM roofline; then a serve-time burst over a pool of family
+    tuples with the configuration-5 request lists."""
+    from paper_2607_01299_amd.pipeline import FamilyComposeBurst, FamilyPipeline
+    w = W.segment_workload(2)
+    q, k, v, _, _ = _to_dev(w, torch)
+    T = int(w["cu_seqlens"][-1])
+    h_qk, h_v, d_k, d_v = int(w["q"].shape[1]), int(w["v"].shape[1]), w["d_k"], w["d_v"]
+    n_seg = len(w["lengths"])
+    p = W.pool_workload()
+    S_pool = torch.from_numpy(p["S_seg"]).cuda()
+    out = {}
+    for family in ("scalar", "diagonal"):
+        gate = torch.from_numpy(W.family_gate(family, T, h_v, d_k, w["seed"] + 1000)).cuda()
+        pipe = FamilyPipeline(family, q, k, v, gate, w["cu_seqlens"], seam_w=seam_w)
+        for _ in range(warmup):
+            pipe.run()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            pipe.run()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / steps
+        build_ms = _events_ms(torch, pipe.stream, pipe.build, steps)
+        byts = float(family_build_bytes(family, T, h_qk, h_v, d_k, d_v, n_seg))
+        gbs = byts / (build_ms * 1e-3) / 1e9
+        # pool of family tuples: the configuration-5 states, per-channel or
+        # scalar log-decays ~ U(-3, 0)
+        rng = np.random.default_rng(p["seed"] + 7)
+        ld_shape = (p["n_pool"], h_v) if family == "scalar" else (p["n_pool"], h_v, d_k)
+        ld = torch.from_numpy(rng.uniform(-3.0, 0.0, size=ld_shape).astype(np.float32)).cuda()
+        burst = FamilyComposeBurst(family, ld, S_pool, p["seg_ids"], p["req_offsets"])
+        burst.compose()
+        comp_ms = _events_ms(torch, burst.stream, burst.compose, max(steps // 2, 3))
+        cbytes = float(family_compose_bytes_per_head_step(family, d_k, d_v)) * burst.nnz * h_v
+        cgbs = cbytes / (comp_ms * 1e-3) / 1e9
+        out[family] = {
+            "tokens_per_s": T / dt,
+            "ms_per_step": dt * 1e3,
+            "build_ms": build_ms,
+            "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                         "frac": gbs / PEAK_HBM_GBS, "traffic": None,
+                         "kernel": "family_scan_kernel (build)", "bytes_per_launch": byts},
+            "compose_burst": {"compositions_per_s": burst.nnz / (comp_ms * 1e-3),
+                              "compose_ms": comp_ms,
+                              "roofline": {"bound": "hbm", "achieved": cgbs,
+                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                           "frac": cgbs / PEAK_HBM_GBS, "traffic": None,
+                                           "kernel": "family_compose_kernel",
+                                           "bytes_per_launch": cbytes}},
+        }
+        del pipe, burst
+    return {"workload": W.CONFIG_NAMES[2] + "; gates from workloads.family_gate (softplus)",
+            "burst_workload": W.CONFIG_NAMES[5] + " (family tuples)", **out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -280,6 +361,10 @@ def main():
     ap.add_argument("--seam-w", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-burst", action="store_true")
+    ap.add_argument("--no-families", action="store_true",
+                    help="skip the scalar / diagonal family legs")
+    ap.add_argument("--families-only", action="store_true",
+                    help="run only the scalar / diagonal family legs (profiling)")
     ap.add_argument("--no-segments", action="store_true",
                     help="skip the segment step (profiling the burst alone)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -296,7 +381,7 @@ def main():
         copy_calibration(torch)
         return
     cpu = None
-    if not args.no_cpu_baseline and not args.no_segments:
+    if not args.no_cpu_baseline and not args.no_segments and not args.families_only:
         wl = W.segment_workload(args.config)
         cpu = cpu_baseline(args.config, int(wl["v"].shape[1]))
         print("[bench] cpu baseline done: %.1f tokens/s" % cpu["value"], file=sys.stderr,
@@ -308,6 +393,10 @@ def main():
         sys.exit(1)
     from paper_2607_01299_amd import _lib
     _lib.load()
+    if args.families_only:
+        print(json.dumps({"families": bench_families(torch, args.steps, args.warmup,
+                                                     args.seam_w)}))
+        return
     if args.no_segments:
         burst = bench_compose_burst(torch, max(args.steps // 2, 3), max(args.warmup // 2, 1))
         print(json.dumps({"compose_burst": burst}))
@@ -318,6 +407,8 @@ def main():
           flush=True)
     burst = None if args.no_burst else bench_compose_burst(torch, max(args.steps // 2, 3),
                                                            max(args.warmup // 2, 1))
+    fam = None if args.no_families else bench_families(torch, args.steps, args.warmup,
+                                                         args.seam_w)
     value = seg["tokens"] / (seg["ms_per_step"] * 1e-3)
     out = {
         "metric": METRIC,
@@ -338,6 +429,7 @@ def main():
         "build_ms_in_step": seg["build_ms_in_step"],
         "cpu_baseline": cpu,
         "compose_burst": burst,
+        "families": fam,
     }
     print(json.dumps(out))
 

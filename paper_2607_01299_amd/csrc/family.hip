@@ -27,7 +27,9 @@
 // scalar path has no such limit.
 //
 // Organisation: one workgroup of 4 waves runs one (segment or seam entry,
-// v-head, 64-column block) chain over its chunks in order.  Each wave owns 16
+// v-head, 64-column block) chain over its chunks in order.  Its barriers wait
+// for LDS traffic only, so the next chunk's global loads and this chunk's
+// output stores stay in flight across them.  Each wave owns 16
 // state columns with all d_k rows in registers.  Per chunk the workgroup
 // stages Q, K and its V columns in LDS (register prefetch of the next chunk
 // runs meanwhile), forms the gate prefix and the decayed operands, the
@@ -50,9 +52,14 @@ namespace hypic {
 
 namespace {
 
-constexpr int kFT = 256;  // threads of a scan workgroup
+constexpr int kFT = 512;  // threads of a scan workgroup (8 waves)
 constexpr int FC = 64;    // tokens per chunk
-constexpr int FNC = 64;   // state columns per scan workgroup
+// State columns per scan workgroup: 64, or 32 for float32 inputs at d_k = 128
+// (whose operands would not fit in LDS with 64)
+template <typename ST, int DK>
+constexpr int fnc_of() {
+  return (sizeof(ST) == 4 && DK == 128) ? 32 : 64;
+}
 
 typedef unsigned short u16;
 typedef u16 u16x4 __attribute__((ext_vector_type(4)));
@@ -72,13 +79,11 @@ template <>
 struct Frag<u16> {
   bf16x8 x;
   __device__ void set(int j, float v) { x[j] = static_cast<__bf16>(v); }
-  __device__ void set_raw(int j, u16 b) { x[j] = __builtin_bit_cast(__bf16, b); }
 };
 template <>
 struct Frag<float> {
   float x[8];
   __device__ void set(int j, float v) { x[j] = v; }
-  __device__ void set_raw(int j, float b) { x[j] = b; }
 };
 
 __device__ __forceinline__ f32x4 mma(const Frag<u16>& a, const Frag<u16>& b, f32x4 c) {
@@ -90,64 +95,59 @@ __device__ __forceinline__ f32x4 mma(const Frag<float>& a, const Frag<float>& b,
   return c;
 }
 
-// slot j = M[row][kb + kap(g, j)] (contraction index contiguous in memory)
-template <typename ST>
-__device__ __forceinline__ Frag<ST> frag_row(const ST* M, int ld, int row, int kb, int g) {
-  Frag<ST> f;
-  const ST* p = M + row * ld + kb + 4 * g;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    f.set_raw(j, p[j]);
-    f.set_raw(4 + j, p[16 + j]);
-  }
+// slot j = M[row][kb + kap(g, j)]: two 8-byte (bf16) or 16-byte (float) loads
+__device__ __forceinline__ Frag<u16> frag_row(const u16* M, int ld, int row, int kb, int g) {
+  const u16* p = M + row * ld + kb + 4 * g;
+  const u16x4 lo = *reinterpret_cast<const u16x4*>(p);
+  const u16x4 hi = *reinterpret_cast<const u16x4*>(p + 16);
+  Frag<u16> f;
+  f.x = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  return f;
+}
+__device__ __forceinline__ Frag<float> frag_row(const float* M, int ld, int row, int kb, int g) {
+  const float* p = M + row * ld + kb + 4 * g;
+  const float4 lo = *reinterpret_cast<const float4*>(p);
+  const float4 hi = *reinterpret_cast<const float4*>(p + 16);
+  Frag<float> f;
+  f.x[0] = lo.x; f.x[1] = lo.y; f.x[2] = lo.z; f.x[3] = lo.w;
+  f.x[4] = hi.x; f.x[5] = hi.y; f.x[6] = hi.z; f.x[7] = hi.w;
   return f;
 }
 // slot j = M[row][kb + kap(g, j)] * s[kb + kap(g, j)]
 template <typename ST>
 __device__ __forceinline__ Frag<ST> frag_row_scaled(const ST* M, int ld, int row, int kb, int g,
                                                     const float* s) {
-  Frag<ST> f;
-  const ST* p = M + row * ld + kb + 4 * g;
-  const float* q = s + kb + 4 * g;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    f.set(j, ldv(p + j) * q[j]);
-    f.set(4 + j, ldv(p + 16 + j) * q[16 + j]);
-  }
-  return f;
-}
-// slot j = M[kb + kap(g, j)][col] (contraction index strided)
-template <typename ST>
-__device__ __forceinline__ Frag<ST> frag_col(const ST* M, int ld, int col, int kb, int g) {
+  const Frag<ST> raw = frag_row(M, ld, row, kb, g);
+  const float4 s0 = *reinterpret_cast<const float4*>(s + kb + 4 * g);
+  const float4 s1 = *reinterpret_cast<const float4*>(s + kb + 16 + 4 * g);
+  const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
   Frag<ST> f;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) f.set_raw(j, M[(kb + kap(g, j)) * ld + col]);
+  for (int j = 0; j < 8; ++j) f.set(j, static_cast<float>(raw.x[j]) * sv[j]);
   return f;
 }
 
 template <int FAM, typename ST, int DK>
 struct FamLds {
+  static constexpr int FNC = fnc_of<ST, DK>();
   static constexpr int PAD = (sizeof(ST) == 2) ? 8 : 4;
-  static constexpr int LDK = DK + PAD;   // Q, K rows
-  static constexpr int LDV = FNC + PAD;  // V rows (this workgroup's columns)
-  static constexpr int LDA = FC + PAD;   // A rows
-  static constexpr int NPART = kFT / DK; // token parts of the per-channel prefix
-  ST q[FC * LDK];   // Q, then (diagonal) Q . exp(B - Bbar)
-  ST k[FC * LDK];   // K, then (diagonal) K . exp(Bbar - B)
-  ST v[FC * LDV];
-  ST a[FC * LDA];   // A (lower-triangular 16 x 16 tiles; the upper tiles read stay 0)
-  // scalar family: b (prefix of the gate), exp(b), exp(b_last - b)
-  float bc[FC], gam[FC], dec[FC];
-  // diagonal family, per channel: part totals, Bbar of each 16-token tile,
-  // exp(Bbar_tq - Bbar_tk) for the six tile pairs tk < tq, exp(Bbar), exp(B_last - Bbar),
-  // exp(B_last), B_last
-  float part[NPART * DK];
-  float hb[4 * DK];
+  static constexpr int LDK = DK + PAD;  // Q, K rows (token-major)
+  static constexpr int LDT = FC + PAD;  // rows of the token-minor operands and of A
+  ST q[FC * LDK];     // Q, then (diagonal) Q . exp(B - Bbar)
+  ST k[FC * LDK];     // K, then (diagonal) K . exp(Bbar - B)
+  ST kdt[DK * LDT];   // (K . exp(B_last - B))^T: channel-major
+  ST vt[FNC * LDT];   // V^T of this workgroup's columns: column-major
+  ST a[FC * LDT];     // A (lower 16 x 16 tiles; the upper tiles read stay 0)
+  Frag<ST> s0f[FNC / 16][DK / 32][64];  // S0 as B fragments: column group, 32-row block, lane
+  // scalar family: prefix b of the gate, exp(b)
+  float bc[FC], gam[FC];
+  // diagonal family, per channel: totals of the four 16-token tiles,
+  // exp(Bbar_tq - Bbar_tk) for the six tile pairs tk < tq, exp(Bbar) per tile,
+  // exp(B_last)
+  float part[4 * DK];
   float fx[6 * DK];
   float hx[4 * DK];
-  float gx[4 * DK];
   float lx[DK];
-  float bl[DK];
 };
 
 // index of the tile pair (tq, tk), tk < tq, in fx
@@ -157,19 +157,74 @@ __device__ __forceinline__ int fam_segment_of_rank(const FamArgs& a, int rank) {
   return a.n_inline > 0 ? static_cast<int>(a.order_inline[rank]) : a.order[rank];
 }
 
+// eight consecutive elements of one row, packed for one 16-byte (bf16) or two
+// 16-byte (float) LDS stores
+__device__ __forceinline__ void st8(u16* p, const float (&x)[8]) {
+  bf16x8 b;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) b[j] = static_cast<__bf16>(x[j]);
+  *reinterpret_cast<bf16x8*>(p) = b;
+}
+__device__ __forceinline__ void st8(float* p, const float (&x)[8]) {
+  *reinterpret_cast<float4*>(p) = make_float4(x[0], x[1], x[2], x[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(x[4], x[5], x[6], x[7]);
+}
+// element e of a 16-byte register load of the input type, and its raw bits
+__device__ __forceinline__ uint32_t word_of(const uint4& w, int i) {
+  return (i == 0) ? w.x : ((i == 1) ? w.y : ((i == 2) ? w.z : w.w));
+}
+__device__ __forceinline__ float elem(const uint4& w, int e, const u16*) {
+  const uint32_t word = word_of(w, e >> 1);
+  return __uint_as_float((e & 1) ? (word & 0xffff0000u) : (word << 16));
+}
+__device__ __forceinline__ float elem(const uint4& w, int e, const float*) {
+  return __uint_as_float(word_of(w, e));
+}
+__device__ __forceinline__ void put_raw(u16* p, const uint4& w, int e) {
+  const uint32_t word = word_of(w, e >> 1);
+  *p = static_cast<u16>((e & 1) ? (word >> 16) : (word & 0xffffu));
+}
+__device__ __forceinline__ void put_raw(float* p, const uint4& w, int e) {
+  *p = __uint_as_float(word_of(w, e));
+}
+
+// Buffer resources over [base, base + bytes): loads past the end return zero and
+// stores past it are dropped by the hardware, so a partial chunk needs no
+// branch around its memory operations (and every iteration issues the same
+// number of them, which keeps the compiler's waits on earlier loads partial).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc(const void* base, long bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0,
+                                           static_cast<int>(bytes > 0 ? bytes : 0), 0x00020000);
+}
+__device__ __forceinline__ uint4 bload16(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float bload4(__amdgpu_buffer_rsrc_t r, int off) {
+  return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+__device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, int off, float x, u16*) {
+  __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(u16, static_cast<__bf16>(x)), r, off,
+                                        0, 0);
+}
+__device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, int off, float x, float*) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, off, 0, 0);
+}
+
 template <int FAM, typename ST, int DK, int DV>
 __global__ __launch_bounds__(kFT) void family_scan_kernel(FamArgs args) {
   using L = FamLds<FAM, ST, DK>;
-  constexpr int LDK = L::LDK, LDV = L::LDV, LDA = L::LDA;
+  constexpr int LDK = L::LDK, LDT = L::LDT;
+  constexpr int FNC = L::FNC;
+  constexpr int NCG = FNC / 16;                            // column groups of 16
+  constexpr int NRG = 8 / NCG;                             // row groups (waves per group)
   constexpr int VEC = 16 / static_cast<int>(sizeof(ST));  // elements per 16-byte load
   constexpr int NQ = FC * DK / (VEC * kFT);                // 16-byte loads of Q (and K)
   constexpr int NV = FC * FNC / (VEC * kFT);               // 16-byte loads of V
-  constexpr int NM = DK / 16;                              // state row tiles
-  constexpr int NPART = L::NPART;
-  constexpr int TPC = FC / NPART;                          // tokens per prefix part
+  constexpr int NMH = DK / (16 * NRG);                     // state row tiles per wave
+  constexpr int NOT = 4 / NRG;                             // output token tiles per wave
   constexpr bool DIAG = FAM == FAM_DIAGONAL;
   static_assert(NQ >= 1 && NV >= 1, "tile split");
-  static_assert(TPC % 16 == 0, "prefix parts must hold whole 16-token tiles");
+  static_assert(NMH % 2 == 0, "a wave's state rows must be whole 32-row blocks");
   static_assert(sizeof(L) <= 160 * 1024, "LDS budget");
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
@@ -179,6 +234,7 @@ __global__ __launch_bounds__(kFT) void family_scan_kernel(FamArgs args) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
   const int g = lane >> 4, ln = lane & 15;
+  const int cg = wave % NCG, rgrp = wave / NCG;  // this wave's column group and row group
 
   // ---- work item: XCD-aware numbering of the column blocks of one chain ----
   constexpr int n_cb = DV / FNC;
@@ -217,91 +273,99 @@ __global__ __launch_bounds__(kFT) void family_scan_kernel(FamArgs args) {
   const ST* kg = static_cast<const ST*>(args.k) + hk * DK;
   const ST* vg = static_cast<const ST*>(args.v) + h * DV + cb * FNC;
   const long sh = static_cast<long>(seg) * args.h_v + h;
-  const int col16 = 16 * wave;          // this wave's columns inside the block
+  const int col16 = 16 * cg;            // this wave's columns inside the block
   const int col = cb * FNC + col16;     // ... and in the state
+  const int row0 = rgrp * (DK / NRG);     // this wave's first state row
 
-  // ---- state columns col .. col + 15, all d_k rows ----
-  f32x4 st[NM];
+  // ---- state: rows row0 .. row0 + DK/2 - 1, columns col .. col + 15 ----
+  f32x4 st[NMH];
   if (args.mode == 1) {
     const float* s_in = args.S_in + sh * DK * DV + col + ln;
 #pragma unroll
-    for (int mt = 0; mt < NM; ++mt)
+    for (int mt = 0; mt < NMH; ++mt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) st[mt][i] = s_in[(mt * 16 + 4 * g + i) * DV];
+      for (int i = 0; i < 4; ++i) st[mt][i] = s_in[(row0 + mt * 16 + 4 * g + i) * DV];
   } else {
 #pragma unroll
-    for (int mt = 0; mt < NM; ++mt) st[mt] = zero4();
+    for (int mt = 0; mt < NMH; ++mt) st[mt] = zero4();
   }
 
   // the upper tiles of A read by the A V products, (0, 1) and (2, 3), stay zero
-  for (int idx = tid; idx < 2 * 256; idx += kFT) {
-    const int t = idx >> 8, e = idx & 255;
-    const int r = 32 * t + (e >> 4), c = 32 * t + 16 + (e & 15);
-    stv(sm.a + r * LDA + c, 0.f);
+  {
+    const int t = tid >> 8, e = tid & 255;
+    stv(sm.a + (32 * t + (e >> 4)) * LDT + 32 * t + 16 + (e & 15), 0.f);
   }
 
   // ---- register prefetch of one chunk ----
+  // Q, K, V: token-major 16-byte pieces.  Gates: scalar, lane = token (every
+  // wave holds the chunk's 64 gates); diagonal, thread (channel pc, tile pt)
+  // holds the 16 gates of its channel in its tile (threads below 4 d_k).
   uint4 rq[NQ], rk[NQ], rv[NV];
-  float rg[DIAG ? TPC : 1];
-  const int gc = tid % DK, gpart = tid / DK;  // diagonal prefix: channel, token part
+  float rg[DIAG ? 16 : 1];
+  const int pc = tid % DK, pt = tid / DK;
+  const bool gate_thread = !DIAG || tid < 4 * DK;
+  // n tokens from c0 (n <= 0 past the end: nothing is read, zeros arrive)
   auto prefetch = [&](int c0, int n) __attribute__((always_inline)) {
+    constexpr int SZ = static_cast<int>(sizeof(ST));
+    const auto rsq = rsrc(qg + static_cast<long>(c0) * qk_stride, n * qk_stride * SZ);
+    const auto rsk = rsrc(kg + static_cast<long>(c0) * qk_stride, n * qk_stride * SZ);
+    const auto rsv = rsrc(vg + static_cast<long>(c0) * v_stride, n * v_stride * SZ);
 #pragma unroll
     for (int u = 0; u < NQ; ++u) {
       const int idx = u * kFT + tid;
       const int r = idx / (DK / VEC), cv = idx % (DK / VEC);
-      const long off = static_cast<long>(c0 + r) * qk_stride + cv * VEC;
-      rq[u] = (r < n) ? *reinterpret_cast<const uint4*>(qg + off) : make_uint4(0, 0, 0, 0);
-      rk[u] = (r < n) ? *reinterpret_cast<const uint4*>(kg + off) : make_uint4(0, 0, 0, 0);
+      const int off = static_cast<int>((r * qk_stride + cv * VEC) * SZ);
+      rq[u] = bload16(rsq, off);
+      rk[u] = bload16(rsk, off);
     }
 #pragma unroll
     for (int u = 0; u < NV; ++u) {
       const int idx = u * kFT + tid;
       const int r = idx / (FNC / VEC), cv = idx % (FNC / VEC);
-      rv[u] = (r < n) ? *reinterpret_cast<const uint4*>(vg + static_cast<long>(c0 + r) * v_stride +
-                                                         cv * VEC)
-                      : make_uint4(0, 0, 0, 0);
+      rv[u] = bload16(rsv, static_cast<int>((r * v_stride + cv * VEC) * SZ));
     }
     if constexpr (DIAG) {
+      const long gs = static_cast<long>(args.h_v) * DK;  // gate elements per token
+      const auto rsg = rsrc(args.gate + static_cast<long>(c0) * gs, n * gs * 4);
 #pragma unroll
-      for (int j = 0; j < TPC; ++j) {
-        const int r = gpart * TPC + j;
-        rg[j] = (r < n) ? args.gate[(static_cast<long>(c0 + r) * args.h_v + h) * DK + gc] : 0.f;
-      }
+      for (int j = 0; j < 16; ++j)
+        rg[j] = bload4(rsg, static_cast<int>(((16 * pt + j) * gs + h * DK + pc) * 4));
     } else {
-      rg[0] = (tid < n) ? args.gate[static_cast<long>(c0 + tid) * args.h_v + h] : 0.f;
+      const auto rsg = rsrc(args.gate + static_cast<long>(c0) * args.h_v, n * args.h_v * 4);
+      rg[0] = bload4(rsg, (lane * args.h_v + h) * 4);
     }
   };
   if (lo < hi) prefetch(lo, (hi - lo < FC) ? hi - lo : FC);
-  float ld_acc = 0.f;  // log_decay: wave 0 (scalar) or thread c < DK (diagonal)
+  {
+    // As many (dropped) stores as a chunk's outputs: every path into the chunk
+    // loop then has the same number of memory operations behind the prefetch,
+    // so the waits for it do not extend to the previous chunk's output stores.
+    const auto none = rsrc(nullptr, 0);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 4 * NOT; ++i) bstore(none, 64 * i, 0.f, static_cast<ST*>(nullptr));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  float ld_acc = 0.f;  // log_decay: every lane (scalar) or thread c < DK (diagonal)
 
   for (int c0 = lo; c0 < hi; c0 += FC) {
     const int n = (hi - c0 < FC) ? hi - c0 : FC;
-    __syncthreads();  // the previous chunk is done with every LDS buffer
+    lds_barrier();  // the previous chunk is done with every LDS buffer
 
-    // ---- P0: stage the chunk; gate prefix ----
+    // ---- P0: publish S0; stage Q, K (token-major) and V^T; gate prefix;
+    // (scalar) the decayed keys, channel-major ----
 #pragma unroll
-    for (int u = 0; u < NQ; ++u) {
-      const int idx = u * kFT + tid;
-      const int r = idx / (DK / VEC), cv = idx % (DK / VEC);
-      *reinterpret_cast<uint4*>(sm.q + r * LDK + cv * VEC) = rq[u];
-      *reinterpret_cast<uint4*>(sm.k + r * LDK + cv * VEC) = rk[u];
-    }
+    for (int kl = 0; kl < NMH / 2; ++kl) {
+      Frag<ST> f;
 #pragma unroll
-    for (int u = 0; u < NV; ++u) {
-      const int idx = u * kFT + tid;
-      const int r = idx / (FNC / VEC), cv = idx % (FNC / VEC);
-      *reinterpret_cast<uint4*>(sm.v + r * LDV + cv * VEC) = rv[u];
-    }
-    float pre[DIAG ? TPC : 1];
-    if constexpr (DIAG) {
-      float run = 0.f;
-#pragma unroll
-      for (int j = 0; j < TPC; ++j) {
-        run += rg[j];
-        pre[j] = run;
+      for (int i = 0; i < 4; ++i) {
+        f.set(i, st[2 * kl][i]);
+        f.set(4 + i, st[2 * kl + 1][i]);
       }
-      sm.part[gpart * DK + gc] = run;
-    } else if (wave == 0) {
+      sm.s0f[cg][rgrp * (NMH / 2) + kl][lane] = f;
+    }
+    float dec_l = 0.f, b_l = 0.f;  // scalar: exp(b_last - b) and b of token `lane`
+    if constexpr (!DIAG) {
       float b = rg[0];
 #pragma unroll
       for (int off = 1; off < 64; off <<= 1) {
@@ -309,57 +373,96 @@ __global__ __launch_bounds__(kFT) void family_scan_kernel(FamArgs args) {
         if (lane >= off) b += u;
       }
       const float b_last = __shfl(b, 63, 64);
-      sm.bc[lane] = b;
-      sm.gam[lane] = __expf(b);
-      sm.dec[lane] = __expf(b_last - b);
+      b_l = b;
+      dec_l = __expf(b_last - b);
       ld_acc += b_last;
+      if (wave == 0) {
+        sm.bc[lane] = b;
+        sm.gam[lane] = __expf(b);
+      }
     }
-    if (c0 + FC < hi) prefetch(c0 + FC, (hi - c0 - FC < FC) ? hi - c0 - FC : FC);
-    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < NQ; ++u) {
+      const int idx = u * kFT + tid;
+      const int r = idx / (DK / VEC), cv = idx % (DK / VEC);
+      *reinterpret_cast<uint4*>(sm.q + r * LDK + cv * VEC) = rq[u];
+      *reinterpret_cast<uint4*>(sm.k + r * LDK + cv * VEC) = rk[u];
+      if constexpr (!DIAG) {
+        const float d = __shfl(dec_l, r, 64);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+          stv(sm.kdt + (cv * VEC + e) * LDT + r, elem(rk[u], e, static_cast<const ST*>(nullptr)) * d);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int idx = u * kFT + tid;
+      const int r = idx / (FNC / VEC), cv = idx % (FNC / VEC);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) put_raw(sm.vt + (cv * VEC + e) * LDT + r, rv[u], e);
+    }
+    float pre[DIAG ? 16 : 1];
+    if constexpr (DIAG) {
+      if (gate_thread) {
+        float run = 0.f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          run += rg[j];
+          pre[j] = run;
+        }
+        sm.part[pt * DK + pc] = run;
+      }
+    }
+    prefetch(c0 + FC, (hi - c0 - FC < FC) ? hi - c0 - FC : FC);
+    lds_barrier();
 
     if constexpr (DIAG) {
-      // ---- P1: per-channel prefix B, tile references Bbar, decayed Q and K ----
-      float off = 0.f;
+      // ---- P1: thread (channel pc, tile pt): the tile-referred Q and K, the
+      // decayed keys (channel-major) and the per-channel tile factors ----
+      if (gate_thread) {
+        float hbv[4], b_last = 0.f;
 #pragma unroll
-      for (int p = 0; p < NPART; ++p)
-        if (p < gpart) off += sm.part[p * DK + gc];
-      const int t0 = gpart * TPC;
+        for (int p = 0; p < 4; ++p) {
+          hbv[p] = b_last;  // Bbar of tile p: the gates of the tiles before it
+          b_last += sm.part[p * DK + pc];
+        }
+        float off = hbv[0];
 #pragma unroll
-      for (int tt = 0; tt < TPC / 16; ++tt) {
-        const float bbar = (tt == 0) ? off : off + pre[16 * tt - 1];
-        sm.hb[((t0 >> 4) + tt) * DK + gc] = bbar;
+        for (int p = 1; p < 4; ++p)
+          if (p == pt) off = hbv[p];
+        const float gdec = __expf(b_last - off);
+        const int t0 = 16 * pt;
 #pragma unroll
-        for (int j = 16 * tt; j < 16 * tt + 16; ++j) {
-          const float d = off + pre[j] - bbar;  // <= 0
-          ST* qp = sm.q + (t0 + j) * LDK + gc;
-          ST* kp = sm.k + (t0 + j) * LDK + gc;
-          stv(qp, ldv(qp) * __expf(d));
-          stv(kp, ldv(kp) * __expf(-d));
+        for (int j8 = 0; j8 < 16; j8 += 8) {
+          float kd[8];
+#pragma unroll
+          for (int jj = 0; jj < 8; ++jj) {
+            const int j = j8 + jj, t = t0 + j;
+            ST* qp = sm.q + t * LDK + pc;
+            ST* kp = sm.k + t * LDK + pc;
+            const float kv = ldv(kp);
+            const float e = __expf(pre[j]);      // exp(B_t - Bbar) <= 1
+            const float ie = __expf(-pre[j]);    // >= 1, bounded by 16 tokens of decay
+            stv(qp, ldv(qp) * e);
+            stv(kp, kv * ie);
+            kd[jj] = kv * (gdec * ie);           // K exp(B_last - B_t)
+          }
+          st8(sm.kdt + pc * LDT + t0 + j8, kd);
+        }
+#pragma unroll
+        for (int tk = 0; tk < 3; ++tk)
+          if (tk < pt) sm.fx[pair_idx(pt, tk) * DK + pc] = __expf(off - hbv[tk]);
+        sm.hx[pt * DK + pc] = __expf(off);
+        if (pt == 0) {
+          sm.lx[pc] = __expf(b_last);
+          ld_acc += b_last;
         }
       }
-      if (gpart == NPART - 1) sm.bl[gc] = off + pre[TPC - 1];
-      __syncthreads();
-      // ---- P2: per-channel factors of the tile pairs and the state update ----
-      for (int idx = tid; idx < 15 * DK; idx += kFT) {
-        const int which = idx / DK, c = idx % DK;
-        if (which < 6) {
-          const int tq = (which < 1) ? 1 : ((which < 3) ? 2 : 3);
-          const int tk = which - pair_idx(tq, 0);
-          sm.fx[which * DK + c] = __expf(sm.hb[tq * DK + c] - sm.hb[tk * DK + c]);
-        } else if (which < 10) {
-          sm.hx[(which - 6) * DK + c] = __expf(sm.hb[(which - 6) * DK + c]);
-        } else if (which < 14) {
-          sm.gx[(which - 10) * DK + c] = __expf(sm.bl[c] - sm.hb[(which - 10) * DK + c]);
-        } else {
-          sm.lx[c] = __expf(sm.bl[c]);
-        }
-      }
-      if (tid < DK) ld_acc += sm.bl[tid];
-      __syncthreads();
+      lds_barrier();
     }
 
     // ---- P3: the lower 16 x 16 tiles of A ----
-    for (int tile = wave; tile < 10; tile += 4) {
+    for (int tile = wave; tile < 10; tile += 8) {
       const int tq = (tile < 1) ? 0 : ((tile < 3) ? 1 : ((tile < 6) ? 2 : 3));
       const int tk = tile - tq * (tq + 1) / 2;
       f32x4 acc = zero4();
@@ -378,74 +481,70 @@ __global__ __launch_bounds__(kFT) void family_scan_kernel(FamArgs args) {
         const int t = tq * 16 + 4 * g + i;
         float x = acc[i];
         if constexpr (!DIAG) x *= __expf(fminf(sm.bc[t] - sm.bc[key], 0.f));
-        stv(sm.a + t * LDA + key, (key <= t) ? x : 0.f);
+        stv(sm.a + t * LDT + key, (key <= t) ? x : 0.f);
       }
     }
-    __syncthreads();
+    lds_barrier();
 
-    // ---- P4: outputs and state columns of this wave ----
-    Frag<ST> bv[2];  // V as B operand over the chunk's tokens (shared by A V and the update)
+    // ---- P4: two output tiles and the state rows of this wave ----
+    Frag<ST> bv[2];  // V as B operand over the chunk's tokens (A V and the update)
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) bv[kt] = frag_col(sm.v, LDV, col16 + ln, 32 * kt, g);
-    if (args.o != nullptr) {
-      Frag<ST> bs[NM / 2];  // S0 as B operand over d_k
-#pragma unroll
-      for (int kt = 0; kt < NM / 2; ++kt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          bs[kt].set(i, st[2 * kt][i]);
-          bs[kt].set(4 + i, st[2 * kt + 1][i]);
-        }
+    for (int kt = 0; kt < 2; ++kt) bv[kt] = frag_row(sm.vt, LDT, col16 + ln, 32 * kt, g);
+    {
+      // outputs: rows t < n of this chunk (none when o is NULL)
       const long orow0 = (args.mode == 0) ? static_cast<long>(c0)
                                           : static_cast<long>(seg) * args.w + (c0 - lo);
-      ST* og = static_cast<ST*>(args.o) + static_cast<long>(h) * DV + col + ln;
+      const auto rso = rsrc(args.o ? static_cast<const ST*>(args.o) + orow0 * v_stride : nullptr,
+                            args.o ? n * v_stride * static_cast<long>(sizeof(ST)) : 0);
+      const int ocol = static_cast<int>(h * DV + col + ln);
 #pragma unroll
-      for (int mt = 0; mt < 4; ++mt) {
+      for (int mh = 0; mh < NOT; ++mh) {
+        const int mt = NOT * rgrp + mh;  // token tile
         f32x4 acc = zero4();
 #pragma unroll
-        for (int kt = 0; kt < NM / 2; ++kt) {
+        for (int kt = 0; kt < DK / 32; ++kt) {
           Frag<ST> fa;
           if constexpr (DIAG)
             fa = frag_row_scaled(sm.q, LDK, mt * 16 + ln, 32 * kt, g, sm.hx + mt * DK);
           else
             fa = frag_row(sm.q, LDK, mt * 16 + ln, 32 * kt, g);
-          acc = mma(fa, bs[kt], acc);
+          acc = mma(fa, sm.s0f[cg][kt][lane], acc);
         }
         if constexpr (!DIAG) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) acc[i] *= sm.gam[mt * 16 + 4 * g + i];
+          const float4 gm = *reinterpret_cast<const float4*>(sm.gam + mt * 16 + 4 * g);
+          acc[0] *= gm.x;
+          acc[1] *= gm.y;
+          acc[2] *= gm.z;
+          acc[3] *= gm.w;
         }
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
           if (32 * kt < 16 * (mt + 1))
-            acc = mma(frag_row(sm.a, LDA, mt * 16 + ln, 32 * kt, g), bv[kt], acc);
+            acc = mma(frag_row(sm.a, LDT, mt * 16 + ln, 32 * kt, g), bv[kt], acc);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int t = mt * 16 + 4 * g + i;
-          if (t < n) stv(og + (orow0 + t) * v_stride, acc[i]);
-        }
+        for (int i = 0; i < 4; ++i)
+          bstore(rso, static_cast<int>(((mt * 16 + 4 * g + i) * v_stride + ocol) * sizeof(ST)),
+                 acc[i], static_cast<ST*>(nullptr));
       }
     }
     // S <- exp(B_last) . S0 + (K . exp(B_last - B))^T V
-    const float g_last = DIAG ? 0.f : __expf(sm.bc[FC - 1]);
+    const float g_last = DIAG ? 0.f : __expf(__shfl(b_l, 63, 64));
 #pragma unroll
-    for (int mt = 0; mt < NM; ++mt) {
-      f32x4 acc;
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        acc[i] = st[mt][i] * (DIAG ? sm.lx[mt * 16 + 4 * g + i] : g_last);
-      const int ch = mt * 16 + ln;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        Frag<ST> fa;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const int tok = 32 * kt + kap(g, j);
-          const float s = DIAG ? sm.gx[(tok >> 4) * DK + ch] : sm.dec[tok];
-          fa.set(j, ldv(sm.k + tok * LDK + ch) * s);
-        }
-        acc = mma(fa, bv[kt], acc);
+    for (int mt = 0; mt < NMH; ++mt) {
+      const int r = row0 + mt * 16;
+      f32x4 acc = st[mt];
+      if constexpr (DIAG) {
+        const float4 lx = *reinterpret_cast<const float4*>(sm.lx + r + 4 * g);
+        acc[0] *= lx.x;
+        acc[1] *= lx.y;
+        acc[2] *= lx.z;
+        acc[3] *= lx.w;
+      } else {
+        acc *= g_last;
       }
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+        acc = mma(frag_row(sm.kdt, LDT, r + ln, 32 * kt, g), bv[kt], acc);
       st[mt] = acc;
     }
   }
@@ -454,9 +553,9 @@ __global__ __launch_bounds__(kFT) void family_scan_kernel(FamArgs args) {
   if (args.S_out != nullptr) {
     float* so = args.S_out + sh * DK * DV + col + ln;
 #pragma unroll
-    for (int mt = 0; mt < NM; ++mt)
+    for (int mt = 0; mt < NMH; ++mt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) so[(mt * 16 + 4 * g + i) * DV] = st[mt][i];
+      for (int i = 0; i < 4; ++i) so[(row0 + mt * 16 + 4 * g + i) * DV] = st[mt][i];
   }
   if (args.mode == 0 && args.log_decay != nullptr && cb == 0) {
     if constexpr (DIAG) {
@@ -588,7 +687,9 @@ hipError_t launch_fcompose_d(const FamComposeArgs& a, int d_k, int d_v, int n_re
 hipError_t launch_family_scan(const FamArgs& a, int family, int bf16, int d_k, int d_v,
                               int n_chains, hipStream_t s) {
   if (n_chains <= 0) return hipSuccess;
-  const int64_t n_items = static_cast<int64_t>(n_chains) * a.h_v * (d_v / FNC);
+  const int fnc = bf16 ? fnc_of<uint16_t, 128>() : ((d_k == 128) ? fnc_of<float, 128>()
+                                                                 : fnc_of<float, 64>());
+  const int64_t n_items = static_cast<int64_t>(n_chains) * a.h_v * (d_v / fnc);
   if (n_items > 0x7fffffff) return hipErrorInvalidValue;
   const int n = static_cast<int>(n_items);
   if (family == FAM_DIAGONAL)

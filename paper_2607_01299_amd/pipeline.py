@@ -165,3 +165,112 @@ class ComposeBurst:
     def run(self):
         self.compose()
         self.seam()
+
+
+class FamilyPipeline:
+    """Scalar- or diagonal-family build, composition of the batch's segments in
+    order (one request, or the CSR lists given) and seam rescan, pre-bound."""
+
+    def __init__(self, family, q, k, v, gate, cu_seqlens, *, seam_w=8, seg_ids=None,
+                 req_offsets=None, S_prefix=None, want_post=False):
+        from .ops import FAMILIES
+        self.lib = _lib.load()
+        self.family = FAMILIES[family]
+        dev = q.device
+        self.stream = torch.cuda.current_stream(dev)
+        sp = ctypes.c_void_p(self.stream.cuda_stream)
+        T, h_qk, d_k = q.shape
+        h_v, d_v = v.shape[1], v.shape[2]
+        self.T, self.h_v, self.d_k, self.d_v = T, h_v, d_k, d_v
+        self.dims = Dims(h_qk=h_qk, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_dtype_code(q), chunk=64)
+        self.cdims = Dims(h_qk=h_v, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_lib.HYPIC_F32, chunk=64)
+        self.inputs = (q, k, v, gate)
+        self.cu_h, self.cu_d = _i32_pair(cu_seqlens, dev)
+        n_seg = len(self.cu_h) - 1
+        self.n_seg = n_seg
+        f32 = torch.float32
+        self.o = torch.empty((T, h_v, d_v), dtype=q.dtype, device=dev)
+        self.S_seg = torch.empty((n_seg, h_v, d_k, d_v), dtype=f32, device=dev)
+        ld_shape = (n_seg, h_v) if family == "scalar" else (n_seg, h_v, d_k)
+        self.log_decay = torch.empty(ld_shape, dtype=f32, device=dev)
+        ws_bytes = self.lib.hypic_workspace_bytes(_lib.HYPIC_OP_BUILD, ctypes.byref(self.dims),
+                                                  n_seg)
+        self.ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        self._build_args = (
+            ctypes.byref(self.dims), self.family, _p(q), _p(k), _p(v), _p(gate), _p(self.cu_d),
+            self.cu_h.ctypes.data_as(ctypes.c_void_p), n_seg, _p(self.o), _p(self.S_seg),
+            _p(self.log_decay), _p(self.ws), ws_bytes, sp)
+        if seg_ids is None:
+            seg_ids = np.arange(n_seg, dtype=np.int32)
+            req_offsets = np.array([0, n_seg], dtype=np.int32)
+        self.ids_h, self.ids_d = _i32_pair(seg_ids, dev)
+        self.off_h, self.off_d = _i32_pair(req_offsets, dev)
+        n_req = len(self.off_h) - 1
+        nnz = int(self.off_h[-1])
+        self.n_req, self.nnz = n_req, nnz
+        self.S_prefix = S_prefix
+        self.S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=f32, device=dev)
+        self.S_inc = torch.empty((nnz, h_v, d_k, d_v), dtype=f32, device=dev)
+        self._compose_args = (
+            ctypes.byref(self.cdims), self.family, _p(self.log_decay), _p(self.S_seg), n_seg,
+            _p(self.ids_d), self.ids_h.ctypes.data_as(ctypes.c_void_p), _p(self.off_d),
+            self.off_h.ctypes.data_as(ctypes.c_void_p), n_req, _p(S_prefix), _p(self.S_out),
+            _p(self.S_inc), None, 0, sp)
+        lens = np.diff(self.cu_h)
+        self.seam_w = seam_w
+        self.ts_h, self.ts_d = _i32_pair(self.cu_h[:-1][self.ids_h], dev)
+        self.tl_h, self.tl_d = _i32_pair(lens[self.ids_h], dev)
+        self.o_seam = torch.empty((nnz, seam_w, h_v, d_v), dtype=q.dtype, device=dev)
+        self.S_post = (torch.empty((nnz, h_v, d_k, d_v), dtype=f32, device=dev)
+                       if want_post else None)
+        self._seam_args = (
+            ctypes.byref(self.dims), self.family, _p(q), _p(k), _p(v), _p(gate), T,
+            _p(self.ts_d), _p(self.tl_d), self.ts_h.ctypes.data_as(ctypes.c_void_p),
+            self.tl_h.ctypes.data_as(ctypes.c_void_p), nnz, seam_w, _p(self.S_inc),
+            _p(self.o_seam), _p(self.S_post), None, 0, sp)
+
+    def build(self):
+        _lib.check(self.lib.hypic_family_build(*self._build_args))
+
+    def compose(self):
+        _lib.check(self.lib.hypic_family_compose(*self._compose_args))
+
+    def seam(self):
+        _lib.check(self.lib.hypic_family_seam(*self._seam_args))
+
+    def run(self):
+        self.build()
+        self.compose()
+        self.seam()
+
+
+class FamilyComposeBurst:
+    """Many requests composed from a pool of scalar- or diagonal-family
+    tuples (Eq. (6) with the compressed operators of Tab. 3), pre-bound."""
+
+    def __init__(self, family, log_decay, S_seg, seg_ids, req_offsets):
+        from .ops import FAMILIES
+        self.lib = _lib.load()
+        self.family = FAMILIES[family]
+        dev = S_seg.device
+        self.stream = torch.cuda.current_stream(dev)
+        sp = ctypes.c_void_p(self.stream.cuda_stream)
+        n_pool, h_v, d_k, d_v = S_seg.shape
+        self.pool = (log_decay, S_seg)
+        self.cdims = Dims(h_qk=h_v, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_lib.HYPIC_F32, chunk=64)
+        self.ids_h, self.ids_d = _i32_pair(seg_ids, dev)
+        self.off_h, self.off_d = _i32_pair(req_offsets, dev)
+        n_req = len(self.off_h) - 1
+        nnz = int(self.off_h[-1])
+        self.n_req, self.nnz, self.h_v, self.d_k, self.d_v = n_req, nnz, h_v, d_k, d_v
+        f32 = torch.float32
+        self.S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=f32, device=dev)
+        self.S_inc = torch.empty((nnz, h_v, d_k, d_v), dtype=f32, device=dev)
+        self._compose_args = (
+            ctypes.byref(self.cdims), self.family, _p(log_decay), _p(S_seg), n_pool,
+            _p(self.ids_d), self.ids_h.ctypes.data_as(ctypes.c_void_p), _p(self.off_d),
+            self.off_h.ctypes.data_as(ctypes.c_void_p), n_req, None, _p(self.S_out),
+            _p(self.S_inc), None, 0, sp)
+
+    def compose(self):
+        _lib.check(self.lib.hypic_family_compose(*self._compose_args))
