@@ -251,6 +251,56 @@ int32_t hypic_family_seam(const hypic_dims* dims, int32_t family, const void* q,
                           float* S_post, void* workspace, size_t workspace_bytes,
                           void* stream);
 
+/* ------------------------------------------------------------------------
+ * Reuse-time steps next to the linear-attention cache.
+ * R(p) is the rotary position embedding: it rotates channel pairs (2i, 2i+1)
+ * of a d-vector by p * base^(-2i/d).  Angles are formed in float64.
+ * ------------------------------------------------------------------------ */
+
+/*
+ * hypic_rope_shift_state -- Eq. (7): a state cached with its keys rotated for
+ * positions starting at a is moved to positions starting at b by rotating its
+ * d_k rows, S_out[e, h] = R(delta[e]) S_in[e, h] with delta[e] = b - a.  Exact
+ * for transitions that commute with R (the scalar family; pair-shared gates).
+ *   S_in, S_out  [n, h_v, d_k, d_v] f32, 16-byte aligned; S_out may equal S_in.
+ *   delta        [n] int32 device.
+ *   base         RoPE base (> 0, finite).
+ */
+int32_t hypic_rope_shift_state(const hypic_dims* dims, const float* S_in, float* S_out,
+                               int32_t n, const int32_t* delta, double base, void* stream);
+
+/*
+ * hypic_rope_rerotate_keys -- Eq. (8): cached keys of segment s rotated from
+ * positions starting at a to positions starting at b, k_out = R(delta[s]) k_in
+ * for each of its tokens and heads, delta[s] = b - a (values are unchanged).
+ *   k_in, k_out  [T, h_qk, d_k] in dims->dtype; k_out may equal k_in.
+ *   cu_seqlens   [n_seg + 1] int32 device / _host as in hypic_build_segment;
+ *                the longest segment must be under 4,194,240 tokens.
+ *   delta        [n_seg] int32 device.
+ */
+int32_t hypic_rope_rerotate_keys(const hypic_dims* dims, const void* k_in, void* k_out,
+                                 const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                                 int32_t n_seg, const int32_t* delta, double base,
+                                 void* stream);
+
+/*
+ * hypic_causal_conv -- the depthwise causal convolution in front of a
+ * linear-attention layer, over packed segments with a carried conv state
+ * (Sec. 4.2: a segment cached on its own starts from zeros; at reuse its
+ * first width - 1 outputs are recomputed from the previous segment's state):
+ *   y[t, c] = act(sum_{j < width} weight[c, j] * xx[t + j, c]),
+ *   xx = concat(state_in[s], x[tokens of segment s]),  act = SiLU if silu else identity,
+ *   state_out[s] = the last width - 1 rows of xx.
+ *   x, y        [T, channels] in dtype (HYPIC_F32 or HYPIC_BF16); y must not alias x.
+ *   weight      [channels, width] f32, 1 <= width <= 8.
+ *   state_in    [n_seg, width - 1, channels] f32, or NULL for zeros.
+ *   state_out   [n_seg, width - 1, channels] f32, or NULL.
+ */
+int32_t hypic_causal_conv(int32_t dtype, int32_t channels, int32_t width, const void* x,
+                          const float* weight, const int32_t* cu_seqlens,
+                          const int32_t* cu_seqlens_host, int32_t n_seg, const float* state_in,
+                          void* y, float* state_out, int32_t silu, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -10,7 +10,8 @@ def __getattr__(name):
     # the torch-facing calls load torch lazily so that the generators and the
     # library loader stay importable without it
     if name in ("build_segment", "compose_segments", "seam_rescan", "make_dims",
-                "family_build", "family_compose", "family_seam"):
+                "family_build", "family_compose", "family_seam", "rope_shift_state",
+                "rope_rerotate_keys", "causal_conv"):
         from . import ops
         return getattr(ops, name)
     raise AttributeError(name)

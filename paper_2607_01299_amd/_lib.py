@@ -33,6 +33,9 @@ EXPORTS = (
     "hypic_family_build",
     "hypic_family_compose",
     "hypic_family_seam",
+    "hypic_rope_shift_state",
+    "hypic_rope_rerotate_keys",
+    "hypic_causal_conv",
 )
 
 HYPIC_FAMILY_SCALAR = 1
@@ -96,6 +99,14 @@ def load():
         ctypes.POINTER(Dims), _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _I32, _P, _P, _P,
         _P, _SZ, _P]
     lib.hypic_family_seam.restype = _I32
+    lib.hypic_rope_shift_state.argtypes = [ctypes.POINTER(Dims), _P, _P, _I32, _P, ctypes.c_double,
+                                           _P]
+    lib.hypic_rope_shift_state.restype = _I32
+    lib.hypic_rope_rerotate_keys.argtypes = [ctypes.POINTER(Dims), _P, _P, _P, _P, _I32, _P,
+                                             ctypes.c_double, _P]
+    lib.hypic_rope_rerotate_keys.restype = _I32
+    lib.hypic_causal_conv.argtypes = [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _I32, _P]
+    lib.hypic_causal_conv.restype = _I32
     _lib = lib
     return lib
 

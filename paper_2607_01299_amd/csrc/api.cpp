@@ -2,6 +2,7 @@
 // kernel dispatch.  Nothing is enqueued unless every check passes.
 
 #include <algorithm>
+#include <cmath>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -345,6 +346,75 @@ int32_t hypic_family_seam(const hypic_dims* dims, int32_t family, const void* q,
   a.S_out = S_post;
   return hip_status(hypic::launch_family_scan(a, family, dims->dtype == HYPIC_BF16, dims->d_k,
                                               dims->d_v, n_entries,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+// ---------------------------------------------------------------------------
+// reuse-time steps next to the cache: RoPE state shift, key re-rotation, conv
+// ---------------------------------------------------------------------------
+
+namespace {
+
+// cu[0] == 0, non-decreasing; returns the longest segment or -1
+int64_t check_offsets(const int32_t* cu_host, int32_t n_seg) {
+  if (cu_host[0] != 0) return -1;
+  int64_t longest = 0;
+  for (int32_t s = 0; s < n_seg; ++s) {
+    const int64_t len = static_cast<int64_t>(cu_host[s + 1]) - cu_host[s];
+    if (len < 0) return -1;
+    longest = len > longest ? len : longest;
+  }
+  return longest;
+}
+
+bool good_base(double base) { return std::isfinite(base) && base > 0.0; }
+
+}  // namespace
+
+int32_t hypic_rope_shift_state(const hypic_dims* dims, const float* S_in, float* S_out,
+                               int32_t n, const int32_t* delta, double base, void* stream) {
+  int32_t st = check_dims(dims);
+  if (st != HYPIC_OK) return st;
+  if (n < 0 || !good_base(base)) return HYPIC_EINVAL;
+  if (n == 0) return HYPIC_OK;
+  if (!S_in || !S_out || !delta || !aligned16(S_in) || !aligned16(S_out)) return HYPIC_EINVAL;
+  if (static_cast<int64_t>(n) * dims->h_v > 0x7fffffff) return HYPIC_EINVAL;
+  return hip_status(hypic::launch_rope_state(S_in, S_out, delta, n, dims->h_v, dims->d_k,
+                                             dims->d_v, base, static_cast<hipStream_t>(stream)));
+}
+
+int32_t hypic_rope_rerotate_keys(const hypic_dims* dims, const void* k_in, void* k_out,
+                                 const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                                 int32_t n_seg, const int32_t* delta, double base,
+                                 void* stream) {
+  int32_t st = check_dims(dims);
+  if (st != HYPIC_OK) return st;
+  if (n_seg < 0 || !good_base(base)) return HYPIC_EINVAL;
+  if (n_seg == 0) return HYPIC_OK;
+  if (!k_in || !k_out || !cu_seqlens || !cu_seqlens_host || !delta) return HYPIC_EINVAL;
+  const int64_t longest = check_offsets(cu_seqlens_host, n_seg);
+  if (longest < 0 || (longest + 63) / 64 > 65535) return HYPIC_EINVAL;
+  return hip_status(hypic::launch_rope_keys(k_in, k_out, dims->dtype == HYPIC_BF16, cu_seqlens,
+                                            delta, n_seg, static_cast<int>(longest), dims->h_qk,
+                                            dims->d_k, base, static_cast<hipStream_t>(stream)));
+}
+
+int32_t hypic_causal_conv(int32_t dtype, int32_t channels, int32_t width, const void* x,
+                          const float* weight, const int32_t* cu_seqlens,
+                          const int32_t* cu_seqlens_host, int32_t n_seg, const float* state_in,
+                          void* y, float* state_out, int32_t silu, void* stream) {
+  if (dtype != HYPIC_F32 && dtype != HYPIC_BF16) return HYPIC_EUNSUPPORTED;
+  if (width < 1 || width > 8) return HYPIC_EUNSUPPORTED;
+  if (channels < 1 || n_seg < 0) return HYPIC_EINVAL;
+  if (n_seg == 0) return HYPIC_OK;
+  if (!x || !weight || !y || !cu_seqlens || !cu_seqlens_host) return HYPIC_EINVAL;
+  if (x == y) return HYPIC_EINVAL;
+  const int64_t longest = check_offsets(cu_seqlens_host, n_seg);
+  if (longest < 0 || (longest + 63) / 64 > 65535 || (channels + 255) / 256 > 65535)
+    return HYPIC_EINVAL;
+  return hip_status(hypic::launch_causal_conv(x, weight, dtype == HYPIC_BF16, cu_seqlens, n_seg,
+                                              static_cast<int>(longest), state_in, y, state_out,
+                                              channels, width, silu ? 1 : 0,
                                               static_cast<hipStream_t>(stream)));
 }
 

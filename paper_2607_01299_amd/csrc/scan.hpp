@@ -98,6 +98,15 @@ hipError_t launch_family_scan(const FamArgs& a, int family, int bf16, int d_k, i
 hipError_t launch_family_compose(const FamComposeArgs& a, int family, int d_k, int d_v,
                                  int n_req, hipStream_t s);
 
+hipError_t launch_rope_state(const float* S_in, float* S_out, const int32_t* delta, int n,
+                             int h_v, int d_k, int d_v, double base, hipStream_t s);
+hipError_t launch_rope_keys(const void* k_in, void* k_out, int bf16, const int32_t* cu,
+                            const int32_t* delta, int n_seg, int max_len, int heads, int d,
+                            double base, hipStream_t s);
+hipError_t launch_causal_conv(const void* x, const float* w, int bf16, const int32_t* cu,
+                              int n_seg, int max_len, const float* state_in, void* y,
+                              float* state_out, int C, int K, int silu, hipStream_t s);
+
 hipError_t launch_lpt_order(const int32_t* cu, int n, int32_t* order, hipStream_t s);
 // Launches the scan over n_chains (segments or seam entries) x h_v heads;
 // returns hipErrorInvalidValue if the grid would exceed 2^31 - 1 workgroups.

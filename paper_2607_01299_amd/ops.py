@@ -257,3 +257,60 @@ def family_seam(family, q, k, v, gate, tok_start, tok_len, w, S_in, *, tok_start
         _ptr(ln_d), _hptr(st_h), _hptr(ln_h), n_e, int(w), _ptr(S_in), _ptr(o_seam),
         _ptr(S_post), None, 0, _stream(dev)))
     return o_seam, S_post
+
+
+# ---------------------------------------------------------------------------
+# reuse-time steps: RoPE state shift (Eq. (7)), key re-rotation (Eq. (8)),
+# causal conv with carried state (Sec. 4.2)
+# ---------------------------------------------------------------------------
+
+def rope_shift_state(S, delta, base=10000.0, out=None):
+    """S [n, h_v, d_k, d_v] float32 -> R(delta[e]) S[e, h] (out may be S)."""
+    lib = _lib.load()
+    _contig(S, "S")
+    n, h_v, d_k, d_v = S.shape
+    dev = S.device
+    dims = Dims(h_qk=h_v, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_lib.HYPIC_F32, chunk=64)
+    _, dl = _index_pair(delta, None, dev)
+    out = torch.empty_like(S) if out is None else out
+    _lib.check(lib.hypic_rope_shift_state(ctypes.byref(dims), _ptr(S), _ptr(out), n, _ptr(dl),
+                                          float(base), _stream(dev)))
+    return out
+
+
+def rope_rerotate_keys(k, cu_seqlens, delta, base=10000.0, out=None):
+    """k [T, h, d] (bf16 or f32) -> R(delta[s]) k for the tokens of segment s."""
+    lib = _lib.load()
+    _contig(k, "k")
+    T, h, d = k.shape
+    dev = k.device
+    dims = Dims(h_qk=h, h_v=h, d_k=d, d_v=d, dtype=_dtype_code(k), chunk=64)
+    cu_h, cu_d = _index_pair(cu_seqlens, None, dev)
+    _, dl = _index_pair(delta, None, dev)
+    out = torch.empty_like(k) if out is None else out
+    _lib.check(lib.hypic_rope_rerotate_keys(ctypes.byref(dims), _ptr(k), _ptr(out), _ptr(cu_d),
+                                            _hptr(cu_h), len(cu_h) - 1, _ptr(dl), float(base),
+                                            _stream(dev)))
+    return out
+
+
+def causal_conv(x, weight, cu_seqlens, state_in=None, *, silu=True, want_state=True):
+    """x [T, C] (bf16 or f32), weight [C, K] float32 -> (y [T, C], state_out
+    [n_seg, K - 1, C] float32 or None)."""
+    lib = _lib.load()
+    _contig(x, "x")
+    _contig(weight, "weight")
+    T, C = x.shape
+    K = weight.shape[1]
+    dev = x.device
+    cu_h, cu_d = _index_pair(cu_seqlens, None, dev)
+    n_seg = len(cu_h) - 1
+    y = torch.empty_like(x)
+    st_out = (torch.empty((n_seg, K - 1, C), dtype=torch.float32, device=dev)
+              if want_state else None)
+    if state_in is not None:
+        _contig(state_in, "state_in")
+    _lib.check(lib.hypic_causal_conv(_dtype_code(x), C, K, _ptr(x), _ptr(weight), _ptr(cu_d),
+                                     _hptr(cu_h), n_seg, _ptr(state_in), _ptr(y), _ptr(st_out),
+                                     1 if silu else 0, _stream(dev)))
+    return y, st_out

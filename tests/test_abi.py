@@ -199,3 +199,31 @@ def test_family_calls_reject_unknown_family(lib, family):
     assert _fbuild(lib, family, [0, 10]) == _lib.HYPIC_EUNSUPPORTED
     assert _fcompose(lib, family, [0], [0, 1]) == _lib.HYPIC_EUNSUPPORTED
     assert _fseam(lib, family, [0], [4]) == _lib.HYPIC_EUNSUPPORTED
+
+
+def test_adjacent_calls_reject_bad_arguments(lib):
+    d = _dims()
+    dl = FAKE
+    assert lib.hypic_rope_shift_state(ctypes.byref(d), FAKE, FAKE, 3, dl, -1.0, None) == \
+        _lib.HYPIC_EINVAL
+    assert lib.hypic_rope_shift_state(ctypes.byref(d), FAKE_ODD, FAKE, 3, dl, 1e4, None) == \
+        _lib.HYPIC_EINVAL
+    assert lib.hypic_rope_shift_state(ctypes.byref(d), FAKE, FAKE, 0, dl, 1e4, None) == _lib.HYPIC_OK
+    assert lib.hypic_rope_shift_state(ctypes.byref(_dims(d_k=48)), FAKE, FAKE, 3, dl, 1e4,
+                                      None) == _lib.HYPIC_EUNSUPPORTED
+    cu = np.array([0, 5, 3], dtype=np.int32)
+    hcu = cu.ctypes.data_as(ctypes.c_void_p)
+    assert lib.hypic_rope_rerotate_keys(ctypes.byref(d), FAKE, FAKE, FAKE, hcu, 2, dl, 1e4,
+                                        None) == _lib.HYPIC_EINVAL
+    assert lib.hypic_rope_rerotate_keys(ctypes.byref(d), FAKE, FAKE, FAKE, hcu, 1, dl,
+                                        float("nan"), None) == _lib.HYPIC_EINVAL
+    assert lib.hypic_causal_conv(_lib.HYPIC_BF16, 16, 9, FAKE, FAKE, FAKE, hcu, 1, None, FAKE_ODD,
+                                 None, 1, None) == _lib.HYPIC_EUNSUPPORTED
+    assert lib.hypic_causal_conv(_lib.HYPIC_BF16, 16, 4, FAKE, FAKE, FAKE, hcu, 2, None, FAKE_ODD,
+                                 None, 1, None) == _lib.HYPIC_EINVAL     # decreasing offsets
+    assert lib.hypic_causal_conv(_lib.HYPIC_BF16, 16, 4, FAKE, FAKE, FAKE, hcu, 1, None, FAKE,
+                                 None, 1, None) == _lib.HYPIC_EINVAL     # y aliases x
+    assert lib.hypic_causal_conv(7, 16, 4, FAKE, FAKE, FAKE, hcu, 1, None, FAKE_ODD, None, 1,
+                                 None) == _lib.HYPIC_EUNSUPPORTED
+    assert lib.hypic_causal_conv(_lib.HYPIC_F32, 16, 4, FAKE, FAKE, FAKE, hcu, 0, None, FAKE_ODD,
+                                 None, 1, None) == _lib.HYPIC_OK
