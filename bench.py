@@ -352,6 +352,50 @@ def bench_families(torch, steps, warmup, seam_w):
             "burst_workload": W.CONFIG_NAMES[5] + " (family tuples)", **out}
 
 
+def bench_adjacent(torch, steps):
+    """The reuse-time steps next to the cache, each an HBM stream: the Eq. (7)
+    state shift over the 512-entry serve-time pool, the Eq. (8) re-rotation of
+    32 x 4096 cached bf16 keys (16 heads, d = 128) and the width-4 causal conv
+    over the q, k, v channels (6144) of 8 x 2048 bf16 tokens.  Inputs are drawn
+    on the device (timing only)."""
+    from paper_2607_01299_amd import ops
+    g = torch.Generator(device="cuda").manual_seed(W.SEED_BASE + 9)
+    out = {}
+
+    def leg(name, fn, byts, workload):
+        fn()
+        ms = _events_ms(torch, torch.cuda.current_stream(), fn, steps)
+        gbs = byts / (ms * 1e-3) / 1e9
+        out[name] = {"ms": ms, "workload": workload,
+                     "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS,
+                                  "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "traffic": None,
+                                  "bytes_per_launch": byts}}
+
+    S = torch.randn((512, 16, 128, 128), device="cuda", generator=g)
+    S_out = torch.empty_like(S)
+    delta = torch.arange(512, dtype=torch.int32, device="cuda") * 1024
+    leg("rope_shift_state", lambda: ops.rope_shift_state(S, delta, out=S_out),
+        2.0 * S.numel() * 4, "512 x 16 heads x 128 x 128 float32 states")
+    del S, S_out
+    k = torch.randn((32 * 4096, 16, 128), device="cuda", generator=g).to(torch.bfloat16)
+    k_out = torch.empty_like(k)
+    cu = W.cu_from_lengths([4096] * 32)
+    cu_d = torch.from_numpy(cu).cuda()
+    dl = torch.arange(32, dtype=torch.int32, device="cuda") * 4096
+    leg("rope_rerotate_keys", lambda: ops.rope_rerotate_keys(k, cu, dl, out=k_out,
+                                                             cu_seqlens_dev=cu_d),
+        2.0 * k.numel() * 2, "32 x 4096 tokens x 16 heads x 128 bf16 keys")
+    del k, k_out
+    x = torch.randn((8 * 2048, 6144), device="cuda", generator=g).to(torch.bfloat16)
+    wt = torch.randn((6144, 4), device="cuda", generator=g) * 0.5
+    cu = W.cu_from_lengths([2048] * 8)
+    cu_d = torch.from_numpy(cu).cuda()
+    leg("causal_conv", lambda: ops.causal_conv(x, wt, cu, cu_seqlens_dev=cu_d),
+        2.0 * x.numel() * 2 + wt.numel() * 4 + 2 * 8 * 3 * 6144 * 4,
+        "8 x 2048 tokens x 6144 bf16 channels, width 4, SiLU")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -362,9 +406,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-burst", action="store_true")
     ap.add_argument("--no-families", action="store_true",
-                    help="skip the scalar / diagonal family legs")
+                    help="skip the scalar / diagonal family and reuse-time-step legs")
     ap.add_argument("--families-only", action="store_true",
-                    help="run only the scalar / diagonal family legs (profiling)")
+                    help="run only the family and reuse-time-step legs (profiling)")
     ap.add_argument("--no-segments", action="store_true",
                     help="skip the segment step (profiling the burst alone)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -395,7 +439,8 @@ def main():
     _lib.load()
     if args.families_only:
         print(json.dumps({"families": bench_families(torch, args.steps, args.warmup,
-                                                     args.seam_w)}))
+                                                     args.seam_w),
+                          "adjacent": bench_adjacent(torch, args.steps)}))
         return
     if args.no_segments:
         burst = bench_compose_burst(torch, max(args.steps // 2, 3), max(args.warmup // 2, 1))
@@ -409,6 +454,7 @@ def main():
                                                            max(args.warmup // 2, 1))
     fam = None if args.no_families else bench_families(torch, args.steps, args.warmup,
                                                          args.seam_w)
+    adj = None if args.no_families else bench_adjacent(torch, args.steps)
     value = seg["tokens"] / (seg["ms_per_step"] * 1e-3)
     out = {
         "metric": METRIC,
@@ -430,6 +476,7 @@ def main():
         "cpu_baseline": cpu,
         "compose_burst": burst,
         "families": fam,
+        "adjacent": adj,
     }
     print(json.dumps(out))
 

@@ -273,7 +273,7 @@ int32_t hypic_rope_shift_state(const hypic_dims* dims, const float* S_in, float*
  * hypic_rope_rerotate_keys -- Eq. (8): cached keys of segment s rotated from
  * positions starting at a to positions starting at b, k_out = R(delta[s]) k_in
  * for each of its tokens and heads, delta[s] = b - a (values are unchanged).
- *   k_in, k_out  [T, h_qk, d_k] in dims->dtype; k_out may equal k_in.
+ *   k_in, k_out  [T, h_qk, d_k] in dims->dtype, 16-byte aligned; k_out may equal k_in.
  *   cu_seqlens   [n_seg + 1] int32 device / _host as in hypic_build_segment;
  *                the longest segment must be under 4,194,240 tokens.
  *   delta        [n_seg] int32 device.
@@ -291,7 +291,8 @@ int32_t hypic_rope_rerotate_keys(const hypic_dims* dims, const void* k_in, void*
  *   y[t, c] = act(sum_{j < width} weight[c, j] * xx[t + j, c]),
  *   xx = concat(state_in[s], x[tokens of segment s]),  act = SiLU if silu else identity,
  *   state_out[s] = the last width - 1 rows of xx.
- *   x, y        [T, channels] in dtype (HYPIC_F32 or HYPIC_BF16); y must not alias x.
+ *   x, y        [T, channels] in dtype (HYPIC_F32 or HYPIC_BF16), 16-byte aligned;
+ *               y must not alias x.
  *   weight      [channels, width] f32, 1 <= width <= 8.
  *   state_in    [n_seg, width - 1, channels] f32, or NULL for zeros.
  *   state_out   [n_seg, width - 1, channels] f32, or NULL.

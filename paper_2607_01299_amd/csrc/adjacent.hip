@@ -8,8 +8,8 @@
 // R(p) rotates channel pairs (2i, 2i + 1) by p * base^(-2i/d).  Angles are
 // formed and reduced in float64 (positions reach 1e5 and more, where a float32
 // angle is off by far more than the result's precision), then applied in
-// float32.  All three are elementwise streams: 16-byte accesses per lane where
-// the layout allows, bounded by HBM bandwidth.
+// float32.  All three are elementwise streams with 16-byte accesses per lane,
+// bounded by HBM bandwidth.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -72,85 +72,164 @@ __global__ __launch_bounds__(256) void rope_state_kernel(const float* S_in, floa
 
 // ---------------------------------------------------------------------------
 // Eq. (8): k_out[t, h] = R(delta[s]) k_in[t, h] for the tokens t of segment s;
-// grid (segment, 64-token block): blocks past a segment's end exit at once
+// grid (segment, 64-token block): blocks past a segment's end exit at once.
+// Each lane moves 16 bytes (VEC elements, VEC / 2 channel pairs).
 // ---------------------------------------------------------------------------
+template <typename T>
+struct alignas(16) Vec16 {
+  static constexpr int N = 16 / static_cast<int>(sizeof(T));
+  T v[N];
+};
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void rope_keys_kernel(const T* k_in, T* k_out,
                                                         const int32_t* cu, const int32_t* delta,
                                                         int heads, double base) {
+  constexpr int VEC = Vec16<T>::N;
   __shared__ float cs[D / 2], sn[D / 2];
   const int s = blockIdx.x;
   const int t0 = cu[s] + 64 * static_cast<int>(blockIdx.y);
   const int t1 = min(t0 + 64, cu[s + 1]);
   if (t0 >= t1) return;  // uniform across the workgroup
   rope_table(cs, sn, D, delta[s], base);
-  const int pairs = heads * (D / 2);
+  const int per_row = heads * D / VEC;  // 16-byte pieces per token
   const long row = static_cast<long>(heads) * D;
-  for (int idx = threadIdx.x; idx < (t1 - t0) * pairs; idx += 256) {
-    const int t = t0 + idx / pairs, r = idx % pairs;
-    const int hh = r / (D / 2), i = r % (D / 2);
-    const long o = t * row + hh * D + 2 * i;
-    const float a = to_float(k_in[o]), b = to_float(k_in[o + 1]);
-    from_float(k_out + o, cs[i] * a - sn[i] * b);
-    from_float(k_out + o + 1, sn[i] * a + cs[i] * b);
+  for (int idx = threadIdx.x; idx < (t1 - t0) * per_row; idx += 256) {
+    const int t = t0 + idx / per_row, r = idx % per_row;
+    const long o = t * row + static_cast<long>(r) * VEC;
+    const int i0 = (r * VEC) % D / 2;  // first channel pair of this piece
+    const Vec16<T> a = *reinterpret_cast<const Vec16<T>*>(k_in + o);
+    Vec16<T> b;
+#pragma unroll
+    for (int p = 0; p < VEC / 2; ++p) {
+      const float x = to_float(a.v[2 * p]), y = to_float(a.v[2 * p + 1]);
+      const float c = cs[i0 + p], sv = sn[i0 + p];
+      from_float(&b.v[2 * p], c * x - sv * y);
+      from_float(&b.v[2 * p + 1], sv * x + c * y);
+    }
+    *reinterpret_cast<Vec16<T>*>(k_out + o) = b;
   }
 }
 
 // ---------------------------------------------------------------------------
 // causal depthwise convolution over packed segments with carried conv state:
 //   y[t, c] = act(sum_j w[c, j] xx[t + j, c]),  xx = concat(state_in[s], x[segment s])
-// grid (segment, 64-token block, 256-channel block)
+// grid (segment, 64-token block, channel block); each lane carries VEC
+// consecutive channels (one 16-byte load and store per token when the rows
+// allow it, VEC = 1 otherwise) and slides a register window of the width - 1
+// previous inputs down the block's tokens, loading eight tokens at a time.
 // ---------------------------------------------------------------------------
 constexpr int kMaxWidth = 8;
 
-template <typename T>
+template <typename T, int VEC>
+struct alignas(VEC * sizeof(T)) Piece {
+  T v[VEC];
+};
+
+template <typename T, int VEC, int K>
 __global__ __launch_bounds__(256) void conv_kernel(const T* x, const float* w, const int32_t* cu,
                                                    const float* state_in, T* y, float* state_out,
-                                                   int C, int K, int silu) {
+                                                   int C, int silu) {
+  constexpr int TB = 8;  // tokens loaded together
+  static_assert(TB >= K - 1, "the window must fit one batch");
   const int s = blockIdx.x;
-  const int c = blockIdx.z * 256 + threadIdx.x;
+  const int c0 = (blockIdx.z * 256 + threadIdx.x) * VEC;  // first channel of this lane
   const int lo = cu[s], hi = cu[s + 1];
   const int t0 = lo + 64 * static_cast<int>(blockIdx.y);
-  if (c >= C) return;
-  float wk[kMaxWidth], win[kMaxWidth];
+  if (c0 >= C) return;  // C is a multiple of VEC
+  float wk[K][VEC];
 #pragma unroll
-  for (int j = 0; j < kMaxWidth; ++j) wk[j] = (j < K) ? w[static_cast<long>(c) * K + j] : 0.f;
-  // raw input at position p of xx (p < K - 1: the carried state)
-  auto xx = [&](int p) -> float {
-    if (p >= K - 1) return to_float(x[static_cast<long>(lo + p - (K - 1)) * C + c]);
-    return state_in ? state_in[(static_cast<long>(s) * (K - 1) + p) * C + c] : 0.f;
+  for (int j = 0; j < K; ++j)
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) wk[j][e] = w[static_cast<long>(c0 + e) * K + j];
+  auto load_x = [&](int t, float (&out)[VEC]) __attribute__((always_inline)) {
+    const Piece<T, VEC> a =
+        *reinterpret_cast<const Piece<T, VEC>*>(x + static_cast<long>(t) * C + c0);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) out[e] = to_float(a.v[e]);
+  };
+  // raw inputs at position p of xx (p < K - 1: the carried state)
+  auto xx = [&](int p, float (&out)[VEC]) __attribute__((always_inline)) {
+    if (p >= K - 1) {
+      load_x(lo + p - (K - 1), out);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e)
+        out[e] = state_in ? state_in[(static_cast<long>(s) * (K - 1) + p) * C + c0 + e] : 0.f;
+    }
   };
   if (t0 < hi) {
     const int r0 = t0 - lo;  // first output row of this block within the segment
-    // window: xx[r0 .. r0 + K - 2] precede the first output's own input
+    // win[j]: the input K - 1 - j tokens before the next output's own input
+    float win[K > 1 ? K - 1 : 1][VEC];
 #pragma unroll
-    for (int j = 0; j < kMaxWidth - 1; ++j) win[j] = (j < K - 1) ? xx(r0 + j) : 0.f;
+    for (int j = 0; j < K - 1; ++j) xx(r0 + j, win[j]);
     const int t1 = min(t0 + 64, hi);
-    for (int t = t0; t < t1; ++t) {
-      const float cur = to_float(x[static_cast<long>(t) * C + c]);
-      float acc = 0.f;
+    for (int tb = t0; tb < t1; tb += TB) {
+      float cur[TB][VEC];
 #pragma unroll
-      for (int j = 0; j < kMaxWidth - 1; ++j)
-        if (j < K - 1) acc += wk[j] * win[j];
-      // the newest input takes tap K - 1
+      for (int u = 0; u < TB; ++u) load_x((tb + u < t1) ? tb + u : t1 - 1, cur[u]);
 #pragma unroll
-      for (int j = 0; j < kMaxWidth; ++j)
-        if (j == K - 1) acc += wk[j] * cur;
-      if (silu) acc = acc / (1.f + __expf(-acc));
-      from_float(y + static_cast<long>(t) * C + c, acc);
+      for (int u = 0; u < TB; ++u) {
+        Piece<T, VEC> out;
 #pragma unroll
-      for (int j = 0; j < kMaxWidth - 2; ++j) win[j] = win[j + 1];
+        for (int e = 0; e < VEC; ++e) {
+          float acc = 0.f;
 #pragma unroll
-      for (int j = 0; j < kMaxWidth - 1; ++j)
-        if (j == K - 2) win[j] = cur;
+          for (int j = 0; j < K; ++j) {
+            const int idx = u - (K - 1) + j;  // batch position of tap j's input
+            acc += wk[j][e] * ((idx >= 0) ? cur[idx >= 0 ? idx : 0][e]
+                                          : win[idx >= 0 ? 0 : K - 1 + idx][e]);
+          }
+          if (silu) acc = acc * __builtin_amdgcn_rcpf(1.f + __expf(-acc));
+          from_float(&out.v[e], acc);
+        }
+        if (tb + u < t1)
+          *reinterpret_cast<Piece<T, VEC>*>(y + static_cast<long>(tb + u) * C + c0) = out;
+      }
+      // the last K - 1 inputs of this batch precede the next one
+#pragma unroll
+      for (int j = 0; j < K - 1; ++j)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) win[j][e] = cur[TB - (K - 1) + j][e];
     }
   }
   // the block that holds the segment's first tokens hands on its last K - 1 inputs
   if (state_out != nullptr && blockIdx.y == 0) {
     const int L = hi - lo;
-    for (int i = 0; i < K - 1; ++i)
-      state_out[(static_cast<long>(s) * (K - 1) + i) * C + c] = xx(L + i);
+    for (int i = 0; i < K - 1; ++i) {
+      float v[VEC];
+      xx(L + i, v);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e)
+        state_out[(static_cast<long>(s) * (K - 1) + i) * C + c0 + e] = v[e];
+    }
   }
+}
+
+template <typename T, int VEC>
+hipError_t launch_conv_v(const T* x, const float* w, const int32_t* cu, const float* state_in,
+                         T* y, float* state_out, int C, int K, int silu, dim3 grid,
+                         hipStream_t s) {
+  switch (K) {
+#define HYPIC_CONV_CASE(KK)                                                                 \
+  case KK:                                                                                  \
+    hipLaunchKernelGGL((conv_kernel<T, VEC, KK>), grid, dim3(256), 0, s, x, w, cu, state_in, \
+                       y, state_out, C, silu);                                              \
+    break;
+    HYPIC_CONV_CASE(1)
+    HYPIC_CONV_CASE(2)
+    HYPIC_CONV_CASE(3)
+    HYPIC_CONV_CASE(4)
+    HYPIC_CONV_CASE(5)
+    HYPIC_CONV_CASE(6)
+    HYPIC_CONV_CASE(7)
+    HYPIC_CONV_CASE(8)
+#undef HYPIC_CONV_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 template <int DK>
@@ -204,14 +283,20 @@ hipError_t launch_causal_conv(const void* x, const float* w, int bf16, const int
                               int n_seg, int max_len, const float* state_in, void* y,
                               float* state_out, int C, int K, int silu, hipStream_t s) {
   if (n_seg <= 0) return hipSuccess;
-  const dim3 grid(n_seg, max_len > 0 ? (max_len + 63) / 64 : 1, (C + 255) / 256);
-  if (bf16)
-    hipLaunchKernelGGL((conv_kernel<u16>), grid, dim3(256), 0, s, static_cast<const u16*>(x), w,
-                       cu, state_in, static_cast<u16*>(y), state_out, C, K, silu);
-  else
-    hipLaunchKernelGGL((conv_kernel<float>), grid, dim3(256), 0, s, static_cast<const float*>(x),
-                       w, cu, state_in, static_cast<float*>(y), state_out, C, K, silu);
-  return hipGetLastError();
+  if (K < 1 || K > kMaxWidth) return hipErrorInvalidValue;
+  // 16 bytes per lane when every row starts 16-byte aligned, one channel otherwise
+  const int vec = (C % (bf16 ? 8 : 4) == 0) ? (bf16 ? 8 : 4) : 1;
+  const dim3 grid(n_seg, max_len > 0 ? (max_len + 63) / 64 : 1, (C + 256 * vec - 1) / (256 * vec));
+  if (bf16) {
+    const u16* xi = static_cast<const u16*>(x);
+    u16* yo = static_cast<u16*>(y);
+    return (vec == 8) ? launch_conv_v<u16, 8>(xi, w, cu, state_in, yo, state_out, C, K, silu, grid, s)
+                      : launch_conv_v<u16, 1>(xi, w, cu, state_in, yo, state_out, C, K, silu, grid, s);
+  }
+  const float* xi = static_cast<const float*>(x);
+  float* yo = static_cast<float*>(y);
+  return (vec == 4) ? launch_conv_v<float, 4>(xi, w, cu, state_in, yo, state_out, C, K, silu, grid, s)
+                    : launch_conv_v<float, 1>(xi, w, cu, state_in, yo, state_out, C, K, silu, grid, s);
 }
 
 }  // namespace hypic

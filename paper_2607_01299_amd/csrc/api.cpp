@@ -392,6 +392,7 @@ int32_t hypic_rope_rerotate_keys(const hypic_dims* dims, const void* k_in, void*
   if (n_seg < 0 || !good_base(base)) return HYPIC_EINVAL;
   if (n_seg == 0) return HYPIC_OK;
   if (!k_in || !k_out || !cu_seqlens || !cu_seqlens_host || !delta) return HYPIC_EINVAL;
+  if (!aligned16(k_in) || !aligned16(k_out)) return HYPIC_EINVAL;
   const int64_t longest = check_offsets(cu_seqlens_host, n_seg);
   if (longest < 0 || (longest + 63) / 64 > 65535) return HYPIC_EINVAL;
   return hip_status(hypic::launch_rope_keys(k_in, k_out, dims->dtype == HYPIC_BF16, cu_seqlens,
@@ -408,7 +409,7 @@ int32_t hypic_causal_conv(int32_t dtype, int32_t channels, int32_t width, const 
   if (channels < 1 || n_seg < 0) return HYPIC_EINVAL;
   if (n_seg == 0) return HYPIC_OK;
   if (!x || !weight || !y || !cu_seqlens || !cu_seqlens_host) return HYPIC_EINVAL;
-  if (x == y) return HYPIC_EINVAL;
+  if (x == y || !aligned16(x) || !aligned16(y)) return HYPIC_EINVAL;
   const int64_t longest = check_offsets(cu_seqlens_host, n_seg);
   if (longest < 0 || (longest + 63) / 64 > 65535 || (channels + 255) / 256 > 65535)
     return HYPIC_EINVAL;

@@ -264,29 +264,40 @@ def family_seam(family, q, k, v, gate, tok_start, tok_len, w, S_in, *, tok_start
 # causal conv with carried state (Sec. 4.2)
 # ---------------------------------------------------------------------------
 
+def _device_i32(x, device):
+    """A device int32 tensor as is, else a synchronous copy of host values."""
+    if isinstance(x, torch.Tensor) and x.is_cuda:
+        if x.dtype != torch.int32 or not x.is_contiguous():
+            raise HypicError(_lib.HYPIC_EINVAL, "device index arrays must be contiguous int32")
+        return x
+    return _index_pair(x, None, device)[1]
+
+
 def rope_shift_state(S, delta, base=10000.0, out=None):
-    """S [n, h_v, d_k, d_v] float32 -> R(delta[e]) S[e, h] (out may be S)."""
+    """S [n, h_v, d_k, d_v] float32 -> R(delta[e]) S[e, h] (out may be S).
+    delta: [n] int32, a device tensor or host values."""
     lib = _lib.load()
     _contig(S, "S")
     n, h_v, d_k, d_v = S.shape
     dev = S.device
     dims = Dims(h_qk=h_v, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_lib.HYPIC_F32, chunk=64)
-    _, dl = _index_pair(delta, None, dev)
+    dl = _device_i32(delta, dev)
     out = torch.empty_like(S) if out is None else out
     _lib.check(lib.hypic_rope_shift_state(ctypes.byref(dims), _ptr(S), _ptr(out), n, _ptr(dl),
                                           float(base), _stream(dev)))
     return out
 
 
-def rope_rerotate_keys(k, cu_seqlens, delta, base=10000.0, out=None):
-    """k [T, h, d] (bf16 or f32) -> R(delta[s]) k for the tokens of segment s."""
+def rope_rerotate_keys(k, cu_seqlens, delta, base=10000.0, out=None, cu_seqlens_dev=None):
+    """k [T, h, d] (bf16 or f32) -> R(delta[s]) k for the tokens of segment s.
+    delta: [n_seg] int32, a device tensor or host values."""
     lib = _lib.load()
     _contig(k, "k")
     T, h, d = k.shape
     dev = k.device
     dims = Dims(h_qk=h, h_v=h, d_k=d, d_v=d, dtype=_dtype_code(k), chunk=64)
-    cu_h, cu_d = _index_pair(cu_seqlens, None, dev)
-    _, dl = _index_pair(delta, None, dev)
+    cu_h, cu_d = _index_pair(cu_seqlens, cu_seqlens_dev, dev)
+    dl = _device_i32(delta, dev)
     out = torch.empty_like(k) if out is None else out
     _lib.check(lib.hypic_rope_rerotate_keys(ctypes.byref(dims), _ptr(k), _ptr(out), _ptr(cu_d),
                                             _hptr(cu_h), len(cu_h) - 1, _ptr(dl), float(base),
@@ -294,7 +305,8 @@ def rope_rerotate_keys(k, cu_seqlens, delta, base=10000.0, out=None):
     return out
 
 
-def causal_conv(x, weight, cu_seqlens, state_in=None, *, silu=True, want_state=True):
+def causal_conv(x, weight, cu_seqlens, state_in=None, *, silu=True, want_state=True,
+                cu_seqlens_dev=None):
     """x [T, C] (bf16 or f32), weight [C, K] float32 -> (y [T, C], state_out
     [n_seg, K - 1, C] float32 or None)."""
     lib = _lib.load()
@@ -303,7 +315,7 @@ def causal_conv(x, weight, cu_seqlens, state_in=None, *, silu=True, want_state=T
     T, C = x.shape
     K = weight.shape[1]
     dev = x.device
-    cu_h, cu_d = _index_pair(cu_seqlens, None, dev)
+    cu_h, cu_d = _index_pair(cu_seqlens, cu_seqlens_dev, dev)
     n_seg = len(cu_h) - 1
     y = torch.empty_like(x)
     st_out = (torch.empty((n_seg, K - 1, C), dtype=torch.float32, device=dev)

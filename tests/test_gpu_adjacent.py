@@ -115,13 +115,14 @@ def test_rope_rerotate_keys(hy, dt, d):
                 assert rel(o[lo:hi, hh], ref) <= tol, (s, hh)
 
 
-@pytest.mark.parametrize("dt,K,with_state", [(W.F32, 4, True), (W.BF16, 4, False),
-                                             (W.F32, 1, False), (W.BF16, 8, True)])
-def test_causal_conv(hy, dt, K, with_state):
+@pytest.mark.parametrize("dt,K,with_state,C", [(W.F32, 4, True, 300), (W.BF16, 4, False, 300),
+                                               (W.F32, 1, False, 300), (W.BF16, 8, True, 300),
+                                               (W.BF16, 4, True, 2064), (W.F32, 3, True, 1030)])
+def test_causal_conv(hy, dt, K, with_state, C):
     lens = [130, 0, 1, 2, 64, 65, 300]
-    _say("causal conv %s K=%d state=%s lengths %s" % (dt, K, with_state, lens))
+    _say("causal conv %s K=%d state=%s C=%d lengths %s" % (dt, K, with_state, C, lens))
     rng = np.random.default_rng(75)
-    T, C = sum(lens), 300
+    T = sum(lens)
     x = rng.standard_normal((T, C)).astype(np.float32)
     if dt == W.BF16:
         x = W.round_bf16(x)
