@@ -22,7 +22,10 @@
 // (two steps ahead on split grids, one on full-width ones).
 // Small grids split the columns of each head over NCB = 4 workgroups (numbered
 // so that they land on one XCD and share its L2 for P_hat); large grids keep
-// one workgroup per head, so each byte of the pool tuple is read once.
+// one workgroup per head, so each byte of the pool tuple is read once, ordered
+// head-major so that concurrent requests share one head's pool slice in the
+// memory-side cache.  The incoming states are written with non-temporal
+// stores, which keep them from displacing that slice.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -70,8 +73,13 @@ __global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
     chain = full / NCB + b / NCB;
     cb = b % NCB;
   }
-  const int req = chain / args.h_v;
-  const int h = chain % args.h_v;
+  // Split grids are request-major.  Full-width grids are head-major: the
+  // workgroups resident at one time then draw on one head's slice of the pool
+  // (n_pool x 128 KiB at d = 128), which the memory-side cache can keep while
+  // the incoming states stream past it (written non-temporally, below).
+  const int n_req = n_chains / args.h_v;
+  const int req = (NCB == 1) ? chain % n_req : chain / args.h_v;
+  const int h = (NCB == 1) ? chain / n_req : chain % args.h_v;
   const int c0 = cb * NC;
   const long state_sz = static_cast<long>(DK) * DV;
   const long hs = static_cast<long>(req) * args.h_v + h;
@@ -180,7 +188,8 @@ __global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
 #pragma unroll
       for (int mt = 0; mt < NT; ++mt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) const_cast<float*>(tile_ptr(dst, mt))[i * DV] = s[mt][i];
+        for (int i = 0; i < 4; ++i)
+          __builtin_nontemporal_store(s[mt][i], const_cast<float*>(tile_ptr(dst, mt)) + i * DV);
     }
 #pragma unroll
     for (int mt = 0; mt < NT; ++mt) {

@@ -579,8 +579,12 @@ __global__ __launch_bounds__(kCT) void family_compose_kernel(FamComposeArgs a) {
   constexpr bool DIAG = FAM == FAM_DIAGONAL;
   constexpr int LOOK = 2;
   const int tid = threadIdx.x;
+  // head-major: the workgroups resident at one time share one head's slice of
+  // the pool in the memory-side cache; incoming states stream past it
+  // non-temporally
   const int chain = blockIdx.x / NPART, part = blockIdx.x % NPART;
-  const int req = chain / a.h_v, h = chain % a.h_v;
+  const int n_req = static_cast<int>(gridDim.x) / (NPART * a.h_v);
+  const int req = chain % n_req, h = chain / n_req;
   const long state_sz = static_cast<long>(DK) * DV;
   const long hs = static_cast<long>(req) * a.h_v + h;
   int e[NU];
@@ -627,7 +631,9 @@ __global__ __launch_bounds__(kCT) void family_compose_kernel(FamComposeArgs a) {
         if (a.S_incoming != nullptr) {
           float* dst = a.S_incoming + (static_cast<long>(jj) * a.h_v + h) * state_sz;
 #pragma unroll
-          for (int u = 0; u < NU; ++u) *reinterpret_cast<float4*>(dst + e[u]) = s[u];
+          for (int u = 0; u < NU; ++u)
+            __builtin_nontemporal_store(f32x4{s[u].x, s[u].y, s[u].z, s[u].w},
+                                        reinterpret_cast<f32x4*>(dst + e[u]));
         }
 #pragma unroll
         for (int u = 0; u < NU; ++u) {
