@@ -14,7 +14,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "scan.hpp"
+#include "family.hpp"
 
 namespace hypic {
 

@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "../../include/hypic.h"
+#include "family.hpp"
 #include "scan.hpp"
 
 namespace {

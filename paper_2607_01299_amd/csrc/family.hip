@@ -46,7 +46,7 @@
 #include <stdint.h>
 
 #include "mfma.hpp"
-#include "scan.hpp"
+#include "family.hpp"
 
 namespace hypic {
 
