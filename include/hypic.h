@@ -14,6 +14,12 @@
  *                          recurrence from a composed incoming state, emitting
  *                          their outputs and the advanced state (Sec. 4.3, seam
  *                          propagation through linear-attention layers).
+ * The same three for the scalar and diagonal transition families of Tab. 1
+ * (hypic_family_build, hypic_family_compose, hypic_family_seam), and three
+ * reuse-time steps next to the cache: the state RoPE shift of Eq. (7)
+ * (hypic_rope_shift_state), the cached-key re-rotation of Eq. (8)
+ * (hypic_rope_rerotate_keys) and the causal conv with a carried state
+ * (hypic_causal_conv, Sec. 4.2 warm-up).
  *
  * Math (Tab. 1 GDN row, Eq. (2)), per head, S in R^{d_k x d_v}:
  *   S_t = alpha_t (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T,
