@@ -5,7 +5,7 @@ A step is one pass of the whole hot path over one batch of synthetic input:
 segment build (o, S_seg, P_hat, log_decay for every segment and head), Eq. (6)
 composition of the batch's segments in order (emitting the state entering
 each segment) and the seam rescan of every segment's first w tokens from that
-state.  Default workload: 16 heads, d_k = d_v = 128, 8 independent segments of
+state.  ms_per_step_graph reports the same step replayed as one HIP graph.  Default workload: 16 heads, d_k = d_v = 128, 8 independent segments of
 2048 bf16 tokens, chunk 64, seam w = 8.  value = tokens / s over the timed
 steps, inputs resident in HBM.
 
@@ -183,6 +183,7 @@ def bench_segments(torch, cfg, steps, warmup, seam_w):
         pipe.run()
     torch.cuda.synchronize()
     stream = pipe.stream
+    # eager steps, with the build bracketed by events inside each step
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(steps)]
     t0 = time.perf_counter()
@@ -195,6 +196,17 @@ def bench_segments(torch, cfg, steps, warmup, seam_w):
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     build_in_step_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    # the same step replayed as one HIP graph, for reference (the launches of
+    # an eager step already queue back to back, so the graph does not shorten it)
+    pipe.capture()
+    for _ in range(max(warmup, 1)):
+        pipe.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        pipe.replay()
+    torch.cuda.synchronize()
+    dt_graph = time.perf_counter() - t0
     # the build kernel's average launch duration: `steps` launches back to back
     # between one pair of events on the launch stream (amortises the markers)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -210,6 +222,7 @@ def bench_segments(torch, cfg, steps, warmup, seam_w):
     achieved = flop / (build_ms * 1e-3) / 1e12
     return {
         "ms_per_step": dt / steps * 1e3,
+        "ms_per_step_graph": dt_graph / steps * 1e3,
         "tokens": T,
         "build_ms": build_ms,
         "build_ms_in_step": build_in_step_ms,
@@ -471,6 +484,7 @@ def main():
         "data": "synthetic (seeded generators; the paper's datasets are not used)",
         "config": seg["config"],
         "roofline": seg["roofline"],
+        "ms_per_step_graph": seg["ms_per_step_graph"],
         "build_ms": seg["build_ms"],
         "build_ms_in_step": seg["build_ms_in_step"],
         "cpu_baseline": cpu,

@@ -112,6 +112,27 @@ class SegmentPipeline:
         self.compose()
         self.seam()
 
+    def capture(self):
+        """Capture build, composition and seams as one HIP graph (replayed by
+        replay() on the stream current at that time).  The kernels write no
+        memory through memsets, so replays are safe to repeat."""
+        self.run()  # first launches (one-time kernel attribute set-up) stay outside
+        torch.cuda.synchronize(self.device)
+        graph = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream(device=self.device)
+        side.wait_stream(torch.cuda.current_stream(self.device))
+        with torch.cuda.graph(graph, stream=side):
+            h = ctypes.c_void_p(torch.cuda.current_stream(self.device).cuda_stream)
+            _lib.check(self.lib.hypic_build_segment(*(self._build_args[:-1] + (h,))))
+            _lib.check(self.lib.hypic_compose_segments(*(self._compose_args[:-1] + (h,))))
+            _lib.check(self.lib.hypic_seam_rescan(*(self._seam_args[:-1] + (h,))))
+        torch.cuda.synchronize(self.device)
+        self.graph = graph
+        return graph
+
+    def replay(self):
+        self.graph.replay()
+
 
 class ComposeBurst:
     """Requests composed from a pool of cached tuples, then seam rescans."""
