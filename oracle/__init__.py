@@ -13,5 +13,6 @@ from .gdn import (  # noqa: F401
     build_segments,
     compose,
     seam,
+    compose_with_seams,
 )
 from . import families  # noqa: F401,E402  (scalar / diagonal families, RoPE, conv)

@@ -201,3 +201,50 @@ def seam(q, k, v, beta, log_alpha, tok_start, tok_len, w, S_in,
         o_seam[e, :w_eff, h] = o_eh
         S_post[e, h] = S_eh
     return o_seam, S_post
+
+
+def compose_with_seams(P_tail, log_decay_tail, S_tail, q, k, v, beta, log_alpha, seam_start,
+                       seam_len, w, seg_ids, req_offsets, S_prefix=None, req_head_pairs=None):
+    """Reuse with seam windows that advance the state (Sec. 4.3: the seam is left
+    out of the cached tuple and, at reuse, recomputed through the layer from the
+    composed state).
+
+    Pool entry ``i`` is cached as the tuple of its tail, tokens
+    ``[seam_start[i] + w_i, seam_start[i] + seam_len[i])`` with
+    ``w_i = min(w, seam_len[i])`` (``P_tail, log_decay_tail, S_tail`` are built over
+    those tokens), and its seam is its first ``w_i`` tokens.  For request ``r``,
+    starting from the prefix state (zero when None), each listed entry ``i`` in
+    order runs its seam tokens through the recurrence of Eq. (2) from the
+    running state (emitting their outputs and advancing the state), then applies
+    its tail tuple by Eq. (4): ``S <- exp(log_decay_i) P_tail_i S + S_tail_i``.
+
+    Returns (S_out [n_req, h_v, d_k, d_v], o_seam [nnz, w, h_v, d_v] (rows past
+    w_i NaN), S_incoming [nnz, h_v, d_k, d_v], the state entering each listed
+    entry's seam), in the CSR order of ``seg_ids``.
+    """
+    T, h_qk, d_k = np.shape(k)
+    h_v, d_v = np.shape(v)[1], np.shape(v)[2]
+    offs = [int(x) for x in req_offsets]
+    ids = [int(x) for x in seg_ids]
+    n_req = len(offs) - 1
+    S_out = np.full((n_req, h_v, d_k, d_v), np.nan)
+    o_seam = np.full((len(ids), w, h_v, d_v), np.nan)
+    S_inc = np.full((len(ids), h_v, d_k, d_v), np.nan)
+    if req_head_pairs is None:
+        req_head_pairs = [(r, h) for r in range(n_req) for h in range(h_v)]
+    for r, h in req_head_pairs:
+        g = qk_head_of(h, h_v, h_qk)
+        S = np.zeros((d_k, d_v)) if S_prefix is None else np.array(S_prefix[r, h],
+                                                                    dtype=np.float64)
+        for j in range(offs[r], offs[r + 1]):
+            i = ids[j]
+            lo = int(seam_start[i])
+            wi = min(int(w), int(seam_len[i]))
+            S_inc[j, h] = S
+            o_seam[j, :wi, h], S = recurrence(q[lo:lo + wi, g], k[lo:lo + wi, g],
+                                              v[lo:lo + wi, h], beta[lo:lo + wi, h],
+                                              log_alpha[lo:lo + wi, h], S0=S)
+            T_i = np.exp(log_decay_tail[i, h]) * np.asarray(P_tail[i, h], dtype=np.float64)
+            S = T_i @ S + np.asarray(S_tail[i, h], dtype=np.float64)
+        S_out[r, h] = S
+    return S_out, o_seam, S_inc

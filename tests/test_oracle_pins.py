@@ -424,3 +424,75 @@ def test_planted_mistakes_are_caught(kind):
     o_bad, _ = _mutant(kind)(q, k, v, beta, a)
     assert _rel(o_good, o_ref) < 1e-12
     assert _rel(o_bad, o_ref) > 1e-3
+
+
+# --------------------------------------------------------------------------
+# Seam windows that advance the state (Sec. 4.3, reading A)
+# --------------------------------------------------------------------------
+
+def test_seam_advance_reuse_equals_concatenated_recurrence():
+    """Entries cached as tail tuples over [w, L) and reused with their seams run
+    from the composed state reproduce, for each request, the recurrence over the
+    concatenation of its segments behind the prefix: the end state, and the
+    outputs at every seam position (including a segment shorter than w)."""
+    rng = np.random.default_rng(91)
+    d_k, d_v, h_qk, h_v, w = 6, 5, 1, 2, 4
+    lens = [9, 3, 12, 7]
+    cu = np.concatenate([[0], np.cumsum(lens)])
+    T = int(cu[-1])
+    q = rng.standard_normal((T, h_qk, d_k))
+    k = rng.standard_normal((T, h_qk, d_k))
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    v = rng.standard_normal((T, h_v, d_v))
+    beta = rng.uniform(0.1, 0.9, size=(T, h_v))
+    la = rng.uniform(-0.2, 0.0, size=(T, h_v))
+    # tail tuples: tokens [start + w_i, end) of each entry
+    tails = [(int(cu[i]) + min(w, lens[i]), int(cu[i + 1])) for i in range(4)]
+    P = np.zeros((4, h_v, d_k, d_k))
+    ld = np.zeros((4, h_v))
+    S = np.zeros((4, h_v, d_k, d_v))
+    for i, (a, b) in enumerate(tails):
+        for h in range(h_v):
+            _, S[i, h] = gdn.recurrence(q[a:b, 0], k[a:b, 0], v[a:b, h], beta[a:b, h], la[a:b, h])
+            P[i, h], ld[i, h] = gdn.segment_operator(k[a:b, 0], beta[a:b, h], la[a:b, h])
+    ids = [2, 0, 1, 3, 1]
+    offs = [0, 3, 5]
+    prefix = rng.standard_normal((2, h_v, d_k, d_v))
+    S_out, o_seam, S_inc = gdn.compose_with_seams(P, ld, S, q, k, v, beta, la, cu[:-1], lens, w,
+                                                  ids, offs, S_prefix=prefix)
+    for r in range(2):
+        sel = ids[offs[r]:offs[r + 1]]
+        idx = np.concatenate([np.arange(cu[i], cu[i + 1]) for i in sel])
+        for h in range(h_v):
+            o_full, S_full = gdn.recurrence(q[idx, 0], k[idx, 0], v[idx, h], beta[idx, h],
+                                            la[idx, h], S0=prefix[r, h])
+            assert np.allclose(S_out[r, h], S_full, atol=1e-12, rtol=0)
+            pos = 0
+            for j, i in enumerate(sel):
+                wi = min(w, lens[i])
+                jj = offs[r] + j
+                assert np.allclose(o_seam[jj, :wi, h], o_full[pos:pos + wi], atol=1e-12, rtol=0)
+                assert np.all(np.isnan(o_seam[jj, wi:, h]))
+                pos += lens[i]
+    # the incoming state of the first listed entry is the prefix
+    assert np.array_equal(S_inc[0], prefix[0])
+
+
+def test_seam_advance_differs_from_full_tuples_plus_advancing_seam():
+    """Applying the full-segment tuple after a seam that already advanced the
+    state counts the seam tokens twice: the result is wrong, so the tuple must be
+    the tail's (a planted-mistake check on the reading)."""
+    rng = np.random.default_rng(92)
+    d, L, w = 5, 10, 4
+    q, k, v = (rng.standard_normal((L, 1, d)) for _ in range(3))
+    k /= np.linalg.norm(k, axis=-1, keepdims=True)
+    beta = rng.uniform(0.2, 0.9, size=(L, 1))
+    la = rng.uniform(-0.2, 0.0, size=(L, 1))
+    _, S_full_tuple = gdn.recurrence(q[:, 0], k[:, 0], v[:, 0], beta[:, 0], la[:, 0])
+    P_full, ld_full = gdn.segment_operator(k[:, 0], beta[:, 0], la[:, 0])
+    prefix = rng.standard_normal((1, 1, d, d))
+    wrong, _, _ = gdn.compose_with_seams(P_full[None, None], np.array([[ld_full]]),
+                                         S_full_tuple[None, None], q, k, v, beta, la, [0], [L],
+                                         w, [0], [0, 1], S_prefix=prefix)
+    _, right = gdn.recurrence(q[:, 0], k[:, 0], v[:, 0], beta[:, 0], la[:, 0], S0=prefix[0, 0])
+    assert np.linalg.norm(wrong[0, 0] - right) / np.linalg.norm(right) > 1e-3
