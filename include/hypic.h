@@ -19,7 +19,8 @@
  * reuse-time steps next to the cache: the state RoPE shift of Eq. (7)
  * (hypic_rope_shift_state), the cached-key re-rotation of Eq. (8)
  * (hypic_rope_rerotate_keys) and the causal conv with a carried state
- * (hypic_causal_conv, Sec. 4.2 warm-up).
+ * (hypic_causal_conv, Sec. 4.2 warm-up).  hypic_compose_with_seams reuses tail
+ * tuples with seam windows that advance the state (Sec. 4.3).
  *
  * Math (Tab. 1 GDN row, Eq. (2)), per head, S in R^{d_k x d_v}:
  *   S_t = alpha_t (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T,
@@ -36,8 +37,8 @@
  *   enqueued and no output is touched.
  * - Pointers are DEVICE pointers unless the name ends in _host (host memory,
  *   read only during the call).  The caller owns all memory; the library never
- *   allocates or frees, keeps no pointer after returning and has no mutable
- *   global state, so calls are reentrant.
+ *   allocates or frees device or host memory, keeps no pointer after
+ *   returning and has no mutable global state, so calls are reentrant.
  * - Every call enqueues its kernels on `stream` (a hipStream_t; NULL means the
  *   default stream) and returns without synchronising.
  * - Layouts are dense row-major (C order).  Token tensors are packed:
@@ -256,6 +257,52 @@ int32_t hypic_family_seam(const hypic_dims* dims, int32_t family, const void* q,
                           int32_t n_entries, int32_t w, const float* S_in, void* o_seam,
                           float* S_post, void* workspace, size_t workspace_bytes,
                           void* stream);
+
+/*
+ * hypic_compose_with_seams -- reuse with seam windows that advance the state
+ * (Sec. 4.3: the first w tokens of each reused segment are left out of its
+ * cached tuple and recomputed through the layer from the composed state).
+ * Pool entry i is cached as the tuple of its tail, the tokens
+ * [seam_start[i] + w_i, seam_start[i] + seam_len[i]) with w_i = min(w, seam_len[i])
+ * (built with hypic_build_segment over those tokens), and its seam is its first
+ * w_i tokens.  For each request r and v-head h, from S = S_prefix[r, h] (zero
+ * when NULL), each listed entry i = seg_ids[j] in order does
+ *     (o_seam[j, 0 .. w_i - 1, h], S) = the recurrence of Eq. (2) over the seam from S;
+ *     S <- exp(log_decay[i, h]) * P_hat[i, h] @ S + S_seg[i, h]        (Eq. (4))
+ * then S_out[r, h] = S.  Composing the tail tuples this way equals the
+ * recurrence over the concatenated segments.
+ *   P_hat, log_decay, S_seg  the pool of tail tuples, as in hypic_compose_segments.
+ *   q, k, v, beta, log_alpha  packed token arrays ([n_tokens, ...], as in the build)
+ *                            holding every entry's seam tokens.
+ *   seam_start, seam_len [n_pool] int32 device / _host: first token and segment
+ *                            length of entry i (seam_len >= 1; seam_start + w_i <= n_tokens).
+ *   w                        seam width >= 1.
+ *   seg_ids, req_offsets     CSR request lists as in hypic_compose_segments.
+ *   S_prefix [n_req, h_v, d_k, d_v] f32 or NULL; S_out [n_req, h_v, d_k, d_v] f32
+ *                            (16-byte aligned).
+ *   o_seam [nnz, w, h_v, d_v] dtype, in the CSR order of seg_ids; rows >= w_i
+ *                            are not written.
+ *   workspace  at least hypic_seam_compose_workspace_bytes(dims, n_req, max_n)
+ *              bytes, max_n = the longest request's entry count: two running
+ *              states per request and the per-step entry lists.
+ * dims->dtype gives the token type and the composition arithmetic as in
+ * hypic_seam_rescan and hypic_compose_segments.  Requests run longest first
+ * (Eq. (9) list order); each step enqueues one seam and one composition launch
+ * over the requests still running.
+ */
+size_t hypic_seam_compose_workspace_bytes(const hypic_dims* dims, int32_t n_req,
+                                          int32_t max_per_request);
+int32_t hypic_compose_with_seams(const hypic_dims* dims, const float* P_hat,
+                                 const float* log_decay, const float* S_seg, int32_t n_pool,
+                                 const void* q, const void* k, const void* v, const float* beta,
+                                 const float* log_alpha, int32_t n_tokens,
+                                 const int32_t* seam_start, const int32_t* seam_start_host,
+                                 const int32_t* seam_len, const int32_t* seam_len_host, int32_t w,
+                                 const int32_t* seg_ids, const int32_t* seg_ids_host,
+                                 const int32_t* req_offsets, const int32_t* req_offsets_host,
+                                 int32_t n_req, const float* S_prefix, float* S_out,
+                                 void* o_seam, void* workspace, size_t workspace_bytes,
+                                 void* stream);
 
 /* ------------------------------------------------------------------------
  * Reuse-time steps next to the linear-attention cache.

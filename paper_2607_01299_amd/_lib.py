@@ -36,6 +36,8 @@ EXPORTS = (
     "hypic_rope_shift_state",
     "hypic_rope_rerotate_keys",
     "hypic_causal_conv",
+    "hypic_seam_compose_workspace_bytes",
+    "hypic_compose_with_seams",
 )
 
 HYPIC_FAMILY_SCALAR = 1
@@ -107,6 +109,12 @@ def load():
     lib.hypic_rope_rerotate_keys.restype = _I32
     lib.hypic_causal_conv.argtypes = [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _I32, _P]
     lib.hypic_causal_conv.restype = _I32
+    lib.hypic_seam_compose_workspace_bytes.argtypes = [ctypes.POINTER(Dims), _I32, _I32]
+    lib.hypic_seam_compose_workspace_bytes.restype = _SZ
+    lib.hypic_compose_with_seams.argtypes = [
+        ctypes.POINTER(Dims), _P, _P, _P, _I32, _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _I32,
+        _P, _P, _P, _P, _I32, _P, _P, _P, _P, _SZ, _P]
+    lib.hypic_compose_with_seams.restype = _I32
     _lib = lib
     return lib
 

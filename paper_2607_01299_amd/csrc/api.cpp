@@ -351,6 +351,146 @@ int32_t hypic_family_seam(const hypic_dims* dims, int32_t family, const void* q,
 }
 
 // ---------------------------------------------------------------------------
+// reuse with seam windows that advance the state (Sec. 4.3)
+// ---------------------------------------------------------------------------
+
+namespace {
+
+struct SeamComposeLayout {
+  size_t states, order, lists, total;  // byte offsets of the parts, total size
+};
+
+SeamComposeLayout seam_compose_layout(const hypic_dims* d, int64_t n_req, int64_t max_n) {
+  SeamComposeLayout l{};
+  const size_t state = static_cast<size_t>(d->h_v) * d->d_k * d->d_v * sizeof(float);
+  l.states = 0;
+  l.order = round_up(2 * static_cast<size_t>(n_req) * state);
+  l.lists = l.order + round_up(static_cast<size_t>(n_req) * sizeof(int32_t));
+  l.total = l.lists + round_up((4 * static_cast<size_t>(max_n) * n_req + n_req + 1) *
+                               sizeof(int32_t));
+  return l;
+}
+
+}  // namespace
+
+size_t hypic_seam_compose_workspace_bytes(const hypic_dims* dims, int32_t n_req,
+                                          int32_t max_per_request) {
+  if (check_dims(dims) != HYPIC_OK || n_req <= 0 || max_per_request < 0) return 0;
+  return seam_compose_layout(dims, n_req, max_per_request).total;
+}
+
+int32_t hypic_compose_with_seams(const hypic_dims* dims, const float* P_hat,
+                                 const float* log_decay, const float* S_seg, int32_t n_pool,
+                                 const void* q, const void* k, const void* v, const float* beta,
+                                 const float* log_alpha, int32_t n_tokens,
+                                 const int32_t* seam_start, const int32_t* seam_start_host,
+                                 const int32_t* seam_len, const int32_t* seam_len_host, int32_t w,
+                                 const int32_t* seg_ids, const int32_t* seg_ids_host,
+                                 const int32_t* req_offsets, const int32_t* req_offsets_host,
+                                 int32_t n_req, const float* S_prefix, float* S_out,
+                                 void* o_seam, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  int32_t st = check_dims(dims);
+  if (st != HYPIC_OK) return st;
+  if (n_req < 0 || n_pool < 0 || n_tokens < 0 || w < 1) return HYPIC_EINVAL;
+  if (n_req == 0) return HYPIC_OK;
+  if (!req_offsets || !req_offsets_host || !S_out || !aligned16(S_out) ||
+      (S_prefix && !aligned16(S_prefix)))
+    return HYPIC_EINVAL;
+  if (req_offsets_host[0] != 0) return HYPIC_EINVAL;
+  int32_t max_n = 0;
+  for (int32_t r = 0; r < n_req; ++r) {
+    const int32_t n = req_offsets_host[r + 1] - req_offsets_host[r];
+    if (n < 0) return HYPIC_EINVAL;
+    max_n = n > max_n ? n : max_n;
+  }
+  const int32_t nnz = req_offsets_host[n_req];
+  if (nnz > 0) {
+    if (!P_hat || !log_decay || !S_seg || !seg_ids || !seg_ids_host || !q || !k || !v || !beta ||
+        !log_alpha || !seam_start || !seam_start_host || !seam_len || !seam_len_host || !o_seam)
+      return HYPIC_EINVAL;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o_seam)) return HYPIC_EINVAL;
+    for (int32_t j = 0; j < nnz; ++j)
+      if (seg_ids_host[j] < 0 || seg_ids_host[j] >= n_pool) return HYPIC_EINVAL;
+    for (int32_t i = 0; i < n_pool; ++i) {
+      const int64_t len = seam_len_host[i], start = seam_start_host[i];
+      if (len < 1 || start < 0) return HYPIC_EINVAL;
+      if (start + (len < w ? len : w) > n_tokens) return HYPIC_EINVAL;
+    }
+  }
+  if (static_cast<int64_t>(n_req) * dims->h_v * 4 > 0x7fffffff ||
+      static_cast<int64_t>(max_n) * n_req > 0x7fffffff)
+    return HYPIC_EINVAL;
+  const SeamComposeLayout l = seam_compose_layout(dims, n_req, max_n);
+  if (workspace == nullptr || workspace_bytes < l.total) return HYPIC_EWORKSPACE;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  unsigned char* ws = static_cast<unsigned char*>(workspace);
+  const long state_floats = static_cast<long>(dims->h_v) * dims->d_k * dims->d_v;
+  float* cur = reinterpret_cast<float*>(ws + l.states);
+  float* tmp = cur + static_cast<long>(n_req) * state_floats;
+  int32_t* order = reinterpret_cast<int32_t*>(ws + l.order);
+  int32_t* lists = reinterpret_cast<int32_t*>(ws + l.lists);
+  const long plane = static_cast<long>(max_n) * n_req;
+  int32_t *ts = lists, *tl = lists + plane, *sid = lists + 2 * plane, *orow = lists + 3 * plane;
+  int32_t* iota = lists + 4 * plane;
+
+  // requests longest first (Eq. (9) list order, ties by index): the requests
+  // still running at step j are ranks 0 .. A_j - 1
+  st = hip_status(hypic::launch_lpt_order(req_offsets, n_req, order, s));
+  if (st == HYPIC_OK && max_n > 0)
+    st = hip_status(hypic::launch_seam_steps(order, req_offsets, seg_ids, seam_start, seam_len,
+                                             n_req, max_n, ts, tl, sid, orow, iota, s));
+  if (st == HYPIC_OK)
+    st = hip_status(hypic::launch_permute_states(S_prefix, cur, order, n_req, state_floats, 0, s));
+  for (int32_t j = 0; j < max_n && st == HYPIC_OK; ++j) {
+    int32_t active = 0;  // A_j: requests with more than j entries
+    for (int32_t r = 0; r < n_req; ++r)
+      active += (req_offsets_host[r + 1] - req_offsets_host[r]) > j;
+    // seam: the running state of each active request through its entry's
+    // first w tokens, outputs to the entry's CSR row
+    hypic::ScanArgs a{};
+    a.q = q;
+    a.k = k;
+    a.v = v;
+    a.beta = beta;
+    a.log_alpha = log_alpha;
+    a.h_qk = dims->h_qk;
+    a.h_v = dims->h_v;
+    a.group = dims->h_v / dims->h_qk;
+    a.n_tokens = n_tokens;
+    a.mode = 1;
+    a.n_roles = 1;
+    a.tok_start = ts + static_cast<long>(j) * n_req;
+    a.tok_len = tl + static_cast<long>(j) * n_req;
+    a.w = w;
+    a.S_in = cur;
+    a.o = o_seam;
+    a.S_out = tmp;
+    a.out_entry = orow + static_cast<long>(j) * n_req;
+    st = hip_status(hypic::launch_scan(a, dims->dtype == HYPIC_BF16, dims->d_k, dims->d_v,
+                                       dims->chunk, active, s));
+    if (st != HYPIC_OK) break;
+    // the entry's tail tuple, Eq. (4)
+    hypic::ComposeArgs c{};
+    c.P_hat = P_hat;
+    c.log_decay = log_decay;
+    c.S_seg = S_seg;
+    c.seg_ids = sid + static_cast<long>(j) * n_req;
+    c.req_offsets = iota;
+    c.S_prefix = tmp;
+    c.S_out = cur;
+    c.S_incoming = nullptr;
+    c.h_v = dims->h_v;
+    st = hip_status(hypic::launch_compose(c, dims->dtype == HYPIC_F32, dims->d_k, dims->d_v,
+                                          active, s));
+  }
+  if (st == HYPIC_OK)
+    st = hip_status(hypic::launch_permute_states(cur, S_out, order, n_req, state_floats, 1, s));
+  return st;
+}
+
+// ---------------------------------------------------------------------------
 // reuse-time steps next to the cache: RoPE state shift, key re-rotation, conv
 // ---------------------------------------------------------------------------
 

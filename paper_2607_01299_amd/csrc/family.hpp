@@ -61,4 +61,12 @@ hipError_t launch_causal_conv(const void* x, const float* w, int bf16, const int
                               int n_seg, int max_len, const float* state_in, void* y,
                               float* state_out, int C, int K, int silu, hipStream_t s);
 
+hipError_t launch_seam_steps(const int32_t* order, const int32_t* req_offsets,
+                             const int32_t* seg_ids, const int32_t* seam_start,
+                             const int32_t* seam_len, int n_req, int max_n, int32_t* ts,
+                             int32_t* tl, int32_t* sid, int32_t* orow, int32_t* iota,
+                             hipStream_t s);
+hipError_t launch_permute_states(const float* src, float* dst, const int32_t* order, int n,
+                                 long floats, int scatter, hipStream_t s);
+
 }  // namespace hypic

@@ -424,7 +424,7 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(ScanArgs args) {
               if (args.mode == 0)
                 row = c0 + r;
               else
-                row = static_cast<long>(seg) * args.w + (c0 - lo) + r;
+                row = static_cast<long>(seam_out_entry(args, seg)) * args.w + (c0 - lo) + r;
               TIn* orow = og + row * v_stride + h * DV + col0;
 #pragma unroll
               for (int nt = 0; nt < NTS; ++nt) IO::store(orow + nt * 16 + ln, oq[mt][nt][i]);

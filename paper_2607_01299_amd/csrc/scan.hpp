@@ -36,7 +36,13 @@ struct ScanArgs {
   float* log_decay;          // build, may be null
   int32_t n_inline;          // build: > 0 when the order is held in order_inline
   uint16_t order_inline[kInlineOrder];
+  const int32_t* out_entry;  // seam: output entry of each entry (NULL: the same)
 };
+
+// Entry of the seam output o[n, w, h_v, d_v] that seam entry e writes.
+__device__ __forceinline__ int32_t seam_out_entry(const ScanArgs& a, int e) {
+  return a.out_entry != nullptr ? a.out_entry[e] : e;
+}
 
 // Segment scheduled at position `rank` of the longest-first order.
 __device__ __forceinline__ int32_t segment_of_rank(const ScanArgs& a, int rank) {

@@ -864,8 +864,9 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
 #pragma unroll
       for (int s = 0; s < 4; ++s) vA[s] = frag_of(vn[s >> 1], s & 1);
       const long orow0 = (args.mode == 0) ? static_cast<long>(c0)
-                         : ch.batched ? static_cast<long>(ch.e0 + c) * args.w
-                                      : static_cast<long>(ch.seg) * args.w + (c0 - ch.lo);
+                         : ch.batched ? static_cast<long>(seam_out_entry(args, ch.e0 + c)) * args.w
+                                      : static_cast<long>(seam_out_entry(args, ch.seg)) * args.w +
+                                            (c0 - ch.lo);
 #pragma unroll
       for (int tq = 0; tq < 2; ++tq) {
         f32x16 acc = zero16();

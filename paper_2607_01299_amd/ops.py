@@ -326,3 +326,41 @@ def causal_conv(x, weight, cu_seqlens, state_in=None, *, silu=True, want_state=T
                                      _hptr(cu_h), n_seg, _ptr(state_in), _ptr(y), _ptr(st_out),
                                      1 if silu else 0, _stream(dev)))
     return y, st_out
+
+
+# ---------------------------------------------------------------------------
+# reuse with seam windows that advance the state (Sec. 4.3)
+# ---------------------------------------------------------------------------
+
+def compose_with_seams(P_hat, log_decay, S_seg, q, k, v, beta, log_alpha, seam_start, seam_len,
+                       w, seg_ids, req_offsets, S_prefix=None):
+    """Tail tuples of the pool composed with each entry's seam run from the
+    running state first (see include/hypic.h).  Token dtype gives the
+    composition arithmetic (bf16: split bf16; f32: float32 matrix cores).
+    Returns (S_out [n_req, h_v, d_k, d_v], o_seam [nnz, w, h_v, d_v])."""
+    lib = _lib.load()
+    for name, t in (("P_hat", P_hat), ("log_decay", log_decay), ("S_seg", S_seg), ("q", q),
+                    ("k", k), ("v", v), ("beta", beta), ("log_alpha", log_alpha)):
+        _contig(t, name)
+    dev = S_seg.device
+    n_pool, h_v, d_k, d_v = S_seg.shape
+    dims = make_dims(q, v, 64)
+    ss_h, ss_d = _index_pair(seam_start, None, dev)
+    sl_h, sl_d = _index_pair(seam_len, None, dev)
+    ids_h, ids_d = _index_pair(seg_ids, None, dev)
+    off_h, off_d = _index_pair(req_offsets, None, dev)
+    n_req = len(off_h) - 1
+    nnz = int(off_h[-1])
+    max_n = int(np.max(np.diff(off_h))) if n_req > 0 else 0
+    S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=torch.float32, device=dev)
+    o_seam = torch.empty((nnz, w, h_v, d_v), dtype=q.dtype, device=dev)
+    need = lib.hypic_seam_compose_workspace_bytes(ctypes.byref(dims), n_req, max_n)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    if S_prefix is not None:
+        _contig(S_prefix, "S_prefix")
+    _lib.check(lib.hypic_compose_with_seams(
+        ctypes.byref(dims), _ptr(P_hat), _ptr(log_decay), _ptr(S_seg), n_pool, _ptr(q), _ptr(k),
+        _ptr(v), _ptr(beta), _ptr(log_alpha), q.shape[0], _ptr(ss_d), _hptr(ss_h), _ptr(sl_d),
+        _hptr(sl_h), int(w), _ptr(ids_d), _hptr(ids_h), _ptr(off_d), _hptr(off_h), n_req,
+        _ptr(S_prefix), _ptr(S_out), _ptr(o_seam), _ptr(ws), need, _stream(dev)))
+    return S_out, o_seam

@@ -188,6 +188,48 @@ class ComposeBurst:
         self.seam()
 
 
+class SeamAdvanceBurst:
+    """Requests composed from a pool of tail tuples with each entry's seam run
+    from the running state first (hypic_compose_with_seams), pre-bound."""
+
+    def __init__(self, P_hat, log_decay, S_seg, seg_ids, req_offsets, tokens, seam_start,
+                 seam_len, w, *, S_prefix=None):
+        self.lib = _lib.load()
+        dev = S_seg.device
+        self.stream = torch.cuda.current_stream(dev)
+        sp = ctypes.c_void_p(self.stream.cuda_stream)
+        n_pool, h_v, d_k, d_v = S_seg.shape
+        q, k, v, beta, log_alpha = tokens
+        self.tokens = tokens
+        self.pool = (P_hat, log_decay, S_seg)
+        self.dims = Dims(h_qk=q.shape[1], h_v=h_v, d_k=d_k, d_v=d_v, dtype=_dtype_code(q),
+                         chunk=64)
+        self.ss_h, self.ss_d = _i32_pair(seam_start, dev)
+        self.sl_h, self.sl_d = _i32_pair(seam_len, dev)
+        self.ids_h, self.ids_d = _i32_pair(seg_ids, dev)
+        self.off_h, self.off_d = _i32_pair(req_offsets, dev)
+        n_req = len(self.off_h) - 1
+        nnz = int(self.off_h[-1])
+        max_n = int(np.max(np.diff(self.off_h))) if n_req > 0 else 0
+        self.n_req, self.nnz, self.h_v, self.d_k, self.d_v = n_req, nnz, h_v, d_k, d_v
+        self.S_prefix = S_prefix
+        self.S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=torch.float32, device=dev)
+        self.o_seam = torch.empty((nnz, w, h_v, d_v), dtype=q.dtype, device=dev)
+        need = self.lib.hypic_seam_compose_workspace_bytes(ctypes.byref(self.dims), n_req, max_n)
+        self.ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        self._args = (
+            ctypes.byref(self.dims), _p(P_hat), _p(log_decay), _p(S_seg), n_pool, _p(q), _p(k),
+            _p(v), _p(beta), _p(log_alpha), q.shape[0], _p(self.ss_d),
+            self.ss_h.ctypes.data_as(ctypes.c_void_p), _p(self.sl_d),
+            self.sl_h.ctypes.data_as(ctypes.c_void_p), int(w), _p(self.ids_d),
+            self.ids_h.ctypes.data_as(ctypes.c_void_p), _p(self.off_d),
+            self.off_h.ctypes.data_as(ctypes.c_void_p), n_req, _p(S_prefix), _p(self.S_out),
+            _p(self.o_seam), _p(self.ws), need, sp)
+
+    def run(self):
+        _lib.check(self.lib.hypic_compose_with_seams(*self._args))
+
+
 class FamilyPipeline:
     """Scalar- or diagonal-family build, composition of the batch's segments in
     order (one request, or the CSR lists given) and seam rescan, pre-bound."""

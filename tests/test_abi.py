@@ -227,3 +227,30 @@ def test_adjacent_calls_reject_bad_arguments(lib):
                                  None) == _lib.HYPIC_EUNSUPPORTED
     assert lib.hypic_causal_conv(_lib.HYPIC_F32, 16, 4, FAKE, FAKE, FAKE, hcu, 0, None, FAKE_ODD,
                                  None, 1, None) == _lib.HYPIC_OK
+
+
+def test_compose_with_seams_rejects_bad_arguments(lib):
+    d = _dims()
+    ids = np.array([0, 1], dtype=np.int32)
+    offs = np.array([0, 2], dtype=np.int32)
+    ss = np.array([0, 10], dtype=np.int32)
+    sl = np.array([10, 10], dtype=np.int32)
+    h = lambda a: a.ctypes.data_as(ctypes.c_void_p)  # noqa: E731
+
+    def call(ids=ids, offs=offs, ss=ss, sl=sl, n_pool=2, n_tokens=20, w=8, ws=FAKE, ws_bytes=1 << 30,
+             o=FAKE):
+        return lib.hypic_compose_with_seams(
+            ctypes.byref(d), FAKE, FAKE, FAKE, n_pool, FAKE, FAKE, FAKE, FAKE, FAKE, n_tokens, FAKE,
+            h(ss), FAKE, h(sl), w, FAKE, h(ids), FAKE, h(offs), len(offs) - 1, None, FAKE, o, ws,
+            ws_bytes, None)
+
+    assert call(ids=np.array([0, 2], dtype=np.int32)) == _lib.HYPIC_EINVAL      # id >= n_pool
+    assert call(n_tokens=15) == _lib.HYPIC_EINVAL                                # seam past the end
+    assert call(sl=np.array([10, 0], dtype=np.int32)) == _lib.HYPIC_EINVAL       # empty entry
+    assert call(w=0) == _lib.HYPIC_EINVAL
+    assert call(o=FAKE_ODD) == _lib.HYPIC_EINVAL
+    assert call(ws=None) == _lib.HYPIC_EWORKSPACE
+    need = lib.hypic_seam_compose_workspace_bytes(ctypes.byref(d), 1, 2)
+    assert need >= 2 * 4 * 128 * 128 * 4
+    assert call(ws_bytes=need - 1) == _lib.HYPIC_EWORKSPACE
+    assert call(offs=np.array([0], dtype=np.int32)) == _lib.HYPIC_OK             # no request
