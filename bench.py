@@ -269,6 +269,14 @@ def bench_compose_burst(torch, steps, warmup):
     nnz, h_v = burst.nnz, burst.h_v
     byts = float(compose_bytes_per_head_step(burst.d_k, burst.d_v)) * nnz * h_v
     gbs = byts / (comp_ms * 1e-3) / 1e9
+    # the same requests with seams that advance the state (Sec. 4.3): the pool
+    # tuples read as tail tuples, each entry's 64 tokens as its seam
+    from paper_2607_01299_amd.pipeline import SeamAdvanceBurst
+    adv = SeamAdvanceBurst(P, g, S, p["seg_ids"], p["req_offsets"], toks, p["tok_start_pool"],
+                           p["seam_len_pool"], p["w"])
+    adv.run()
+    adv_ms = _events_ms(torch, adv.stream, adv.run, max(steps // 2, 2))
+    del adv
     return {
         "compositions_per_s": nnz / (dt / steps),
         "requests_per_s": burst.n_req / (dt / steps),
@@ -278,6 +286,8 @@ def bench_compose_burst(torch, steps, warmup):
                      "frac": gbs / PEAK_HBM_GBS,
                      "traffic": measured_traffic("compose", W.CONFIG_NAMES[5]),
                      "kernel": "compose_kernel", "bytes_per_launch": byts},
+        "seam_advance": {"ms_per_burst": adv_ms, "compositions_per_s": nnz / (adv_ms * 1e-3),
+                         "note": "seams run from the running state, then tail tuples (Sec. 4.3)"},
         "config": {"workload": W.CONFIG_NAMES[5], "requests": burst.n_req,
                    "compositions": nnz, "pool": int(p["n_pool"]), "h_v": h_v,
                    "d_k": burst.d_k, "d_v": burst.d_v, "seam_w": p["w"], "seed": p["seed"]},

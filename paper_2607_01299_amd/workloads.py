@@ -186,6 +186,8 @@ def pool_workload(seed=None, n_pool=512, n_req=256, n_min=8, n_max=64,
     return {"P_hat": P_hat, "log_decay": log_decay, "S_seg": S_seg,
             "seg_ids": seg_ids, "req_offsets": req_offsets, "tokens": toks,
             "tok_start": tok_start, "tok_len": tok_len, "w": w,
+            "tok_start_pool": (np.arange(n_pool) * seam_tokens).astype(np.int32),
+            "seam_len_pool": np.full(n_pool, seam_tokens, dtype=np.int32),
             "h_qk": heads, "h_v": heads, "d_k": d, "d_v": d, "dtype": BF16,
             "chunk": 64, "cfg": 5, "seed": seed, "n_pool": n_pool}
 
