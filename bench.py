@@ -361,7 +361,9 @@ def bench_families(torch, steps, warmup, seam_w):
             "build_ms": build_ms,
             "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                          "frac": gbs / PEAK_HBM_GBS, "traffic": None,
-                         "kernel": "family_scan_kernel (build)", "bytes_per_launch": byts},
+                         "kernel": ("family_pipe_kernel (build)" if family == "scalar"
+                                    else "family_scan_kernel (build)"),
+                         "bytes_per_launch": byts},
             "compose_burst": {"compositions_per_s": burst.nnz / (comp_ms * 1e-3),
                               "compose_ms": comp_ms,
                               "roofline": {"bound": "hbm", "achieved": cgbs,

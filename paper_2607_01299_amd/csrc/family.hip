@@ -26,17 +26,22 @@
 // consecutive tokens of a chunk to be above about -80 (float32 range); the
 // scalar path has no such limit.
 //
-// Organisation: one workgroup of 4 waves runs one (segment or seam entry,
-// v-head, 64-column block) chain over its chunks in order.  Its barriers wait
-// for LDS traffic only, so the next chunk's global loads and this chunk's
-// output stores stay in flight across them.  Each wave owns 16
-// state columns with all d_k rows in registers.  Per chunk the workgroup
-// stages Q, K and its V columns in LDS (register prefetch of the next chunk
-// runs meanwhile), forms the gate prefix and the decayed operands, the
-// 16 x 16 tiles of A on the matrix cores, then each wave its outputs and its
-// state columns.  bf16 inputs use bf16 matrix-core products with float32
-// accumulation (every decayed operand is rounded to bf16 once); float32
-// inputs use the float32 matrix cores.
+// Organisation: one workgroup of 8 waves runs one (segment or seam entry,
+// v-head, column block) chain over its chunks in order; its barriers wait for
+// LDS traffic only, so global loads and output stores stay in flight across
+// them.  Two kernels:
+//  * family_scan_kernel (diagonal family; float32 inputs of either family):
+//    per chunk the whole workgroup stages Q, K and its V columns in LDS
+//    (register prefetch of the next chunk runs meanwhile), forms the gate
+//    prefix and the decayed operands, the 16 x 16 tiles of A on the matrix
+//    cores, then the outputs and the state, which stays in registers (each
+//    wave a 16-column group and a share of the d_k rows).
+//  * family_pipe_kernel (scalar family, bf16 inputs): four waves hold the
+//    state and make the outputs of chunk c while the other four stage and
+//    form chunk c + 1, double-buffered.
+// bf16 inputs use bf16 matrix-core products with float32 accumulation (every
+// decayed operand is rounded to bf16 once); float32 inputs use the float32
+// matrix cores.
 //
 // Composition (Eq. (6) with the compressed operators of Tab. 3) is
 // elementwise: S <- exp(log_decay_i) . S + S_seg_i, streamed 16 bytes per
@@ -116,6 +121,17 @@ __device__ __forceinline__ Frag<float> frag_row(const float* M, int ld, int row,
   f.x[4] = hi.x; f.x[5] = hi.y; f.x[6] = hi.z; f.x[7] = hi.w;
   return f;
 }
+// frag_row over a token-minor operand stored with its 4-token groups permuted:
+// token t of the row sits at t ^ x (x a multiple of 8, uniform over the wave)
+__device__ __forceinline__ Frag<u16> frag_row_sw(const u16* M, int ld, int row, int kb, int g,
+                                                 int x) {
+  const u16* p = M + row * ld;
+  const u16x4 lo = *reinterpret_cast<const u16x4*>(p + ((kb + 4 * g) ^ x));
+  const u16x4 hi = *reinterpret_cast<const u16x4*>(p + ((kb + 16 + 4 * g) ^ x));
+  Frag<u16> f;
+  f.x = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  return f;
+}
 // slot j = M[row][kb + kap(g, j)] * s[kb + kap(g, j)]
 template <typename ST>
 __device__ __forceinline__ Frag<ST> frag_row_scaled(const ST* M, int ld, int row, int kb, int g,
@@ -183,6 +199,15 @@ __device__ __forceinline__ float elem(const uint4& w, int e, const u16*) {
 }
 __device__ __forceinline__ float elem(const uint4& w, int e, const float*) {
   return __uint_as_float(word_of(w, e));
+}
+// element e of two bf16 rows, a in the low half and b in the high half
+__device__ __forceinline__ uint32_t pair_raw(const uint4& a, const uint4& b, int e) {
+  const uint32_t wa = word_of(a, e >> 1), wb = word_of(b, e >> 1);
+  return (e & 1) ? ((wa >> 16) | (wb & 0xffff0000u)) : ((wa & 0xffffu) | (wb << 16));
+}
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return static_cast<uint32_t>(__builtin_bit_cast(u16, static_cast<__bf16>(lo))) |
+         (static_cast<uint32_t>(__builtin_bit_cast(u16, static_cast<__bf16>(hi))) << 16);
 }
 __device__ __forceinline__ void put_raw(u16* p, const uint4& w, int e) {
   const uint32_t word = word_of(w, e >> 1);
@@ -574,6 +599,296 @@ __global__ __launch_bounds__(kFT) void family_scan_kernel(FamArgs args) {
 }
 
 // ---------------------------------------------------------------------------
+// Scalar family, bf16 inputs, software-pipelined: four state waves run chunk
+// c's outputs and state update while four producer waves stage and form chunk
+// c + 1 (its operands double-buffered in LDS).  Producers issue every global
+// load and the state waves every output store, so neither waits on the other's
+// memory operations.  Per iteration: stage A (state: outputs of c; producers:
+// stage c + 1, its gate prefix and decayed keys, prefetch c + 2), stage C
+// (state: update of c; producers: the A tiles of c + 1), each closed by an
+// LDS-only barrier.  (The diagonal family keeps the 8-wave kernel above: its
+// tile-referred operands make the producer side the longer one, 0.23 ms
+// against 0.22 ms on 16 heads x 8 x 2048 tokens.)
+// ---------------------------------------------------------------------------
+template <int DK>
+struct PipeLds {
+  static constexpr int LDK = DK + 8;  // Q, K rows (token-major)
+  static constexpr int LDT = FC + 8;  // rows of the token-minor operands and of A
+  // The token-minor operands are written as 4-byte token pairs by lanes that
+  // run over 8-column groups; their tokens are permuted per 16-row band (row
+  // r keeps token t at t ^ (SW * (r >> 4)), SW = 16 for V^T and for the keys
+  // at d_k = 64, 8 for the keys at d_k = 128) so those writes meet 64
+  // distinct banks, while every 4-token group the matrix cores read stays whole.
+  static constexpr int SWV = 16, SWK = (DK == 128) ? 8 : 16;
+  u16 q[2][FC * LDK];    // Q, by chunk parity
+  u16 kdt[2][DK * LDT];  // (K . exp(b_last - b))^T
+  u16 vt[2][64 * LDT];   // V^T of the block's 64 columns
+  u16 a[2][FC * LDT];    // A (lower 16 x 16 tiles; the upper tiles read stay 0)
+  u16 k[FC * LDK];       // K; producers only
+  float bc[2][FC], gam[2][FC];  // prefix b of the gate, exp(b)
+};
+
+template <int DK, int DV>
+__global__ __launch_bounds__(512) void family_pipe_kernel(FamArgs args) {
+  using L = PipeLds<DK>;
+  constexpr int LDK = L::LDK, LDT = L::LDT, SWV = L::SWV, SWK = L::SWK;
+  constexpr int PT = 256;                 // producer threads
+  constexpr int NQ = FC * DK / (8 * PT);  // 16-byte loads of Q (and K) per producer thread
+  constexpr int NV = FC * 64 / (8 * PT);  // 16-byte loads of V
+  constexpr int NM = DK / 16;             // state row tiles
+  static_assert(NQ >= 2 && NV == 2, "tile split");
+  static_assert(sizeof(L) <= 160 * 1024, "LDS budget");
+
+  extern __shared__ __align__(16) unsigned char smem_raw[];
+  L& sm = *reinterpret_cast<L*>(smem_raw);
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = tid & 63;
+  const int g = lane >> 4, ln = lane & 15;
+  const bool producer = wave >= 4;
+  const int ptid = tid - PT;  // producer thread index
+
+  // ---- work item: XCD-aware numbering of the column blocks of one chain ----
+  constexpr int n_cb = DV / 64;
+  const int n_chains = static_cast<int>(gridDim.x) / n_cb;
+  const int full = (n_chains / 8) * 8 * n_cb;
+  int chain, cb;
+  if (static_cast<int>(blockIdx.x) < full) {
+    const int slot = blockIdx.x / 8;
+    chain = (slot / n_cb) * 8 + blockIdx.x % 8;
+    cb = slot % n_cb;
+  } else {
+    const int b = blockIdx.x - full;
+    chain = full / n_cb + b / n_cb;
+    cb = b % n_cb;
+  }
+  const int rank = chain / args.h_v;
+  const int h = chain % args.h_v;
+  const int hk = h / args.group;
+  int seg, lo, hi;
+  if (args.mode == 0) {
+    seg = fam_segment_of_rank(args, rank);
+    lo = args.cu_seqlens[seg];
+    hi = args.cu_seqlens[seg + 1];
+  } else {
+    seg = rank;
+    lo = args.tok_start[seg];
+    const int len = args.tok_len[seg];
+    hi = lo + ((len < args.w) ? len : args.w);
+  }
+  lo = (lo < 0) ? 0 : ((lo > args.n_tokens) ? args.n_tokens : lo);
+  hi = (hi < lo) ? lo : ((hi > args.n_tokens) ? args.n_tokens : hi);
+  const int nc = (hi - lo + FC - 1) / FC;
+
+  const long qk_stride = static_cast<long>(args.h_qk) * DK;
+  const long v_stride = static_cast<long>(args.h_v) * DV;
+  const long sh = static_cast<long>(seg) * args.h_v + h;
+
+  // the upper tiles of A read by the A V products, (0, 1) and (2, 3), stay zero
+  for (int idx = tid; idx < 2 * 2 * 256; idx += 512) {
+    const int par = idx >> 9, t = (idx >> 8) & 1, e = idx & 255;
+    sm.a[par][(32 * t + (e >> 4)) * LDT + 32 * t + 16 + (e & 15)] = 0;
+  }
+
+  if (!producer) {
+    // ======================= state waves ===================================
+    const int col16 = 16 * wave;           // columns inside the block
+    const int col = cb * 64 + col16;        // ... and in the state
+    f32x4 st[NM];
+    if (args.mode == 1) {
+      const float* s_in = args.S_in + sh * DK * DV + col + ln;
+#pragma unroll
+      for (int mt = 0; mt < NM; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) st[mt][i] = s_in[(mt * 16 + 4 * g + i) * DV];
+    } else {
+#pragma unroll
+      for (int mt = 0; mt < NM; ++mt) st[mt] = zero4();
+    }
+    const int ocol = static_cast<int>(h * DV + col + ln);
+    for (int c = -1; c < nc; ++c) {
+      const int buf = c & 1;
+      const int c0 = lo + c * FC;
+      const int n = (hi - c0 < FC) ? hi - c0 : FC;
+      Frag<u16> bv[2];
+      if (c >= 0) {
+        // ---- stage A: outputs of chunk c, (Q S0) . exp(b) + A V ----
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+          bv[kt] = frag_row_sw(sm.vt[buf], LDT, col16 + ln, 32 * kt, g, SWV * wave);
+        Frag<u16> bs[NM / 2];
+#pragma unroll
+        for (int kt = 0; kt < NM / 2; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            bs[kt].set(i, st[2 * kt][i]);
+            bs[kt].set(4 + i, st[2 * kt + 1][i]);
+          }
+        const long orow0 = (args.mode == 0) ? static_cast<long>(c0)
+                                            : static_cast<long>(seg) * args.w + (c0 - lo);
+        const auto rso = rsrc(args.o ? static_cast<const u16*>(args.o) + orow0 * v_stride : nullptr,
+                              args.o ? n * v_stride * 2 : 0);
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) {
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int kt = 0; kt < NM / 2; ++kt)
+            acc = mma(frag_row(sm.q[buf], LDK, mt * 16 + ln, 32 * kt, g), bs[kt], acc);
+          const float4 gm = *reinterpret_cast<const float4*>(sm.gam[buf] + mt * 16 + 4 * g);
+          acc[0] *= gm.x;
+          acc[1] *= gm.y;
+          acc[2] *= gm.z;
+          acc[3] *= gm.w;
+#pragma unroll
+          for (int kt = 0; kt < 2; ++kt)
+            if (32 * kt < 16 * (mt + 1))
+              acc = mma(frag_row(sm.a[buf], LDT, mt * 16 + ln, 32 * kt, g), bv[kt], acc);
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            bstore(rso, ((mt * 16 + 4 * g + i) * static_cast<int>(v_stride) + ocol) * 2, acc[i],
+                   static_cast<u16*>(nullptr));
+        }
+      }
+      lds_barrier();
+      // ---- stage C: state update of chunk c ----
+      if (c >= 0) {
+        const float g_last = __expf(sm.bc[buf][FC - 1]);
+#pragma unroll
+        for (int mt = 0; mt < NM; ++mt) {
+          f32x4 acc = st[mt] * g_last;
+#pragma unroll
+          for (int kt = 0; kt < 2; ++kt)
+            acc = mma(frag_row_sw(sm.kdt[buf], LDT, mt * 16 + ln, 32 * kt, g, SWK * mt), bv[kt],
+                      acc);
+          st[mt] = acc;
+        }
+      }
+      lds_barrier();
+    }
+    if (args.S_out != nullptr) {
+      float* so = args.S_out + sh * DK * DV + col + ln;
+#pragma unroll
+      for (int mt = 0; mt < NM; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) so[(mt * 16 + 4 * g + i) * DV] = st[mt][i];
+    }
+  } else {
+    // ======================= producer waves ================================
+    const int pw = wave - 4;
+    const u16* qg = static_cast<const u16*>(args.q) + hk * DK;
+    const u16* kg = static_cast<const u16*>(args.k) + hk * DK;
+    const u16* vg = static_cast<const u16*>(args.v) + h * DV + cb * 64;
+    uint4 rq[NQ], rk[NQ], rv[NV];
+    float rg;  // the gate of token `lane` (every producer wave holds the chunk's 64)
+    // K and V go in token pairs: item i of this thread is tokens 2 rp and
+    // 2 rp + 1 of one 8-column group, items running over the groups fastest
+    // (whole rows per load), so the token-minor copies are written as pairs
+    const int rpv = ptid / 8, cvv = ptid % 8;  // V: one item
+    auto prefetch = [&](int c0, int n) __attribute__((always_inline)) {
+      const auto rsq = rsrc(qg + static_cast<long>(c0) * qk_stride, n * qk_stride * 2);
+      const auto rsk = rsrc(kg + static_cast<long>(c0) * qk_stride, n * qk_stride * 2);
+      const auto rsv = rsrc(vg + static_cast<long>(c0) * v_stride, n * v_stride * 2);
+#pragma unroll
+      for (int u = 0; u < NQ; ++u) {
+        const int idx = u * PT + ptid;
+        const int r = idx / (DK / 8), cv = idx % (DK / 8);
+        rq[u] = bload16(rsq, static_cast<int>((r * qk_stride + cv * 8) * 2));
+      }
+#pragma unroll
+      for (int u = 0; u < NQ; ++u) {
+        const int idx = (u >> 1) * PT + ptid;
+        const int r = 2 * (idx / (DK / 8)) + (u & 1), cv = idx % (DK / 8);
+        rk[u] = bload16(rsk, static_cast<int>((r * qk_stride + cv * 8) * 2));
+      }
+#pragma unroll
+      for (int u = 0; u < NV; ++u)
+        rv[u] = bload16(rsv, static_cast<int>(((2 * rpv + u) * v_stride + cvv * 8) * 2));
+      const auto rsg = rsrc(args.gate + static_cast<long>(c0) * args.h_v, n * args.h_v * 4);
+      rg = bload4(rsg, (lane * args.h_v + h) * 4);
+    };
+    if (nc > 0) prefetch(lo, (hi - lo < FC) ? hi - lo : FC);
+    float ld_acc = 0.f;  // log_decay: sum of the chunk gate totals
+    for (int p = 0; p <= nc; ++p) {  // the chunk this iteration forms
+      const int buf = p & 1;
+      const int c0 = lo + p * FC;
+      const bool active = p < nc;
+      // ---- stage A: stage chunk p, its gate prefix and decayed keys;
+      // prefetch chunk p + 1 ----
+      if (active) {
+#pragma unroll
+        for (int u = 0; u < NQ; ++u) {
+          const int idx = u * PT + ptid;
+          const int r = idx / (DK / 8), cv = idx % (DK / 8);
+          *reinterpret_cast<uint4*>(sm.q[buf] + r * LDK + cv * 8) = rq[u];
+        }
+#pragma unroll
+        for (int u = 0; u < NQ; ++u) {
+          const int idx = (u >> 1) * PT + ptid;
+          const int r = 2 * (idx / (DK / 8)) + (u & 1), cv = idx % (DK / 8);
+          *reinterpret_cast<uint4*>(sm.k + r * LDK + cv * 8) = rk[u];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          *reinterpret_cast<uint32_t*>(sm.vt[buf] + (cvv * 8 + e) * LDT +
+                                       ((2 * rpv) ^ (SWV * (cvv >> 1)))) =
+              pair_raw(rv[0], rv[1], e);
+        float b = rg;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const float u = __shfl_up(b, off, 64);
+          if (lane >= off) b += u;
+        }
+        const float b_last = __shfl(b, 63, 64);
+        const float dec = __expf(b_last - b);
+        if (pw == 0) {
+          sm.bc[buf][lane] = b;
+          sm.gam[buf][lane] = __expf(b);
+          ld_acc += b_last;
+        }
+#pragma unroll
+        for (int j = 0; j < NQ / 2; ++j) {
+          const int idx = j * PT + ptid;
+          const int rp = idx / (DK / 8), cv = idx % (DK / 8);
+          const float d0 = __shfl(dec, 2 * rp, 64), d1 = __shfl(dec, 2 * rp + 1, 64);
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            *reinterpret_cast<uint32_t*>(sm.kdt[buf] + (cv * 8 + e) * LDT +
+                                         ((2 * rp) ^ (SWK * (cv >> 1)))) =
+                pack_bf16(elem(rk[2 * j], e, static_cast<const u16*>(nullptr)) * d0,
+                          elem(rk[2 * j + 1], e, static_cast<const u16*>(nullptr)) * d1);
+        }
+        const int c1 = c0 + FC;
+        prefetch(c1, (hi - c1 < FC) ? hi - c1 : FC);
+      }
+      lds_barrier();
+      // ---- stage C: the lower 16 x 16 tiles of A for chunk p ----
+      if (active) {
+        for (int tile = pw; tile < 10; tile += 4) {
+          const int tq = (tile < 1) ? 0 : ((tile < 3) ? 1 : ((tile < 6) ? 2 : 3));
+          const int tk = tile - tq * (tq + 1) / 2;
+          f32x4 acc = zero4();
+#pragma unroll
+          for (int kb = 0; kb < DK; kb += 32)
+            acc = mma(frag_row(sm.q[buf], LDK, tq * 16 + ln, kb, g),
+                      frag_row(sm.k, LDK, tk * 16 + ln, kb, g), acc);
+          const int key = tk * 16 + ln;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int t = tq * 16 + 4 * g + i;
+            const float x = acc[i] * __expf(fminf(sm.bc[buf][t] - sm.bc[buf][key], 0.f));
+            stv(sm.a[buf] + t * LDT + key, (key <= t) ? x : 0.f);
+          }
+        }
+      }
+      lds_barrier();
+    }
+    if (args.mode == 0 && args.log_decay != nullptr && cb == 0 && ptid == 0)
+      args.log_decay[sh] = ld_acc;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // composition: S <- exp(log_decay_i) . S + S_seg_i, elementwise
 // ---------------------------------------------------------------------------
 constexpr int kCT = 256;          // threads
@@ -669,6 +984,24 @@ hipError_t launch_fscan_t(const FamArgs& a, int n_items, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int DK, int DV>
+hipError_t launch_fpipe_t(const FamArgs& a, int n_items, hipStream_t s) {
+  constexpr int bytes = static_cast<int>(sizeof(PipeLds<DK>));
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&family_pipe_kernel<DK, DV>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((family_pipe_kernel<DK, DV>), dim3(n_items), dim3(512), bytes, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_fpipe_d(const FamArgs& a, int d_k, int d_v, int n_items, hipStream_t s) {
+  if (d_k == 64 && d_v == 64) return launch_fpipe_t<64, 64>(a, n_items, s);
+  if (d_k == 64 && d_v == 128) return launch_fpipe_t<64, 128>(a, n_items, s);
+  if (d_k == 128 && d_v == 64) return launch_fpipe_t<128, 64>(a, n_items, s);
+  return launch_fpipe_t<128, 128>(a, n_items, s);
+}
+
 template <int FAM, typename ST>
 hipError_t launch_fscan_d(const FamArgs& a, int d_k, int d_v, int n_items, hipStream_t s) {
   if (d_k == 64 && d_v == 64) return launch_fscan_t<FAM, ST, 64, 64>(a, n_items, s);
@@ -710,10 +1043,11 @@ hipError_t launch_family_scan(const FamArgs& a, int family, int bf16, int d_k, i
   const int64_t n_items = static_cast<int64_t>(n_chains) * a.h_v * (d_v / fnc);
   if (n_items > 0x7fffffff) return hipErrorInvalidValue;
   const int n = static_cast<int>(n_items);
+  // scalar family, bf16 inputs: the software-pipelined kernel (64-column blocks)
   if (family == FAM_DIAGONAL)
     return bf16 ? launch_fscan_d<FAM_DIAGONAL, uint16_t>(a, d_k, d_v, n, s)
                 : launch_fscan_d<FAM_DIAGONAL, float>(a, d_k, d_v, n, s);
-  return bf16 ? launch_fscan_d<FAM_SCALAR, uint16_t>(a, d_k, d_v, n, s)
+  return bf16 ? launch_fpipe_d(a, d_k, d_v, n, s)
               : launch_fscan_d<FAM_SCALAR, float>(a, d_k, d_v, n, s);
 }
 
