@@ -56,7 +56,13 @@ TRAFFIC_FILE = os.path.join(HERE, "profiles", "hbm_traffic.json")
 KERNEL_SOURCES = {
     "scan_bf16": ["scan_bf16.hip", "mfma.hpp", "scan.hpp"],
     "compose": ["compose.hip", "mfma.hpp", "scan.hpp"],
+    "family_scalar_build": ["family.hip", "mfma.hpp", "family.hpp"],
+    "family_diagonal_build": ["family.hip", "mfma.hpp", "family.hpp"],
+    "family_scalar_compose": ["family.hip", "mfma.hpp", "family.hpp"],
+    "family_diagonal_compose": ["family.hip", "mfma.hpp", "family.hpp"],
 }
+FAMILY_WORKLOAD = W.CONFIG_NAMES[2] + "; gates from workloads.family_gate (softplus)"
+FAMILY_BURST_WORKLOAD = W.CONFIG_NAMES[5] + " (family tuples)"
 
 
 def _code_only(src):
@@ -360,7 +366,8 @@ def bench_families(torch, steps, warmup, seam_w):
             "ms_per_step": dt * 1e3,
             "build_ms": build_ms,
             "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                         "frac": gbs / PEAK_HBM_GBS, "traffic": None,
+                         "frac": gbs / PEAK_HBM_GBS,
+                         "traffic": measured_traffic("family_%s_build" % family, FAMILY_WORKLOAD),
                          "kernel": ("family_pipe_kernel (build)" if family == "scalar"
                                     else "family_scan_kernel (build)"),
                          "bytes_per_launch": byts},
@@ -368,13 +375,15 @@ def bench_families(torch, steps, warmup, seam_w):
                               "compose_ms": comp_ms,
                               "roofline": {"bound": "hbm", "achieved": cgbs,
                                            "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                                           "frac": cgbs / PEAK_HBM_GBS, "traffic": None,
+                                           "frac": cgbs / PEAK_HBM_GBS,
+                                           "traffic": measured_traffic(
+                                               "family_%s_compose" % family,
+                                               FAMILY_BURST_WORKLOAD),
                                            "kernel": "family_compose_kernel",
                                            "bytes_per_launch": cbytes}},
         }
         del pipe, burst
-    return {"workload": W.CONFIG_NAMES[2] + "; gates from workloads.family_gate (softplus)",
-            "burst_workload": W.CONFIG_NAMES[5] + " (family tuples)", **out}
+    return {"workload": FAMILY_WORKLOAD, "burst_workload": FAMILY_BURST_WORKLOAD, **out}
 
 
 def bench_adjacent(torch, steps):
