@@ -98,6 +98,29 @@ def measured_traffic(kernel, workload):
     return float(rec["fetch_bytes_per_launch"]) + float(rec["write_bytes_per_launch"])
 
 
+MFMA_FILE = os.path.join(HERE, "profiles", "mfma_counters.json")
+
+
+def measured_mfma(kernel, workload):
+    """Matrix-core counters of a kernel from the committed rocprofv3 passes
+    (MfmaUtil: MFMA-busy cycles over active cycles x SIMDs; bf16 MFMA ops x 512),
+    or None when the kernel's sources changed since they were taken."""
+    try:
+        with open(MFMA_FILE) as f:
+            rec = json.load(f).get(kernel)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("workload") != workload:
+        return None
+    if rec.get("src_sha256") != kernel_source_sha256(kernel):
+        return None
+    out = {"mfma_busy_frac": float(rec["mfma_util_pct"]) / 100.0}
+    if rec.get("mfma_bf16_flop_per_launch") is not None:
+        out["mfma_flop_per_launch"] = float(rec["mfma_bf16_flop_per_launch"])
+        out["mfma_over_algorithmic"] = float(rec["counted_over_algorithmic"])
+    return out
+
+
 def copy_calibration(torch, nbytes=1 << 30, reps=3):
     """A plain device-to-device copy of known size, for scaling HBM counters."""
     src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
@@ -235,7 +258,8 @@ def bench_segments(torch, cfg, steps, warmup, seam_w):
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": measured_traffic("scan_bf16", W.CONFIG_NAMES[cfg]),
-                     "kernel": "scan_kernel (segment build)",
+                     "counter": measured_mfma("scan_bf16", W.CONFIG_NAMES[cfg]),
+                     "kernel": "scan_bf16_kernel (segment build)",
                      "flop_per_launch": flop},
         "config": {"workload": W.CONFIG_NAMES[cfg], "segments": len(w["lengths"]),
                    "tokens": T, "h_qk": int(w["q"].shape[1]), "h_v": int(h_v), "d_k": d_k,
@@ -291,6 +315,7 @@ def bench_compose_burst(torch, steps, warmup):
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": gbs / PEAK_HBM_GBS,
                      "traffic": measured_traffic("compose", W.CONFIG_NAMES[5]),
+                     "counter": measured_mfma("compose", W.CONFIG_NAMES[5]),
                      "kernel": "compose_kernel", "bytes_per_launch": byts},
         "seam_advance": {"ms_per_burst": adv_ms, "compositions_per_s": nnz / (adv_ms * 1e-3),
                          "note": "seams run from the running state, then tail tuples (Sec. 4.3)"},
