@@ -16,3 +16,4 @@ from .gdn import (  # noqa: F401
     compose_with_seams,
 )
 from . import families  # noqa: F401,E402  (scalar / diagonal families, RoPE, conv)
+from . import kda  # noqa: F401,E402  (the KDA row of Tab. 1)
