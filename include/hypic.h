@@ -20,7 +20,9 @@
  * (hypic_rope_shift_state), the cached-key re-rotation of Eq. (8)
  * (hypic_rope_rerotate_keys) and the causal conv with a carried state
  * (hypic_causal_conv, Sec. 4.2 warm-up).  hypic_compose_with_seams reuses tail
- * tuples with seam windows that advance the state (Sec. 4.3).
+ * tuples with seam windows that advance the state (Sec. 4.3).  hypic_kda_build
+ * and hypic_kda_seam build and rescan the KDA row of Tab. 1 (delta rule with a
+ * per-channel gate); its tuples compose with hypic_compose_segments.
  *
  * Math (Tab. 1 GDN row, Eq. (2)), per head, S in R^{d_k x d_v}:
  *   S_t = alpha_t (I - beta_t k_t k_t^T) S_{t-1} + beta_t k_t v_t^T,
@@ -257,6 +259,47 @@ int32_t hypic_family_seam(const hypic_dims* dims, int32_t family, const void* q,
                           int32_t n_entries, int32_t w, const float* S_in, void* o_seam,
                           float* S_post, void* workspace, size_t workspace_bytes,
                           void* stream);
+
+/*
+ * hypic_kda_build -- Sec. 4.2 cache tuples for a layer of the KDA row of Tab. 1:
+ *     S_t = (I - beta_t k_t k_t^T) diag(exp(g_t)) S_{t-1} + beta_t k_t v_t^T,
+ *     o_t = S_t^T q_t,
+ * from S = 0 for every segment, with the Tab. 3 operator
+ *     T_C = prod_t (I - beta_t k_t k_t^T) diag(exp(g_t))   (later tokens left)
+ * stored as T_C = exp(log_decay) * P_hat.  log_decay is the sum, over the
+ * segment's chunks of 64 tokens from its start, of each chunk's largest
+ * per-channel gate sum (a scale that keeps P_hat in float32 range); the tuple
+ * (P_hat, log_decay, S_seg) composes with hypic_compose_segments unchanged.
+ *   q, k, v, beta, cu_seqlens, o, S_seg  as in hypic_build_segment.
+ *   gate      [T, h_v, d_k] float32: the per-channel log gates g_t (natural log).
+ *   P_hat     [n_seg, h_v, d_k, d_k] float32 or NULL (no operator; then
+ *             log_decay is not written).
+ *   log_decay [n_seg, h_v] float32, written with P_hat.
+ * q, k, v 16-byte aligned.  The chunked kernel refers each key's gate to its
+ * 16-token tile: every channel's gate sum over any 16 consecutive tokens of a
+ * segment must stay above about -80, else results lose float32 range.
+ * Workspace: hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg) bytes (the
+ * longest-first order of more than 128 segments), as for the GDN build.
+ */
+int32_t hypic_kda_build(const hypic_dims* dims, const void* q, const void* k, const void* v,
+                        const float* beta, const float* gate, const int32_t* cu_seqlens,
+                        const int32_t* cu_seqlens_host, int32_t n_seg, void* o, float* S_seg,
+                        float* P_hat, float* log_decay, void* workspace, size_t workspace_bytes,
+                        void* stream);
+
+/*
+ * hypic_kda_seam -- Sec. 4.3 seam rescan for a KDA layer: entry e runs tokens
+ * [tok_start[e], tok_start[e] + min(w, tok_len[e])) through the KDA recurrence
+ * from S_in[e].  Arguments and outputs as in hypic_seam_rescan with the
+ * per-channel gate [n_tokens, h_v, d_k] in place of log_alpha (w may exceed 64).
+ * Workspace: none.
+ */
+int32_t hypic_kda_seam(const hypic_dims* dims, const void* q, const void* k, const void* v,
+                       const float* beta, const float* gate, int32_t n_tokens,
+                       const int32_t* tok_start, const int32_t* tok_len,
+                       const int32_t* tok_start_host, const int32_t* tok_len_host,
+                       int32_t n_entries, int32_t w, const float* S_in, void* o_seam,
+                       float* S_post, void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * hypic_compose_with_seams -- reuse with seam windows that advance the state

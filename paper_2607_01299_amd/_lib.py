@@ -38,6 +38,8 @@ EXPORTS = (
     "hypic_causal_conv",
     "hypic_seam_compose_workspace_bytes",
     "hypic_compose_with_seams",
+    "hypic_kda_build",
+    "hypic_kda_seam",
 )
 
 HYPIC_FAMILY_SCALAR = 1
@@ -109,6 +111,13 @@ def load():
     lib.hypic_rope_rerotate_keys.restype = _I32
     lib.hypic_causal_conv.argtypes = [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _I32, _P]
     lib.hypic_causal_conv.restype = _I32
+    lib.hypic_kda_build.argtypes = [
+        ctypes.POINTER(Dims), _P, _P, _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _P, _SZ, _P]
+    lib.hypic_kda_build.restype = _I32
+    lib.hypic_kda_seam.argtypes = [
+        ctypes.POINTER(Dims), _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _I32, _P, _P, _P,
+        _P, _SZ, _P]
+    lib.hypic_kda_seam.restype = _I32
     lib.hypic_seam_compose_workspace_bytes.argtypes = [ctypes.POINTER(Dims), _I32, _I32]
     lib.hypic_seam_compose_workspace_bytes.restype = _SZ
     lib.hypic_compose_with_seams.argtypes = [

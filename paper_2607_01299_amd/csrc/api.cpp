@@ -8,6 +8,7 @@
 
 #include "../../include/hypic.h"
 #include "family.hpp"
+#include "kda.hpp"
 #include "scan.hpp"
 
 namespace {
@@ -348,6 +349,112 @@ int32_t hypic_family_seam(const hypic_dims* dims, int32_t family, const void* q,
   return hip_status(hypic::launch_family_scan(a, family, dims->dtype == HYPIC_BF16, dims->d_k,
                                               dims->d_v, n_entries,
                                               static_cast<hipStream_t>(stream)));
+}
+
+// ---------------------------------------------------------------------------
+// the KDA row of Tab. 1
+// ---------------------------------------------------------------------------
+
+int32_t hypic_kda_build(const hypic_dims* dims, const void* q, const void* k, const void* v,
+                        const float* beta, const float* gate, const int32_t* cu_seqlens,
+                        const int32_t* cu_seqlens_host, int32_t n_seg, void* o, float* S_seg,
+                        float* P_hat, float* log_decay, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  int32_t st = check_dims(dims);
+  if (st != HYPIC_OK) return st;
+  if (n_seg < 0) return HYPIC_EINVAL;
+  if (n_seg == 0) return HYPIC_OK;
+  if (!q || !k || !v || !beta || !gate || !cu_seqlens || !cu_seqlens_host || !S_seg)
+    return HYPIC_EINVAL;
+  if (P_hat != nullptr && log_decay == nullptr) return HYPIC_EINVAL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return HYPIC_EINVAL;
+  if (cu_seqlens_host[0] != 0) return HYPIC_EINVAL;
+  for (int32_t s = 0; s < n_seg; ++s)
+    if (cu_seqlens_host[s + 1] < cu_seqlens_host[s]) return HYPIC_EINVAL;
+  if (static_cast<int64_t>(n_seg) * dims->h_v * 2 > 0x7fffffff) return HYPIC_EINVAL;
+  const size_t need = hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return HYPIC_EWORKSPACE;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hypic::KdaArgs a{};
+  if (n_seg <= hypic::kInlineOrder) {
+    int32_t idx[hypic::kInlineOrder];
+    for (int32_t i = 0; i < n_seg; ++i) idx[i] = i;
+    std::stable_sort(idx, idx + n_seg, [&](int32_t x, int32_t y) {
+      return cu_seqlens_host[x + 1] - cu_seqlens_host[x] >
+             cu_seqlens_host[y + 1] - cu_seqlens_host[y];
+    });
+    for (int32_t i = 0; i < n_seg; ++i) a.order_inline[i] = static_cast<uint16_t>(idx[i]);
+    a.n_inline = n_seg;
+  } else {
+    int32_t* order = static_cast<int32_t*>(workspace);
+    st = hip_status(hypic::launch_lpt_order(cu_seqlens, n_seg, order, s));
+    if (st != HYPIC_OK) return st;
+    a.order = order;
+  }
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.gate = gate;
+  a.h_qk = dims->h_qk;
+  a.h_v = dims->h_v;
+  a.group = dims->h_v / dims->h_qk;
+  a.n_tokens = cu_seqlens_host[n_seg];
+  a.mode = 0;
+  a.cu_seqlens = cu_seqlens;
+  a.o = o;
+  a.S_out = S_seg;
+  a.P_hat = P_hat;
+  a.log_decay = log_decay;
+  return hip_status(
+      hypic::launch_kda_scan(a, dims->dtype == HYPIC_BF16, dims->d_k, dims->d_v, n_seg, s));
+}
+
+int32_t hypic_kda_seam(const hypic_dims* dims, const void* q, const void* k, const void* v,
+                       const float* beta, const float* gate, int32_t n_tokens,
+                       const int32_t* tok_start, const int32_t* tok_len,
+                       const int32_t* tok_start_host, const int32_t* tok_len_host,
+                       int32_t n_entries, int32_t w, const float* S_in, void* o_seam,
+                       float* S_post, void* workspace, size_t workspace_bytes, void* stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  int32_t st = check_dims(dims);
+  if (st != HYPIC_OK) return st;
+  if (n_entries < 0 || n_tokens < 0 || w < 1) return HYPIC_EINVAL;
+  if (n_entries == 0) return HYPIC_OK;
+  if (!q || !k || !v || !beta || !gate || !tok_start || !tok_len || !tok_start_host ||
+      !tok_len_host || !S_in || !o_seam)
+    return HYPIC_EINVAL;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return HYPIC_EINVAL;
+  for (int32_t e = 0; e < n_entries; ++e) {
+    const int64_t len = tok_len_host[e];
+    const int64_t start = tok_start_host[e];
+    if (len < 1 || start < 0) return HYPIC_EINVAL;
+    const int64_t w_eff = len < w ? len : w;
+    if (start + w_eff > n_tokens) return HYPIC_EINVAL;
+  }
+  if (static_cast<int64_t>(n_entries) * dims->h_v * 2 > 0x7fffffff) return HYPIC_EINVAL;
+
+  hypic::KdaArgs a{};
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.gate = gate;
+  a.h_qk = dims->h_qk;
+  a.h_v = dims->h_v;
+  a.group = dims->h_v / dims->h_qk;
+  a.n_tokens = n_tokens;
+  a.mode = 1;
+  a.tok_start = tok_start;
+  a.tok_len = tok_len;
+  a.w = w;
+  a.S_in = S_in;
+  a.o = o_seam;
+  a.S_out = S_post;
+  return hip_status(hypic::launch_kda_scan(a, dims->dtype == HYPIC_BF16, dims->d_k, dims->d_v,
+                                           n_entries, static_cast<hipStream_t>(stream)));
 }
 
 // ---------------------------------------------------------------------------

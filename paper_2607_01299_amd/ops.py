@@ -260,6 +260,65 @@ def family_seam(family, q, k, v, gate, tok_start, tok_len, w, S_in, *, tok_start
 
 
 # ---------------------------------------------------------------------------
+# the KDA row of Tab. 1 (delta rule with a per-channel gate)
+# ---------------------------------------------------------------------------
+
+def kda_build(q, k, v, beta, gate, cu_seqlens, cu_seqlens_dev=None, *, want_o=True,
+              want_operator=True):
+    """Zero-start build of every segment of a KDA layer.
+
+    beta: [T, h_v] float32; gate: [T, h_v, d_k] float32 per-channel log gates.
+    Returns dict(o, S_seg, P_hat, log_decay) with T_C = exp(log_decay) P_hat
+    (P_hat and log_decay None without the operator); the tuples compose with
+    compose_segments.
+    """
+    lib = _lib.load()
+    for name, t in (("q", q), ("k", k), ("v", v), ("beta", beta), ("gate", gate)):
+        _contig(t, name)
+    dev = q.device
+    dims = make_dims(q, v, 64)
+    cu_h, cu_d = _index_pair(cu_seqlens, cu_seqlens_dev, dev)
+    n_seg = len(cu_h) - 1
+    T, h_v, d_v = v.shape
+    d_k = q.shape[2]
+    o = torch.empty((T, h_v, d_v), dtype=q.dtype, device=dev) if want_o else None
+    S_seg = torch.empty((n_seg, h_v, d_k, d_v), dtype=torch.float32, device=dev)
+    P_hat = (torch.empty((n_seg, h_v, d_k, d_k), dtype=torch.float32, device=dev)
+             if want_operator else None)
+    log_decay = torch.empty((n_seg, h_v), dtype=torch.float32, device=dev) if want_operator else None
+    ws, ws_bytes = _workspace(_lib.HYPIC_OP_BUILD, dims, n_seg, dev)
+    _lib.check(lib.hypic_kda_build(
+        ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(gate), _ptr(cu_d),
+        _hptr(cu_h), n_seg, _ptr(o), _ptr(S_seg), _ptr(P_hat), _ptr(log_decay), _ptr(ws),
+        ws_bytes, _stream(dev)))
+    return {"o": o, "S_seg": S_seg, "P_hat": P_hat, "log_decay": log_decay}
+
+
+def kda_seam(q, k, v, beta, gate, tok_start, tok_len, w, S_in, *, tok_start_dev=None,
+             tok_len_dev=None, want_post=True):
+    """Seam rescan of each entry's first min(w, tok_len) tokens from S_in for a
+    KDA layer.  Returns (o_seam, S_post or None)."""
+    lib = _lib.load()
+    for name, t in (("q", q), ("k", k), ("v", v), ("beta", beta), ("gate", gate),
+                    ("S_in", S_in)):
+        _contig(t, name)
+    dev = q.device
+    dims = make_dims(q, v, 64)
+    st_h, st_d = _index_pair(tok_start, tok_start_dev, dev)
+    ln_h, ln_d = _index_pair(tok_len, tok_len_dev, dev)
+    n_e = len(st_h)
+    T, h_v, d_v = v.shape
+    d_k = q.shape[2]
+    o_seam = torch.empty((n_e, w, h_v, d_v), dtype=q.dtype, device=dev)
+    S_post = torch.empty((n_e, h_v, d_k, d_v), dtype=torch.float32, device=dev) if want_post else None
+    _lib.check(lib.hypic_kda_seam(
+        ctypes.byref(dims), _ptr(q), _ptr(k), _ptr(v), _ptr(beta), _ptr(gate), T, _ptr(st_d),
+        _ptr(ln_d), _hptr(st_h), _hptr(ln_h), n_e, int(w), _ptr(S_in), _ptr(o_seam),
+        _ptr(S_post), None, 0, _stream(dev)))
+    return o_seam, S_post
+
+
+# ---------------------------------------------------------------------------
 # reuse-time steps: RoPE state shift (Eq. (7)), key re-rotation (Eq. (8)),
 # causal conv with carried state (Sec. 4.2)
 # ---------------------------------------------------------------------------

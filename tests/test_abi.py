@@ -201,6 +201,43 @@ def test_family_calls_reject_unknown_family(lib, family):
     assert _fseam(lib, family, [0], [4]) == _lib.HYPIC_EUNSUPPORTED
 
 
+def _kbuild(lib, cu, beta=FAKE, gate=FAKE, P_hat=FAKE, log_decay=FAKE, q=FAKE, dims=None,
+            ws_bytes=1 << 20):
+    cu = np.asarray(cu, dtype=np.int32)
+    d = _dims() if dims is None else dims
+    return lib.hypic_kda_build(
+        ctypes.byref(d), q, FAKE, FAKE, beta, gate, FAKE, cu.ctypes.data_as(ctypes.c_void_p),
+        len(cu) - 1, FAKE, FAKE, P_hat, log_decay, FAKE, ws_bytes, None)
+
+
+def _kseam(lib, start, length, w=8, n_tokens=100, gate=FAKE, S_in=FAKE):
+    st = np.asarray(start, dtype=np.int32)
+    ln = np.asarray(length, dtype=np.int32)
+    return lib.hypic_kda_seam(
+        ctypes.byref(_dims()), FAKE, FAKE, FAKE, FAKE, gate, n_tokens, FAKE, FAKE,
+        st.ctypes.data_as(ctypes.c_void_p), ln.ctypes.data_as(ctypes.c_void_p), len(st), w,
+        S_in, FAKE, None, None, 0, None)
+
+
+def test_kda_calls_reject_bad_arguments(lib):
+    assert _kbuild(lib, [0, 10, 5]) == _lib.HYPIC_EINVAL           # decreasing offsets
+    assert _kbuild(lib, [3, 10]) == _lib.HYPIC_EINVAL              # offsets not from 0
+    assert _kbuild(lib, [0, 10], gate=None) == _lib.HYPIC_EINVAL
+    assert _kbuild(lib, [0, 10], beta=None) == _lib.HYPIC_EINVAL
+    assert _kbuild(lib, [0, 10], log_decay=None) == _lib.HYPIC_EINVAL  # P_hat without log_decay
+    assert _kbuild(lib, [0, 10], q=FAKE_ODD) == _lib.HYPIC_EINVAL
+    assert _kbuild(lib, [0, 10], dims=_dims(d_k=96)) == _lib.HYPIC_EUNSUPPORTED
+    assert _kbuild(lib, [0, 10], dims=_dims(h_qk=3, h_v=4)) != _lib.HYPIC_OK
+    assert _kbuild(lib, list(range(0, 2000, 10)), ws_bytes=0) == _lib.HYPIC_EWORKSPACE
+    assert _kbuild(lib, [0]) == _lib.HYPIC_OK
+    assert _kseam(lib, [0, 95], [10, 10]) == _lib.HYPIC_EINVAL     # window past the tokens
+    assert _kseam(lib, [0], [0]) == _lib.HYPIC_EINVAL              # empty segment
+    assert _kseam(lib, [0], [4], w=0) == _lib.HYPIC_EINVAL
+    assert _kseam(lib, [0], [4], gate=None) == _lib.HYPIC_EINVAL
+    assert _kseam(lib, [0], [4], S_in=None) == _lib.HYPIC_EINVAL
+    assert _kseam(lib, [], []) == _lib.HYPIC_OK
+
+
 def test_adjacent_calls_reject_bad_arguments(lib):
     d = _dims()
     dl = FAKE
