@@ -42,6 +42,7 @@ from paper_2607_01299_amd import workloads as W  # noqa: E402
 METRIC = "segment-build tokens/s + MFMA util; compositions/s + HBM GB/s (1 MI355X)"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
+PEAK_F32_MFMA_TFLOPS = 157.3
 
 # Algorithmic work of the chunked scan per (token, v-head) at chunk C:
 #   2C(3 d_k + 2 d_v)   K K^T, Q K^T, W, U, (Q K^T . Gamma) Vn
@@ -411,6 +412,51 @@ def bench_families(torch, steps, warmup, seam_w):
     return {"workload": FAMILY_WORKLOAD, "burst_workload": FAMILY_BURST_WORKLOAD, **out}
 
 
+def kda_flops(d_k, d_v, chunk):
+    """Algorithmic FLOPs per (token, v-head) of the chunked KDA build, split by
+    the matrix-core precision each part runs in: the state columns (the Gram
+    K K^T and the A tiles, Y = (K . e^B) S0, N, Q S0, A N, K^T N) in the input
+    precision, the operator columns (Y and N of P_hat, K^T N_P) in float32.
+    The total equals the GDN count of flop_per_token_head."""
+    state = 2 * chunk * (2 * d_k + 2 * d_v) + 6 * d_k * d_v
+    operator = 2 * chunk * d_k + 4 * d_k * d_k
+    return state, operator
+
+
+def bench_kda(torch, steps, warmup):
+    """KDA row of Tab. 1 on the bench workload (16 heads, d = 128, 8 x 2048 bf16
+    tokens, per-channel gates from the diagonal-family generator): the build with
+    its operator, timed with HIP events over back-to-back launches.  The
+    roofline peak is the two-precision one: the state part at the bf16 peak and
+    the operator part at the float32 matrix-core peak, taken in sequence."""
+    from paper_2607_01299_amd import ops
+    w = W.segment_workload(2)
+    q, k, v, beta, _ = _to_dev(w, torch)
+    T = int(w["cu_seqlens"][-1])
+    h_v, d_k, d_v = int(w["v"].shape[1]), w["d_k"], w["d_v"]
+    gate = torch.from_numpy(W.family_gate("diagonal", T, h_v, d_k, w["seed"] + 2000)).cuda()
+    cu = w["cu_seqlens"]
+    for _ in range(warmup):
+        ops.kda_build(q, k, v, beta, gate, cu)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ms = _events_ms(torch, stream, lambda: ops.kda_build(q, k, v, beta, gate, cu), steps)
+    f_state, f_op = kda_flops(d_k, d_v, 64)
+    flop = float(f_state + f_op) * T * h_v
+    achieved = flop / (ms * 1e-3) / 1e12
+    t_min = (float(f_state) * T * h_v / (PEAK_BF16_TFLOPS * 1e12)
+             + float(f_op) * T * h_v / (PEAK_F32_MFMA_TFLOPS * 1e12))
+    peak = flop / t_min / 1e12
+    return {"workload": W.CONFIG_NAMES[2] + "; per-channel gates from workloads.family_gate "
+                        "(diagonal, softplus)",
+            "tokens_per_s": T / (ms * 1e-3), "build_ms": ms,
+            "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                         "frac": achieved / peak, "traffic": None,
+                         "kernel": "kda_scan_kernel (state and operator launches)",
+                         "flop_per_launch": flop,
+                         "peak_note": "bf16 state part at 2500, float32 operator part at 157.3"}}
+
+
 def bench_adjacent(torch, steps):
     """The reuse-time steps next to the cache, each an HBM stream: the Eq. (7)
     state shift over the 512-entry serve-time pool, the Eq. (8) re-rotation of
@@ -499,6 +545,7 @@ def main():
     if args.families_only:
         print(json.dumps({"families": bench_families(torch, args.steps, args.warmup,
                                                      args.seam_w),
+                          "kda": bench_kda(torch, args.steps, args.warmup),
                           "adjacent": bench_adjacent(torch, args.steps)}))
         return
     if args.no_segments:
@@ -513,6 +560,7 @@ def main():
                                                            max(args.warmup // 2, 1))
     fam = None if args.no_families else bench_families(torch, args.steps, args.warmup,
                                                          args.seam_w)
+    kda = None if args.no_families else bench_kda(torch, args.steps, args.warmup)
     adj = None if args.no_families else bench_adjacent(torch, args.steps)
     value = seg["tokens"] / (seg["ms_per_step"] * 1e-3)
     out = {
@@ -536,6 +584,7 @@ def main():
         "cpu_baseline": cpu,
         "compose_burst": burst,
         "families": fam,
+        "kda": kda,
         "adjacent": adj,
     }
     print(json.dumps(out))
