@@ -42,7 +42,6 @@ from paper_2607_01299_amd import workloads as W  # noqa: E402
 METRIC = "segment-build tokens/s + MFMA util; compositions/s + HBM GB/s (1 MI355X)"
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
-PEAK_F32_MFMA_TFLOPS = 157.3
 
 # Algorithmic work of the chunked scan per (token, v-head) at chunk C:
 #   2C(3 d_k + 2 d_v)   K K^T, Q K^T, W, U, (Q K^T . Gamma) Vn
@@ -413,10 +412,9 @@ def bench_families(torch, steps, warmup, seam_w):
 
 
 def kda_flops(d_k, d_v, chunk):
-    """Algorithmic FLOPs per (token, v-head) of the chunked KDA build, split by
-    the matrix-core precision each part runs in: the state columns (the Gram
-    K K^T and the A tiles, Y = (K . e^B) S0, N, Q S0, A N, K^T N) in the input
-    precision, the operator columns (Y and N of P_hat, K^T N_P) in float32.
+    """Algorithmic FLOPs per (token, v-head) of the chunked KDA build, split
+    into the state columns (the Gram K K^T and the A tiles, Y = (K . e^B) S0, N,
+    Q S0, A N, K^T N) and the operator columns (Y and N of P_hat, K^T N_P).
     The total equals the GDN count of flop_per_token_head."""
     state = 2 * chunk * (2 * d_k + 2 * d_v) + 6 * d_k * d_v
     operator = 2 * chunk * d_k + 4 * d_k * d_k
@@ -426,9 +424,9 @@ def kda_flops(d_k, d_v, chunk):
 def bench_kda(torch, steps, warmup):
     """KDA row of Tab. 1 on the bench workload (16 heads, d = 128, 8 x 2048 bf16
     tokens, per-channel gates from the diagonal-family generator): the build with
-    its operator, timed with HIP events over back-to-back launches.  The
-    roofline peak is the two-precision one: the state part at the bf16 peak and
-    the operator part at the float32 matrix-core peak, taken in sequence."""
+    its operator, timed with HIP events over back-to-back launches.  Every
+    product runs on the bf16 matrix cores (the operator columns as three split
+    passes), so the roofline peak is the bf16 one, as for the GDN build."""
     from paper_2607_01299_amd import ops
     w = W.segment_workload(2)
     q, k, v, beta, _ = _to_dev(w, torch)
@@ -444,9 +442,7 @@ def bench_kda(torch, steps, warmup):
     f_state, f_op = kda_flops(d_k, d_v, 64)
     flop = float(f_state + f_op) * T * h_v
     achieved = flop / (ms * 1e-3) / 1e12
-    t_min = (float(f_state) * T * h_v / (PEAK_BF16_TFLOPS * 1e12)
-             + float(f_op) * T * h_v / (PEAK_F32_MFMA_TFLOPS * 1e12))
-    peak = flop / t_min / 1e12
+    peak = PEAK_BF16_TFLOPS
     return {"workload": W.CONFIG_NAMES[2] + "; per-channel gates from workloads.family_gate "
                         "(diagonal, softplus)",
             "tokens_per_s": T / (ms * 1e-3), "build_ms": ms,
@@ -454,7 +450,8 @@ def bench_kda(torch, steps, warmup):
                          "frac": achieved / peak, "traffic": None,
                          "kernel": "kda_scan_kernel (state and operator launches)",
                          "flop_per_launch": flop,
-                         "peak_note": "bf16 state part at 2500, float32 operator part at 157.3"}}
+                         "flop_split": {"state": float(f_state) * T * h_v,
+                                        "operator": float(f_op) * T * h_v}}}
 
 
 def bench_adjacent(torch, steps):

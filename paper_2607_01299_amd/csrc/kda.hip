@@ -26,14 +26,20 @@
 // tile, and each tile pair is completed by the channel vector
 // exp(Bbar_tq - Bbar_tk) <= 1.  Every channel's gate sum over 16 consecutive
 // tokens must stay above about -80 (float32 range), as for the diagonal family.
+// With bf16 operands the state columns form each decayed key
+// exp(B_last - B_t) k_t with one exponential; otherwise (float32 state columns,
+// operator columns) it is the key side times the decay from its tile to the
+// chunk end, which can lose key contributions below about exp(-7) of the
+// chunk's largest where a channel decays by more than 87 within one chunk.
 //
 // Organisation: one 8-wave workgroup runs one (segment or seam entry, v-head,
 // 64-column block) chain over its chunks; each wave holds 16 columns x half the
 // d_k rows of the block's state in registers.  State columns use the input
 // precision on the matrix cores (bf16 operands with float32 accumulation for
-// bf16 inputs); operator columns always use float32 operands on the float32
-// matrix cores, so that the normalised operator does not pick up a bf16
-// rounding per chunk.  The 64 x 64 inverse runs in float32: the four diagonal
+// bf16 inputs); operator columns always keep float32 operands in LDS and run
+// their products as three-pass split bf16, so that the normalised operator
+// does not pick up a one-pass bf16 rounding per chunk.  The 64 x 64 inverse
+// runs in float32: the four diagonal
 // 16 x 16 blocks by forward substitution (one lane per column), then block row
 // by block row, T_ij = -X_i sum_k L_ik T_kj, on the float32 matrix cores.
 
@@ -54,27 +60,54 @@ constexpr int KNC = 64;   // columns per workgroup
 constexpr int NCG = KNC / 16;  // column groups of 16 (waves per row group)
 constexpr int LTD = KC + 4;    // row stride of the float32 64 x 64 matrices
 
-template <typename ST, int DK>
+template <typename ST, int DK, bool OP>
 struct KdaLds {
   static constexpr int PAD = (sizeof(ST) == 2) ? 8 : 4;
   static constexpr int LDK = DK + PAD;  // token-major rows of Q and K
-  static constexpr int LDV = KC + PAD;  // V^T rows
-  ST qk[KC * LDK];    // K . exp(B - Bbar) (G and Y), then Q . exp(B - Bbar) (outputs)
-  ST kk[KC * LDK];    // K, then K . exp(Bbar - B)
-  float lt[KC * LTD]; // diag(beta) G (strict lower) -> its inverse T (in place) -> A
-  ST vt[KNC * LDV];   // V^T of the block's columns (state columns only)
-  Frag<ST> s0f[NCG][DK / 32][64];  // S0 as B fragments: column group, 32-row block, lane
-  Frag<ST> rf[NCG][2][64];         // diag(beta) R, then N, as B fragments over tokens
-  float part[kKT];      // per (token part, channel) gate totals: part pt of channel c at pt d_k + c
-  float fx[6 * DK];     // exp(Bbar_tq - Bbar_tk), tk < tq
-  float hx[4 * DK];     // exp(Bbar) per tile
-  float gl[4 * DK];     // exp(B_last - Bbar) per tile
-  float lx[DK];         // exp(B_last)
-  float beta[KC];
-  float bmax[2];        // per-wave maxima of the channel totals
+  static constexpr int LDV = KC + PAD;  // V^T rows, and rows of the channel-major keys
+  // K . exp(B - Bbar) (G and Y), then Q . exp(B - Bbar) (outputs)
+  alignas(16) ST qk[KC * LDK];
+  alignas(16) ST kk[KC * LDK];    // K, then K . exp(Bbar - B)
+  alignas(16) float lt[KC * LTD]; // diag(beta) G (strict lower) -> its inverse T (in place) -> A
+  // state columns only: V^T of the block's columns; with bf16 operands (PRE)
+  // also K . exp(B) (Y), then Q . exp(B) (outputs), and (K . exp(B_last - B))^T
+  // channel-major (float32 operands form them on the fly: no LDS left for them)
+  static constexpr bool PRE = !OP && sizeof(ST) == 2;
+  alignas(16) ST vt[OP ? 1 : KNC * LDV];
+  alignas(16) ST kb[PRE ? KC * LDK : 1];
+  alignas(16) ST kdt[PRE ? DK * LDV : 1];
+  // S0 as B fragments: column group, 32-row block, lane
+  alignas(16) Frag<ST> s0f[NCG][DK / 32][64];
+  alignas(16) Frag<ST> rf[NCG][2][64];         // diag(beta) R, then N, as B fragments over tokens
+  // per (token part, channel) gate totals: part pt of channel c at pt d_k + c
+  alignas(16) float part[kKT];
+  alignas(16) float fx[6 * DK];     // exp(Bbar_tq - Bbar_tk), tk < tq
+  alignas(16) float hx[4 * DK];     // exp(Bbar) per tile
+  alignas(16) float gl[4 * DK];     // exp(B_last - Bbar) per tile
+  alignas(16) float lx[DK];         // exp(B_last)
+  alignas(16) float beta[KC];
+  alignas(16) float bmax[2];        // per-wave maxima of the channel totals
 };
 
 __device__ __forceinline__ int pair_ix(int tq, int tk) { return tq * (tq - 1) / 2 + tk; }
+
+// One 32-deep product block.  Operator columns (SPLIT) run their float32
+// operands as three bf16 passes (hi hi + hi lo + lo hi: about 2^-16 relative
+// per product, against 2^-9 for one bf16 pass), a sixth of the float32
+// matrix-core time; every other product runs in its operand type.
+template <bool SPLIT>
+__device__ __forceinline__ f32x4 mmk(const Frag<float>& a, const Frag<float>& b, f32x4 c) {
+  if constexpr (SPLIT) {
+    mma_blk<P_SPLIT>(c, a.x, b.x);
+    return c;
+  } else {
+    return mma(a, b, c);
+  }
+}
+template <bool SPLIT>
+__device__ __forceinline__ f32x4 mmk(const Frag<u16>& a, const Frag<u16>& b, f32x4 c) {
+  return mma(a, b, c);
+}
 
 // A-operand fragment of a float32 matrix in the operand type ST
 template <typename ST>
@@ -126,7 +159,7 @@ __device__ __forceinline__ int kda_segment_of_rank(const KdaArgs& a, int rank) {
 // TIN: storage type of q, k, v; ST: operand type; OP: operator columns
 template <typename TIN, typename ST, bool OP, int DK, int DV>
 __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
-  using L = KdaLds<ST, DK>;
+  using L = KdaLds<ST, DK, OP>;
   constexpr int LDK = L::LDK, LDV = L::LDV;
   constexpr int NRG = 8 / NCG;                            // row groups
   constexpr int VEC = 16 / static_cast<int>(sizeof(TIN)); // elements per 16-byte load
@@ -138,6 +171,7 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
   static_assert(NQ >= 1 && NMH % 2 == 0 && NRG == 2, "tile split");
   static_assert(TPT == 16 || TPT == 8, "gate split");
   static_assert(sizeof(L) <= 160 * 1024, "LDS budget");
+  constexpr bool PRE = L::PRE;
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
   L& sm = *reinterpret_cast<L*>(smem_raw);
@@ -316,13 +350,24 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
       float base = 0.f;
       if constexpr (TPT == 8) base = (pt & 1) ? sm.part[(pt - 1) * DK + pc] : 0.f;
       const int t0 = TPT * pt;
+      const float hbt = hb[tile], ehb = __expf(hbt);
 #pragma unroll
-      for (int j = 0; j < TPT; ++j) {
-        const int t = t0 + j;
-        const float rel = base + pre[j];  // B_t - Bbar of the token's tile, <= 0
-        const float kv = ldv(sm.kk + t * LDK + pc);
-        stv(sm.qk + t * LDK + pc, kv * __expf(rel));
-        stv(sm.kk + t * LDK + pc, kv * __expf(-rel));
+      for (int j8 = 0; j8 < TPT; j8 += 8) {
+        float kd[8];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          const int j = j8 + jj, t = t0 + j;
+          const float rel = base + pre[j];  // B_t - Bbar of the token's tile, <= 0
+          const float kv = ldv(sm.kk + t * LDK + pc);
+          const float e = __expf(rel);
+          stv(sm.qk + t * LDK + pc, kv * e);
+          stv(sm.kk + t * LDK + pc, kv * __expf(-rel));
+          if constexpr (PRE) {
+            stv(sm.kb + t * LDK + pc, kv * e * ehb);                 // K exp(B_t)
+            kd[jj] = kv * __expf(b_last - hbt - rel);                // K exp(B_last - B_t)
+          }
+        }
+        if constexpr (PRE) st8(sm.kdt + pc * LDV + t0 + j8, kd);
       }
       if (TPT == 16 || (pt & 1) == 0) {
 #pragma unroll
@@ -354,7 +399,7 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
           fa = frag_row_scaled(sm.qk, LDK, tq * 16 + ln, kb, g, sm.fx + pair_ix(tq, tk) * DK);
         else
           fa = frag_row(sm.qk, LDK, tq * 16 + ln, kb, g);
-        acc = mma(fa, frag_row(sm.kk, LDK, tk * 16 + ln, kb, g), acc);
+        acc = mmk<OP>(fa, frag_row(sm.kk, LDK, tk * 16 + ln, kb, g), acc);
       }
       const int key = tk * 16 + ln;
 #pragma unroll
@@ -370,9 +415,14 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
         const int mt = 2 * rgrp + mh;  // token tile
         f32x4 acc = zero4();
 #pragma unroll
-        for (int kt = 0; kt < DK / 32; ++kt)
-          acc = mma(frag_row_scaled(sm.qk, LDK, mt * 16 + ln, 32 * kt, g, sm.hx + mt * DK),
-                    sm.s0f[cg][kt][lane], acc);
+        for (int kt = 0; kt < DK / 32; ++kt) {
+          Frag<ST> fa;
+          if constexpr (PRE)
+            fa = frag_row(sm.kb, LDK, mt * 16 + ln, 32 * kt, g);
+          else
+            fa = frag_row_scaled(sm.qk, LDK, mt * 16 + ln, 32 * kt, g, sm.hx + mt * DK);
+          acc = mmk<OP>(fa, sm.s0f[cg][kt][lane], acc);
+        }
         const float4 bt = *reinterpret_cast<const float4*>(sm.beta + mt * 16 + 4 * g);
         float vv[4] = {0.f, 0.f, 0.f, 0.f};
         if constexpr (!OP) {
@@ -428,11 +478,19 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
     if constexpr (!OP) {
       float base = 0.f;
       if constexpr (TPT == 8) base = (pt & 1) ? sm.part[(pt - 1) * DK + pc] : 0.f;
+      float hbt = 0.f;  // Bbar of this thread's tile
+#pragma unroll
+      for (int p = 0; p < ((TPT == 16) ? pt : pt / 2); ++p)
+        hbt += (TPT == 16) ? sm.part[p * DK + pc]
+                           : sm.part[(2 * p) * DK + pc] + sm.part[(2 * p + 1) * DK + pc];
+      const float ehb = __expf(hbt);
 #pragma unroll
       for (int j = 0; j < TPT; ++j) {
         const int t = TPT * pt + j;
         ST* qp = sm.qk + t * LDK + pc;
-        stv(qp, ldv(qp) * __expf(base + pre[j]));
+        const float qv = ldv(qp) * __expf(base + pre[j]);
+        stv(qp, qv);
+        if constexpr (PRE) stv(sm.kb + t * LDK + pc, qv * ehb);  // Q exp(B_t)
       }
     }
 #pragma unroll
@@ -441,11 +499,14 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
       if (wave < bi) {
         const int bj = wave;
         f32x4 m = zero4();
-        for (int bk = bj; bk < bi; ++bk) m = mm16(sm.lt, LTD, 16 * bi, 16 * bk, 16 * bk, 16 * bj, m, g, ln);
-        const float4 a = *reinterpret_cast<const float4*>(sm.lt + (16 * bi + ln) * LTD + 16 * bi + 4 * g);
+        for (int bk = bj; bk < bi; ++bk)
+          m = mm16(sm.lt, LTD, 16 * bi, 16 * bk, 16 * bk, 16 * bj, m, g, ln);
+        const float4 a =
+            *reinterpret_cast<const float4*>(sm.lt + (16 * bi + ln) * LTD + 16 * bi + 4 * g);
         const float av[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
-        for (int j = 0; j < 4; ++j) tij = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j], m[j], tij, 0, 0, 0);
+        for (int j = 0; j < 4; ++j)
+          tij = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j], m[j], tij, 0, 0, 0);
       }
       lds_barrier();
       if (wave < bi) {
@@ -464,7 +525,8 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
         if (32 * kt < 16 * (mt + 1))
-          acc = mma(frag_f32<ST>(sm.lt, LTD, mt * 16 + ln, 32 * kt, g), sm.rf[cg][kt][lane], acc);
+          acc = mmk<OP>(frag_f32<ST>(sm.lt, LTD, mt * 16 + ln, 32 * kt, g), sm.rf[cg][kt][lane],
+                        acc);
       nt[mh] = acc;
     }
     lds_barrier();
@@ -490,7 +552,7 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
             fa = frag_row_scaled(sm.qk, LDK, tq * 16 + ln, kb, g, sm.fx + pair_ix(tq, tk) * DK);
           else
             fa = frag_row(sm.qk, LDK, tq * 16 + ln, kb, g);
-          acc = mma(fa, frag_row(sm.kk, LDK, tk * 16 + ln, kb, g), acc);
+          acc = mmk<OP>(fa, frag_row(sm.kk, LDK, tk * 16 + ln, kb, g), acc);
         }
         const int key = tk * 16 + ln;
 #pragma unroll
@@ -514,13 +576,19 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
         const int mt = 2 * rgrp + mh;
         f32x4 acc = zero4();
 #pragma unroll
-        for (int kt = 0; kt < DK / 32; ++kt)
-          acc = mma(frag_row_scaled(sm.qk, LDK, mt * 16 + ln, 32 * kt, g, sm.hx + mt * DK),
-                    sm.s0f[cg][kt][lane], acc);
+        for (int kt = 0; kt < DK / 32; ++kt) {
+          Frag<ST> fa;
+          if constexpr (PRE)
+            fa = frag_row(sm.kb, LDK, mt * 16 + ln, 32 * kt, g);
+          else
+            fa = frag_row_scaled(sm.qk, LDK, mt * 16 + ln, 32 * kt, g, sm.hx + mt * DK);
+          acc = mmk<OP>(fa, sm.s0f[cg][kt][lane], acc);
+        }
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
           if (32 * kt < 16 * (mt + 1))
-            acc = mma(frag_f32<ST>(sm.lt, LTD, mt * 16 + ln, 32 * kt, g), sm.rf[cg][kt][lane], acc);
+            acc = mmk<OP>(frag_f32<ST>(sm.lt, LTD, mt * 16 + ln, 32 * kt, g),
+                          sm.rf[cg][kt][lane], acc);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           bstore(rso, static_cast<int>(((mt * 16 + 4 * g + i) * v_stride + ocol) * sizeof(TIN)),
@@ -543,9 +611,14 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
       acc[2] *= lx.z;
       acc[3] *= lx.w;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-        acc = mma(frag_kdec<ST, DK>(sm.kk, LDK, r + ln, 32 * kt, g, sm.gl), sm.rf[cg][kt][lane],
-                  acc);
+      for (int kt = 0; kt < 2; ++kt) {
+        Frag<ST> fa;
+        if constexpr (PRE)
+          fa = frag_row(sm.kdt, LDV, r + ln, 32 * kt, g);
+        else
+          fa = frag_kdec<ST, DK>(sm.kk, LDK, r + ln, 32 * kt, g, sm.gl);
+        acc = mmk<OP>(fa, sm.rf[cg][kt][lane], acc);
+      }
       if constexpr (OP) acc *= scale;
       st[mt] = acc;
     }
@@ -570,7 +643,7 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
 
 template <typename TIN, typename ST, bool OP, int DK, int DV>
 hipError_t launch_kda_t(const KdaArgs& a, int n_items, hipStream_t s) {
-  constexpr int bytes = static_cast<int>(sizeof(KdaLds<ST, DK>));
+  constexpr int bytes = static_cast<int>(sizeof(KdaLds<ST, DK, OP>));
   static const hipError_t attr = hipFuncSetAttribute(
       reinterpret_cast<const void*>(&kda_scan_kernel<TIN, ST, OP, DK, DV>),
       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
