@@ -255,13 +255,9 @@ __global__ __launch_bounds__(kFT) void family_scan_kernel(FamArgs args) {
     }
     float dec_l = 0.f, b_l = 0.f;  // scalar: exp(b_last - b) and b of token `lane`
     if constexpr (!DIAG) {
-      float b = rg[0];
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const float u = __shfl_up(b, off, 64);
-        if (lane >= off) b += u;
-      }
-      const float b_last = __shfl(b, 63, 64);
+      const float b = wave_inclusive_sum(rg[0]);
+      const float b_last = __builtin_bit_cast(
+          float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, b), 63));
       b_l = b;
       dec_l = __expf(b_last - b);
       ld_acc += b_last;
@@ -692,13 +688,9 @@ __global__ __launch_bounds__(512) void family_pipe_kernel(FamArgs args) {
           *reinterpret_cast<uint32_t*>(sm.vt[buf] + (cvv * 8 + e) * LDT +
                                        ((2 * rpv) ^ (SWV * (cvv >> 1)))) =
               pair_raw(rv[0], rv[1], e);
-        float b = rg;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-          const float u = __shfl_up(b, off, 64);
-          if (lane >= off) b += u;
-        }
-        const float b_last = __shfl(b, 63, 64);
+        const float b = wave_inclusive_sum(rg);
+        const float b_last = __builtin_bit_cast(
+            float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, b), 63));
         const float dec = __expf(b_last - b);
         if (pw == 0) {
           sm.bc[buf][lane] = b;

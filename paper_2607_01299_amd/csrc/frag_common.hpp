@@ -157,5 +157,25 @@ __device__ __forceinline__ void bstore(__amdgpu_buffer_rsrc_t r, int off, float 
   __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, off, 0, 0);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave with DPP moves (no LDS
+// round trip): shifts by 1, 2, 4, 8 inside each row of 16 lanes, then the last
+// lane of row 0 is added to row 1 (and of row 2 to row 3), then the last lane
+// of row 1 to rows 2 and 3.  Lanes whose DPP source falls outside the row, or
+// whose row is masked off, add zero.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_add(float x) {
+  const int v = __builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, ROW_MASK, 0xf, true);
+  return x + __int_as_float(v);
+}
+__device__ __forceinline__ float wave_inclusive_sum(float x) {
+  x = dpp_add<0x111, 0xf>(x);  // row_shr:1
+  x = dpp_add<0x112, 0xf>(x);  // row_shr:2
+  x = dpp_add<0x114, 0xf>(x);  // row_shr:4
+  x = dpp_add<0x118, 0xf>(x);  // row_shr:8
+  x = dpp_add<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+  x = dpp_add<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+  return x;
+}
+
 }  // namespace
 }  // namespace hypic
