@@ -76,6 +76,17 @@ struct KdaLds {
   alignas(16) ST vt[OP ? 1 : KNC * LDV];
   alignas(16) ST kb[PRE ? KC * LDK : 1];
   alignas(16) ST kdt[PRE ? DK * LDV : 1];
+  // the off-diagonal 16 x 16 blocks of the inverse, kept apart from L (TB:
+  // bf16 state columns and operator columns; float32 state columns write them
+  // into lt, which takes a second barrier per block row)
+  static constexpr bool TB = PRE || OP;
+  static constexpr int TBS = 20;  // row stride of a block
+  alignas(16) float tb[TB ? 6 * 16 * TBS : 4];
+  // bf16 state columns (NS): N republished into a second fragment buffer and
+  // A formed into its own array, in one stage
+  static constexpr bool NS = PRE;
+  alignas(16) Frag<ST> rf2[NS ? NCG * 2 * 64 : 1];
+  alignas(16) ST la[NS ? KC * LDV : 1];
   // S0 as B fragments: column group, 32-row block, lane
   alignas(16) Frag<ST> s0f[NCG][DK / 32][64];
   alignas(16) Frag<ST> rf[NCG][2][64];         // diag(beta) R, then N, as B fragments over tokens
@@ -139,17 +150,39 @@ __device__ __forceinline__ Frag<ST> frag_kdec(const ST* kk, int ldk, int c, int 
   return f;
 }
 
-// acc += A[ra.., ca..] B[rb.., cb..] over 16 k (float32 matrix cores), both
-// row-major float32 16 x 16 blocks
-__device__ __forceinline__ f32x4 mm16(const float* M, int ld, int ra, int ca, int rb, int cb,
-                                      f32x4 acc, int g, int ln) {
-  const float4 a = *reinterpret_cast<const float4*>(M + (ra + ln) * ld + ca + 4 * g);
+// acc += A B over 16 k (float32 matrix cores): 16 x 16 row-major float32
+// blocks at A (row stride lda) and B (row stride ldb)
+__device__ __forceinline__ f32x4 mm16p(const float* A, int lda, const float* B, int ldb,
+                                       f32x4 acc, int g, int ln) {
+  const float4 a = *reinterpret_cast<const float4*>(A + ln * lda + 4 * g);
   const float av[4] = {a.x, a.y, a.z, a.w};
 #pragma unroll
   for (int j = 0; j < 4; ++j)
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j], M[(rb + 4 * g + j) * ld + cb + ln], acc, 0,
-                                               0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j], B[(4 * g + j) * ldb + ln], acc, 0, 0, 0);
   return acc;
+}
+
+// A-operand fragment of the inverse T (row tile mt, k tokens 32 kt .. +31)
+// when its off-diagonal blocks are kept apart: the diagonal block from lt, the
+// blocks left of it from tb, zero right of it
+template <typename ST, int TBS>
+__device__ __forceinline__ Frag<ST> frag_T(const float* lt, const float* tb, int mt, int kt,
+                                           int g, int ln) {
+  Frag<ST> f;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int tk = 2 * kt + h;
+    float4 v = {0.f, 0.f, 0.f, 0.f};
+    if (tk == mt)
+      v = *reinterpret_cast<const float4*>(lt + (16 * mt + ln) * LTD + 16 * tk + 4 * g);
+    else if (tk < mt)
+      v = *reinterpret_cast<const float4*>(tb + pair_ix(mt, tk) * 16 * TBS + ln * TBS + 4 * g);
+    f.set(4 * h, v.x);
+    f.set(4 * h + 1, v.y);
+    f.set(4 * h + 2, v.z);
+    f.set(4 * h + 3, v.w);
+  }
+  return f;
 }
 
 __device__ __forceinline__ int kda_segment_of_rank(const KdaArgs& a, int rank) {
@@ -171,7 +204,8 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
   static_assert(NQ >= 1 && NMH % 2 == 0 && NRG == 2, "tile split");
   static_assert(TPT == 16 || TPT == 8, "gate split");
   static_assert(sizeof(L) <= 160 * 1024, "LDS budget");
-  constexpr bool PRE = L::PRE;
+  constexpr bool PRE = L::PRE, TB = L::TB, NS = L::NS;
+  constexpr int TBS = L::TBS;
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
   L& sm = *reinterpret_cast<L*>(smem_raw);
@@ -242,6 +276,7 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
   {
     const int t = tid >> 8, e = tid & 255;
     sm.lt[(32 * t + (e >> 4)) * LTD + 32 * t + 16 + (e & 15)] = 0.f;
+    if constexpr (NS) stv(sm.la + (32 * t + (e >> 4)) * LDV + 32 * t + 16 + (e & 15), 0.f);
   }
 
   // ---- register prefetch of one chunk ----
@@ -499,8 +534,16 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
       if (wave < bi) {
         const int bj = wave;
         f32x4 m = zero4();
-        for (int bk = bj; bk < bi; ++bk)
-          m = mm16(sm.lt, LTD, 16 * bi, 16 * bk, 16 * bk, 16 * bj, m, g, ln);
+        for (int bk = bj; bk < bi; ++bk) {
+          // T_kj: X_j on the diagonal of lt, else the block row bk written before
+          const float* bp = sm.lt + (16 * bk) * LTD + 16 * bj;
+          int ldb = LTD;
+          if (TB && bk > bj) {
+            bp = sm.tb + pair_ix(bk, bj) * 16 * TBS;
+            ldb = TBS;
+          }
+          m = mm16p(sm.lt + (16 * bi) * LTD + 16 * bk, LTD, bp, ldb, m, g, ln);
+        }
         const float4 a =
             *reinterpret_cast<const float4*>(sm.lt + (16 * bi + ln) * LTD + 16 * bi + 4 * g);
         const float av[4] = {a.x, a.y, a.z, a.w};
@@ -508,12 +551,22 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
         for (int j = 0; j < 4; ++j)
           tij = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j], m[j], tij, 0, 0, 0);
       }
-      lds_barrier();
-      if (wave < bi) {
+      if constexpr (TB) {
+        if (wave < bi) {
+          float* tp = sm.tb + pair_ix(bi, wave) * 16 * TBS;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) sm.lt[(16 * bi + 4 * g + i) * LTD + 16 * wave + ln] = -tij[i];
+          for (int i = 0; i < 4; ++i) tp[(4 * g + i) * TBS + ln] = -tij[i];
+        }
+        lds_barrier();
+      } else {
+        lds_barrier();  // L_ij is read by this block row until here
+        if (wave < bi) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            sm.lt[(16 * bi + 4 * g + i) * LTD + 16 * wave + ln] = -tij[i];
+        }
+        lds_barrier();
       }
-      lds_barrier();
     }
 
     // ---- 6: N = T diag(beta) R (two token tiles of this wave's columns) ----
@@ -524,12 +577,17 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
       f32x4 acc = zero4();
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
-        if (32 * kt < 16 * (mt + 1))
-          acc = mmk<OP>(frag_f32<ST>(sm.lt, LTD, mt * 16 + ln, 32 * kt, g), sm.rf[cg][kt][lane],
-                        acc);
+        if (32 * kt < 16 * (mt + 1)) {
+          Frag<ST> ft;
+          if constexpr (TB)
+            ft = frag_T<ST, TBS>(sm.lt, sm.tb, mt, kt, g, ln);
+          else
+            ft = frag_f32<ST>(sm.lt, LTD, mt * 16 + ln, 32 * kt, g);
+          acc = mmk<OP>(ft, sm.rf[cg][kt][lane], acc);
+        }
       nt[mh] = acc;
     }
-    lds_barrier();
+    if constexpr (!NS) lds_barrier();  // every wave is done reading diag(beta) R
     {
       Frag<ST> f;
 #pragma unroll
@@ -537,9 +595,13 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
         f.set(i, nt[0][i]);
         f.set(4 + i, nt[1][i]);
       }
-      sm.rf[cg][rgrp][lane] = f;
+      if constexpr (NS)
+        sm.rf2[(cg * 2 + rgrp) * 64 + lane] = f;
+      else
+        sm.rf[cg][rgrp][lane] = f;
     }
-    // ---- 7: A (lower tiles, inclusive) from the query-side Q ----
+    // ---- 7: A (lower tiles, inclusive) from the query-side Q (into la with
+    // NS, else into lt, whose inverse is no longer read) ----
     if constexpr (!OP) {
       for (int tile = wave; tile < 10; tile += 8) {
         const int tq = (tile < 1) ? 0 : ((tile < 3) ? 1 : ((tile < 6) ? 2 : 3));
@@ -558,7 +620,11 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int t = tq * 16 + 4 * g + i;
-          sm.lt[t * LTD + key] = (key <= t) ? acc[i] : 0.f;
+          const float x = (key <= t) ? acc[i] : 0.f;
+          if constexpr (NS)
+            stv(sm.la + t * LDV + key, x);
+          else
+            sm.lt[t * LTD + key] = x;
         }
       }
     }
@@ -586,9 +652,14 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
         }
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
-          if (32 * kt < 16 * (mt + 1))
-            acc = mmk<OP>(frag_f32<ST>(sm.lt, LTD, mt * 16 + ln, 32 * kt, g),
-                          sm.rf[cg][kt][lane], acc);
+          if (32 * kt < 16 * (mt + 1)) {
+            if constexpr (NS)
+              acc = mmk<OP>(frag_row(sm.la, LDV, mt * 16 + ln, 32 * kt, g),
+                            sm.rf2[(cg * 2 + kt) * 64 + lane], acc);
+            else
+              acc = mmk<OP>(frag_f32<ST>(sm.lt, LTD, mt * 16 + ln, 32 * kt, g),
+                            sm.rf[cg][kt][lane], acc);
+          }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           bstore(rso, static_cast<int>(((mt * 16 + 4 * g + i) * v_stride + ocol) * sizeof(TIN)),
@@ -617,7 +688,10 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
           fa = frag_row(sm.kdt, LDV, r + ln, 32 * kt, g);
         else
           fa = frag_kdec<ST, DK>(sm.kk, LDK, r + ln, 32 * kt, g, sm.gl);
-        acc = mmk<OP>(fa, sm.rf[cg][kt][lane], acc);
+        if constexpr (NS)
+          acc = mmk<OP>(fa, sm.rf2[(cg * 2 + kt) * 64 + lane], acc);
+        else
+          acc = mmk<OP>(fa, sm.rf[cg][kt][lane], acc);
       }
       if constexpr (OP) acc *= scale;
       st[mt] = acc;
