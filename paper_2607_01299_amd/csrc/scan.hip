@@ -572,14 +572,16 @@ hipError_t launch_scan(const ScanArgs& a, int bf16, int d_k, int d_v, int chunk,
       fast ? scan_bf16_items_per_head(d_k, d_v, a.n_roles == 2) : a.n_roles;
   if (fast) {
     // Seams of at most one chunk run back to back through one workgroup's
-    // pipeline, up to 16 entries of one head per workgroup, while that still
-    // leaves two workgroups per compute unit.
+    // pipeline, up to 16 entries of one head per workgroup: as many as make
+    // the launch a single round of workgroups over the 256 compute units, so
+    // that a workgroup of g entries takes g + 2 iterations (the pipeline's
+    // fill) once rather than two rounds of g / 2 + 2.
     ScanArgs b = a;
     b.n_entries = n_chains;
     b.group_e = 1;
     if (a.mode == 1 && a.w <= 64) {
       const int64_t pairs = static_cast<int64_t>(n_chains) * a.h_v;
-      const int64_t ge = pairs / 512;
+      const int64_t ge = (pairs + 255) / 256;
       b.group_e = static_cast<int>((ge < 1) ? 1 : ((ge > 16) ? 16 : ge));
     }
     const int64_t groups = (n_chains + b.group_e - 1) / b.group_e;
