@@ -305,6 +305,13 @@ def bench_compose_burst(torch, steps, warmup):
     adv = SeamAdvanceBurst(P, g, S, p["seg_ids"], p["req_offsets"], toks, p["tok_start_pool"],
                            p["seam_len_pool"], p["w"])
     adv.run()
+    adv1_ms = _events_ms(torch, adv.stream, adv.run, max(steps // 2, 2))
+    del adv
+    # the same burst over two lanes (half the requests each, on two streams), so
+    # that one lane's seam steps overlap the other's compositions
+    adv = SeamAdvanceBurst(P, g, S, p["seg_ids"], p["req_offsets"], toks, p["tok_start_pool"],
+                           p["seam_len_pool"], p["w"], lanes=2)
+    adv.run()
     adv_ms = _events_ms(torch, adv.stream, adv.run, max(steps // 2, 2))
     del adv
     return {
@@ -318,6 +325,7 @@ def bench_compose_burst(torch, steps, warmup):
                      "counter": measured_mfma("compose", W.CONFIG_NAMES[5]),
                      "kernel": "compose_kernel", "bytes_per_launch": byts},
         "seam_advance": {"ms_per_burst": adv_ms, "compositions_per_s": nnz / (adv_ms * 1e-3),
+                         "lanes": 2, "ms_per_burst_one_call": adv1_ms,
                          "note": "seams run from the running state, then tail tuples (Sec. 4.3)"},
         "config": {"workload": W.CONFIG_NAMES[5], "requests": burst.n_req,
                    "compositions": nnz, "pool": int(p["n_pool"]), "h_v": h_v,

@@ -190,14 +190,20 @@ class ComposeBurst:
 
 class SeamAdvanceBurst:
     """Requests composed from a pool of tail tuples with each entry's seam run
-    from the running state first (hypic_compose_with_seams), pre-bound."""
+    from the running state first (hypic_compose_with_seams), pre-bound.
+
+    lanes > 1 splits the requests, dealt longest first, over that many calls on
+    streams of their own (default priority), so that one lane's seam steps
+    (matrix-core work) overlap another's compositions (HBM streams).  Each lane
+    then holds its requests' S_out and o_seam in its own request order;
+    outputs() assembles them in the caller's order.
+    """
 
     def __init__(self, P_hat, log_decay, S_seg, seg_ids, req_offsets, tokens, seam_start,
-                 seam_len, w, *, S_prefix=None):
+                 seam_len, w, *, S_prefix=None, lanes=1):
         self.lib = _lib.load()
         dev = S_seg.device
         self.stream = torch.cuda.current_stream(dev)
-        sp = ctypes.c_void_p(self.stream.cuda_stream)
         n_pool, h_v, d_k, d_v = S_seg.shape
         q, k, v, beta, log_alpha = tokens
         self.tokens = tokens
@@ -206,28 +212,88 @@ class SeamAdvanceBurst:
                          chunk=64)
         self.ss_h, self.ss_d = _i32_pair(seam_start, dev)
         self.sl_h, self.sl_d = _i32_pair(seam_len, dev)
-        self.ids_h, self.ids_d = _i32_pair(seg_ids, dev)
-        self.off_h, self.off_d = _i32_pair(req_offsets, dev)
-        n_req = len(self.off_h) - 1
-        nnz = int(self.off_h[-1])
-        max_n = int(np.max(np.diff(self.off_h))) if n_req > 0 else 0
+        ids = np.ascontiguousarray(np.asarray(seg_ids, dtype=np.int32))
+        offs = np.ascontiguousarray(np.asarray(req_offsets, dtype=np.int32))
+        n_req = len(offs) - 1
+        nnz = int(offs[-1]) if n_req >= 0 else 0
         self.n_req, self.nnz, self.h_v, self.d_k, self.d_v = n_req, nnz, h_v, d_k, d_v
+        self.w = int(w)
         self.S_prefix = S_prefix
-        self.S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=torch.float32, device=dev)
-        self.o_seam = torch.empty((nnz, w, h_v, d_v), dtype=q.dtype, device=dev)
+        lens = np.diff(offs)
+        order = np.argsort(-lens, kind="stable")
+        lanes = max(1, min(int(lanes), max(n_req, 1)))
+        self.groups = ([np.arange(n_req)] if lanes == 1 else
+                       [np.sort(order[i::lanes]) for i in range(lanes)])
+        self.streams = ([self.stream] if lanes == 1 else
+                        [torch.cuda.Stream(device=dev) for _ in range(lanes)])
+        self.lanes = []
+        for grp, st in zip(self.groups, self.streams):
+            g_ids = (ids if lanes == 1 else
+                     np.concatenate([ids[offs[r]:offs[r + 1]] for r in grp] or
+                                    [np.zeros(0, np.int32)]).astype(np.int32))
+            g_offs = (offs if lanes == 1 else
+                      np.concatenate([[0], np.cumsum(lens[grp])]).astype(np.int32))
+            g_pre = (S_prefix if (lanes == 1 or S_prefix is None) else
+                     S_prefix[torch.as_tensor(grp, device=dev)].contiguous())
+            self.lanes.append(self._bind(P_hat, log_decay, S_seg, n_pool, g_ids, g_offs, g_pre,
+                                         st, dev))
+        # rows of the caller's CSR order held by each lane, for outputs()
+        self.rows = [np.concatenate([np.arange(offs[r], offs[r + 1]) for r in grp] or
+                                    [np.zeros(0, np.int64)]) for grp in self.groups]
+        self.S_out = self.lanes[0]["S_out"] if lanes == 1 else None
+        self.o_seam = self.lanes[0]["o_seam"] if lanes == 1 else None
+
+    def _bind(self, P_hat, log_decay, S_seg, n_pool, ids, offs, S_prefix, stream, dev):
+        q, k, v, beta, log_alpha = self.tokens
+        ids_h, ids_d = _i32_pair(ids, dev)
+        off_h, off_d = _i32_pair(offs, dev)
+        n_req = len(off_h) - 1
+        nnz = int(off_h[-1])
+        max_n = int(np.max(np.diff(off_h))) if n_req > 0 else 0
+        S_out = torch.empty((n_req, self.h_v, self.d_k, self.d_v), dtype=torch.float32,
+                            device=dev)
+        o_seam = torch.empty((nnz, self.w, self.h_v, self.d_v), dtype=q.dtype, device=dev)
         need = self.lib.hypic_seam_compose_workspace_bytes(ctypes.byref(self.dims), n_req, max_n)
-        self.ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-        self._args = (
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        args = (
             ctypes.byref(self.dims), _p(P_hat), _p(log_decay), _p(S_seg), n_pool, _p(q), _p(k),
             _p(v), _p(beta), _p(log_alpha), q.shape[0], _p(self.ss_d),
             self.ss_h.ctypes.data_as(ctypes.c_void_p), _p(self.sl_d),
-            self.sl_h.ctypes.data_as(ctypes.c_void_p), int(w), _p(self.ids_d),
-            self.ids_h.ctypes.data_as(ctypes.c_void_p), _p(self.off_d),
-            self.off_h.ctypes.data_as(ctypes.c_void_p), n_req, _p(S_prefix), _p(self.S_out),
-            _p(self.o_seam), _p(self.ws), need, sp)
+            self.sl_h.ctypes.data_as(ctypes.c_void_p), self.w, _p(ids_d),
+            ids_h.ctypes.data_as(ctypes.c_void_p), _p(off_d),
+            off_h.ctypes.data_as(ctypes.c_void_p), n_req, _p(S_prefix), _p(S_out),
+            _p(o_seam), _p(ws), need, ctypes.c_void_p(stream.cuda_stream))
+        return {"S_out": S_out, "o_seam": o_seam, "ws": ws, "keep": (ids_h, ids_d, off_h, off_d,
+                                                                   S_prefix), "args": args}
 
     def run(self):
-        _lib.check(self.lib.hypic_compose_with_seams(*self._args))
+        if len(self.lanes) == 1:
+            _lib.check(self.lib.hypic_compose_with_seams(*self.lanes[0]["args"]))
+            return
+        start = torch.cuda.Event()
+        start.record(self.stream)
+        for lane, st in zip(self.lanes, self.streams):
+            st.wait_event(start)
+            _lib.check(self.lib.hypic_compose_with_seams(*lane["args"]))
+        for st in self.streams:
+            done = torch.cuda.Event()
+            done.record(st)
+            self.stream.wait_event(done)
+
+    def outputs(self):
+        """(S_out, o_seam) in the caller's request and CSR order (copies when
+        lanes > 1), on the burst's stream."""
+        if len(self.lanes) == 1:
+            return self.S_out, self.o_seam
+        dev = self.lanes[0]["S_out"].device
+        S_out = torch.empty((self.n_req, self.h_v, self.d_k, self.d_v), dtype=torch.float32,
+                            device=dev)
+        o_seam = torch.empty((self.nnz, self.w, self.h_v, self.d_v),
+                             dtype=self.lanes[0]["o_seam"].dtype, device=dev)
+        for lane, grp, rows in zip(self.lanes, self.groups, self.rows):
+            S_out[torch.as_tensor(grp, device=dev)] = lane["S_out"]
+            o_seam[torch.as_tensor(rows, device=dev)] = lane["o_seam"]
+        return S_out, o_seam
 
 
 class FamilyPipeline:

@@ -120,3 +120,34 @@ def test_compose_with_seams_serve_burst(hy):
             worst = max(worst, rel(_np(burst.o_seam[j, :, h]), R_o[j, :, h]))
     print("max rel err %.2e" % worst, flush=True)
     assert worst <= TOL[W.BF16]
+
+
+def test_compose_with_seams_two_lanes_equal_one_call(hy):
+    """The serve burst split over two calls on two streams (requests dealt
+    longest first) gives exactly the single call's S_out and o_seam, behind a
+    prefix state, once the lanes' outputs are put back in request order."""
+    _say("compose with seams: serve burst, two lanes against one call")
+    from paper_2607_01299_amd.pipeline import SeamAdvanceBurst
+    p = W.pool_workload()
+    t = p["tokens"]
+    toks = (torch.from_numpy(t["q"]).cuda().to(torch.bfloat16).contiguous(),
+            torch.from_numpy(t["k"]).cuda().to(torch.bfloat16).contiguous(),
+            torch.from_numpy(t["v"]).cuda().to(torch.bfloat16).contiguous(),
+            torch.from_numpy(t["beta"]).cuda(), torch.from_numpy(t["log_alpha"]).cuda())
+    seam_start = (np.arange(p["n_pool"]) * 64).astype(np.int32)
+    seam_len = np.full(p["n_pool"], 64, dtype=np.int32)
+    pool = (torch.from_numpy(p["P_hat"]).cuda(), torch.from_numpy(p["log_decay"]).cuda(),
+            torch.from_numpy(p["S_seg"]).cuda())
+    n_req = len(p["req_offsets"]) - 1
+    prefix = torch.randn((n_req, 16, 128, 128), generator=torch.Generator().manual_seed(9)).cuda()
+    one = SeamAdvanceBurst(*pool, p["seg_ids"], p["req_offsets"], toks, seam_start, seam_len, 64,
+                           S_prefix=prefix)
+    two = SeamAdvanceBurst(*pool, p["seg_ids"], p["req_offsets"], toks, seam_start, seam_len, 64,
+                           S_prefix=prefix, lanes=2)
+    one.run()
+    two.run()
+    two.run()  # a second run on the same bindings
+    S2, o2 = two.outputs()
+    torch.cuda.synchronize()
+    assert torch.equal(one.S_out, S2)
+    assert torch.equal(one.o_seam, o2)
