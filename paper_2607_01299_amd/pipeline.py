@@ -134,8 +134,34 @@ class SegmentPipeline:
         self.graph.replay()
 
 
+def _deal_requests(seg_ids, req_offsets, lanes):
+    """Deal CSR requests over `lanes` groups, longest first (round robin over
+    the requests sorted by entry count, ties by index).  Returns per group:
+    (request indices in ascending order, its CSR seg_ids, its CSR offsets, the
+    caller's CSR rows it holds)."""
+    ids = np.ascontiguousarray(np.asarray(seg_ids, dtype=np.int32))
+    offs = np.ascontiguousarray(np.asarray(req_offsets, dtype=np.int32))
+    lens = np.diff(offs)
+    n_req = len(lens)
+    lanes = max(1, min(int(lanes), max(n_req, 1)))
+    if lanes == 1:
+        return [(np.arange(n_req), ids, offs, np.arange(int(offs[-1]) if n_req else 0))]
+    order = np.argsort(-lens, kind="stable")
+    out = []
+    for i in range(lanes):
+        grp = np.sort(order[i::lanes])
+        rows = np.concatenate([np.arange(offs[r], offs[r + 1]) for r in grp] or
+                              [np.zeros(0, np.int64)]).astype(np.int64)
+        out.append((grp, ids[rows].astype(np.int32),
+                    np.concatenate([[0], np.cumsum(lens[grp])]).astype(np.int32), rows))
+    return out
+
+
 class ComposeBurst:
-    """Requests composed from a pool of cached tuples, then seam rescans."""
+    """Requests composed from a pool of cached tuples, then seam rescans.
+    (Dealing these requests over two streams, as SeamAdvanceBurst can, gains
+    about 1 %: both launches fill the whole GPU, so they overlap only at their
+    edges.)"""
 
     def __init__(self, P_hat, log_decay, S_seg, seg_ids, req_offsets, tokens, tok_start,
                  tok_len, w, *, chunk=64, precision="split", want_post=False):
@@ -212,34 +238,24 @@ class SeamAdvanceBurst:
                          chunk=64)
         self.ss_h, self.ss_d = _i32_pair(seam_start, dev)
         self.sl_h, self.sl_d = _i32_pair(seam_len, dev)
-        ids = np.ascontiguousarray(np.asarray(seg_ids, dtype=np.int32))
-        offs = np.ascontiguousarray(np.asarray(req_offsets, dtype=np.int32))
+        offs = np.asarray(req_offsets, dtype=np.int32)
         n_req = len(offs) - 1
         nnz = int(offs[-1]) if n_req >= 0 else 0
         self.n_req, self.nnz, self.h_v, self.d_k, self.d_v = n_req, nnz, h_v, d_k, d_v
         self.w = int(w)
         self.S_prefix = S_prefix
-        lens = np.diff(offs)
-        order = np.argsort(-lens, kind="stable")
-        lanes = max(1, min(int(lanes), max(n_req, 1)))
-        self.groups = ([np.arange(n_req)] if lanes == 1 else
-                       [np.sort(order[i::lanes]) for i in range(lanes)])
+        self.deal = _deal_requests(seg_ids, req_offsets, lanes)
+        lanes = len(self.deal)
+        self.groups = [d[0] for d in self.deal]
+        self.rows = [d[3] for d in self.deal]
         self.streams = ([self.stream] if lanes == 1 else
                         [torch.cuda.Stream(device=dev) for _ in range(lanes)])
         self.lanes = []
-        for grp, st in zip(self.groups, self.streams):
-            g_ids = (ids if lanes == 1 else
-                     np.concatenate([ids[offs[r]:offs[r + 1]] for r in grp] or
-                                    [np.zeros(0, np.int32)]).astype(np.int32))
-            g_offs = (offs if lanes == 1 else
-                      np.concatenate([[0], np.cumsum(lens[grp])]).astype(np.int32))
+        for (grp, g_ids, g_offs, _), st in zip(self.deal, self.streams):
             g_pre = (S_prefix if (lanes == 1 or S_prefix is None) else
                      S_prefix[torch.as_tensor(grp, device=dev)].contiguous())
             self.lanes.append(self._bind(P_hat, log_decay, S_seg, n_pool, g_ids, g_offs, g_pre,
                                          st, dev))
-        # rows of the caller's CSR order held by each lane, for outputs()
-        self.rows = [np.concatenate([np.arange(offs[r], offs[r + 1]) for r in grp] or
-                                    [np.zeros(0, np.int64)]) for grp in self.groups]
         self.S_out = self.lanes[0]["S_out"] if lanes == 1 else None
         self.o_seam = self.lanes[0]["o_seam"] if lanes == 1 else None
 

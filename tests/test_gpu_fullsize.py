@@ -164,3 +164,4 @@ def test_cfg5_full_burst(pipe_mod):
         print("  request %d head %d (%d segments): %.2e" % (r, h, len(js), e), flush=True)
         worst = max(worst, e)
     assert worst <= TOL
+
