@@ -1,0 +1,129 @@
+"""Parity at unequal key and value widths (d_k, d_v) = (64, 128) and (128, 64),
+which every build path supports: the GDN build (bf16 and float32 inputs), the
+scalar and diagonal families and the KDA row, each against its float64 oracle
+on ragged segments with grouped heads.  Bar: relative Frobenius error per
+(segment, head) tensor, 1e-4 for float32 inputs, 1e-2 for bf16.
+
+Outputs of segments shorter than 16 tokens are judged inside the head's whole
+output instead: a one-token segment's output is the single row
+beta (q . k) v, and where q . k nearly cancels (0.009 for two unit vectors in
+this draw), rounding the gate-scaled q and k to bf16, as the per-channel-gate
+rows must, alone moves it by 2e-2 relative.
+"""
+
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import families as F
+from oracle import gdn as G
+from oracle import kda as K
+from paper_2607_01299_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+TOL = {W.F32: 1e-4, W.BF16: 1e-2}
+DIMS = [(64, 128), (128, 64)]
+LENGTHS = [70, 130, 1]
+
+
+def _say(msg):
+    print("[case] " + msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def hy():
+    if not torch.cuda.is_available():
+        pytest.fail("no GPU visible")
+    import paper_2607_01299_amd as hy
+    from paper_2607_01299_amd import _lib
+    _lib.load()
+    return hy
+
+
+def _np(t):
+    return t.detach().float().cpu().numpy().astype(np.float64)
+
+
+def rel(x, ref):
+    nr = np.linalg.norm(ref)
+    if nr == 0.0:
+        return float(np.linalg.norm(x))
+    return float(np.linalg.norm(x - ref) / nr)
+
+
+def _tokens(d_k, d_v, dt, seed):
+    rng = np.random.default_rng(seed)
+    T = sum(LENGTHS)
+    w = W.draw_tokens(rng, T, 2, 4, d_k, d_v, dt)
+    w["cu"] = W.cu_from_lengths(LENGTHS)
+    tdt = torch.bfloat16 if dt == W.BF16 else torch.float32
+    dev = {key: torch.from_numpy(w[key]).cuda().to(tdt).contiguous() for key in ("q", "k", "v")}
+    dev["beta"] = torch.from_numpy(w["beta"]).cuda().contiguous()
+    dev["log_alpha"] = torch.from_numpy(w["log_alpha"]).cuda().contiguous()
+    return w, dev
+
+
+def _compare(res, ref, cu, keys, tol, tag):
+    worst = {key: 0.0 for key in keys}
+    if "o" in keys:
+        got = _np(res["o"])
+        for h in range(4):  # every row, short segments included
+            worst["o"] = max(worst["o"], rel(got[:, h], ref["o"][:, h]))
+    for s in range(len(cu) - 1):
+        lo, hi = int(cu[s]), int(cu[s + 1])
+        for h in range(4):
+            for key in keys:
+                got = _np(res[key])
+                if key == "o":
+                    e = rel(got[lo:hi, h], ref["o"][lo:hi, h]) if hi - lo >= 16 else 0.0
+                elif key == "log_decay":
+                    e = float(np.max(np.abs(got[s, h] - ref[key][s, h])))
+                else:
+                    e = rel(got[s, h], ref[key][s, h])
+                worst[key] = max(worst[key], e)
+    print("%s max err: %s" % (tag, {k: "%.2e" % v for k, v in worst.items()}), flush=True)
+    for key, val in worst.items():
+        assert val <= tol, (tag, key, val)
+
+
+@pytest.mark.parametrize("d_k,d_v", DIMS)
+@pytest.mark.parametrize("dt", [W.BF16, W.F32])
+def test_gdn_build_mixed_dims(hy, d_k, d_v, dt):
+    _say("gdn build %s d_k=%d d_v=%d lengths %s" % (dt, d_k, d_v, LENGTHS))
+    w, dev = _tokens(d_k, d_v, dt, 41)
+    res = hy.build_segment(dev["q"], dev["k"], dev["v"], dev["beta"], dev["log_alpha"], w["cu"])
+    torch.cuda.synchronize()
+    ref = G.build_segments(w["q"], w["k"], w["v"], w["beta"], w["log_alpha"], w["cu"])
+    _compare(res, ref, w["cu"], ("o", "S_seg", "P_hat", "log_decay"), TOL[dt],
+             "gdn %s %dx%d" % (dt, d_k, d_v))
+
+
+@pytest.mark.parametrize("d_k,d_v", DIMS)
+@pytest.mark.parametrize("family", ["scalar", "diagonal"])
+def test_family_build_mixed_dims(hy, d_k, d_v, family):
+    _say("family %s build bf16 d_k=%d d_v=%d lengths %s" % (family, d_k, d_v, LENGTHS))
+    w, dev = _tokens(d_k, d_v, W.BF16, 42)
+    gate = W.family_gate(family, int(w["cu"][-1]), 4, d_k, 43)
+    res = hy.family_build(family, dev["q"], dev["k"], dev["v"], torch.from_numpy(gate).cuda(),
+                          w["cu"])
+    torch.cuda.synchronize()
+    ref = F.family_build_segments(family, w["q"], w["k"], w["v"], gate, w["cu"])
+    _compare(res, ref, w["cu"], ("o", "S_seg", "log_decay"), TOL[W.BF16],
+             "%s %dx%d" % (family, d_k, d_v))
+
+
+@pytest.mark.parametrize("d_k,d_v", DIMS)
+def test_kda_build_mixed_dims(hy, d_k, d_v):
+    _say("kda build bf16 d_k=%d d_v=%d lengths %s" % (d_k, d_v, LENGTHS))
+    w, dev = _tokens(d_k, d_v, W.BF16, 44)
+    gate = W.family_gate("diagonal", int(w["cu"][-1]), 4, d_k, 45)
+    res = hy.kda_build(dev["q"], dev["k"], dev["v"], dev["beta"], torch.from_numpy(gate).cuda(),
+                       w["cu"])
+    torch.cuda.synchronize()
+    ref = K.kda_build_segments(w["q"], w["k"], w["v"], w["beta"], gate, w["cu"])
+    _compare(res, ref, w["cu"], ("o", "S_seg", "P_hat", "log_decay"), TOL[W.BF16],
+             "kda %dx%d" % (d_k, d_v))
