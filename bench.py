@@ -509,8 +509,10 @@ def bench_adjacent(torch, steps):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # 200 timed steps after 50 warm-up steps: about 50 ms of GPU work, enough
+    # for the clocks to settle (5 + 20 steps read the build about 15 % slower)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--config", type=int, default=2, choices=[2, 3, 4])
     ap.add_argument("--seam-w", type=int, default=8)
     ap.add_argument("--no-cpu-baseline", action="store_true")

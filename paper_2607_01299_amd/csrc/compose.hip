@@ -20,7 +20,7 @@
 //     float32 matrix cores, then S <- e^g (P_hat S) + S_seg in float32.
 // The tuple of a later step is loaded into registers while a step computes
 // (two steps ahead on split grids, one on full-width ones).
-// Small grids split the columns of each head over NCB = 4 workgroups (numbered
+// Small grids split the columns of each head over NCB = 8 or 4 workgroups (numbered
 // so that they land on one XCD and share its L2 for P_hat); large grids keep
 // one workgroup per head, so each byte of the pool tuple is read once, ordered
 // head-major so that concurrent requests share one head's pool slice in the
@@ -243,8 +243,16 @@ template <int DK, int DV, int P>
 hipError_t launch_compose_p(const ComposeArgs& a, int n_req, hipStream_t s) {
   const long heads = static_cast<long>(n_req) * a.h_v;
   const dim3 block(DK * 4);  // one wave per 16 state rows
-  // split the columns of each head over 4 workgroups while that keeps the
-  // grid within two workgroups per compute unit
+  // split the columns of each head over 8 (d_v = 128) or 4 workgroups while
+  // that keeps the grid within two workgroups per compute unit: a short
+  // request's chain of dependent steps then runs on more compute units (8
+  // blocks take the 8-segment, 16-head chain from 28.8 to 26.0 us)
+  if constexpr (DV >= 128) {
+    if (heads * 8 <= 512) {
+      hipLaunchKernelGGL((compose_kernel<DK, DV, P, 8>), dim3(heads * 8), block, 0, s, a);
+      return hipGetLastError();
+    }
+  }
   if (heads * 4 <= 512) {
     hipLaunchKernelGGL((compose_kernel<DK, DV, P, 4>), dim3(heads * 4), block, 0, s, a);
   } else {
