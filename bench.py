@@ -435,18 +435,17 @@ def bench_kda(torch, steps, warmup):
     its operator, timed with HIP events over back-to-back launches.  Every
     product runs on the bf16 matrix cores (the operator columns as three split
     passes), so the roofline peak is the bf16 one, as for the GDN build."""
-    from paper_2607_01299_amd import ops
+    from paper_2607_01299_amd.pipeline import KdaPipeline
     w = W.segment_workload(2)
     q, k, v, beta, _ = _to_dev(w, torch)
     T = int(w["cu_seqlens"][-1])
     h_v, d_k, d_v = int(w["v"].shape[1]), w["d_k"], w["d_v"]
     gate = torch.from_numpy(W.family_gate("diagonal", T, h_v, d_k, w["seed"] + 2000)).cuda()
-    cu = w["cu_seqlens"]
+    pipe = KdaPipeline(q, k, v, beta, gate, w["cu_seqlens"])
     for _ in range(warmup):
-        ops.kda_build(q, k, v, beta, gate, cu)
+        pipe.build()
     torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    ms = _events_ms(torch, stream, lambda: ops.kda_build(q, k, v, beta, gate, cu), steps)
+    ms = _events_ms(torch, pipe.stream, pipe.build, steps)
     f_state, f_op = kda_flops(d_k, d_v, 64)
     flop = float(f_state + f_op) * T * h_v
     achieved = flop / (ms * 1e-3) / 1e12

@@ -389,6 +389,40 @@ class FamilyPipeline:
         self.seam()
 
 
+class KdaPipeline:
+    """KDA build (Tab. 1 KDA row: o, S_seg and the operator tuple), pre-bound;
+    the tuples compose with hypic_compose_segments."""
+
+    def __init__(self, q, k, v, beta, gate, cu_seqlens, *, want_operator=True):
+        self.lib = _lib.load()
+        dev = q.device
+        self.stream = torch.cuda.current_stream(dev)
+        sp = ctypes.c_void_p(self.stream.cuda_stream)
+        T, h_qk, d_k = q.shape
+        h_v, d_v = v.shape[1], v.shape[2]
+        self.dims = Dims(h_qk=h_qk, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_dtype_code(q), chunk=64)
+        self.inputs = (q, k, v, beta, gate)
+        self.cu_h, self.cu_d = _i32_pair(cu_seqlens, dev)
+        n_seg = len(self.cu_h) - 1
+        f32 = torch.float32
+        self.o = torch.empty((T, h_v, d_v), dtype=q.dtype, device=dev)
+        self.S_seg = torch.empty((n_seg, h_v, d_k, d_v), dtype=f32, device=dev)
+        self.P_hat = (torch.empty((n_seg, h_v, d_k, d_k), dtype=f32, device=dev)
+                      if want_operator else None)
+        self.log_decay = (torch.empty((n_seg, h_v), dtype=f32, device=dev)
+                          if want_operator else None)
+        ws_bytes = self.lib.hypic_workspace_bytes(_lib.HYPIC_OP_BUILD, ctypes.byref(self.dims),
+                                                  n_seg)
+        self.ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        self._build_args = (
+            ctypes.byref(self.dims), _p(q), _p(k), _p(v), _p(beta), _p(gate), _p(self.cu_d),
+            self.cu_h.ctypes.data_as(ctypes.c_void_p), n_seg, _p(self.o), _p(self.S_seg),
+            _p(self.P_hat), _p(self.log_decay), _p(self.ws), ws_bytes, sp)
+
+    def build(self):
+        _lib.check(self.lib.hypic_kda_build(*self._build_args))
+
+
 class FamilyComposeBurst:
     """Many requests composed from a pool of scalar- or diagonal-family
     tuples (Eq. (6) with the compressed operators of Tab. 3), pre-bound."""

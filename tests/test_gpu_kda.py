@@ -224,3 +224,17 @@ def test_kda_build_is_deterministic(hy):
     torch.cuda.synchronize()
     for key in ("o", "S_seg", "P_hat", "log_decay"):
         assert torch.equal(a[key], b[key]), key
+
+
+def test_kda_prebound_pipeline_equals_ops(hy):
+    """The pre-bound build the bench times gives exactly the tuple of kda_build."""
+    _say("kda bf16 pre-bound pipeline against kda_build")
+    from paper_2607_01299_amd.pipeline import KdaPipeline
+    w = _workload([300, 40, 129], (2, 4), 128, W.BF16)
+    q, k, v, beta, gate = _dev(w, W.BF16)
+    a = hy.kda_build(q, k, v, beta, gate, w["cu_seqlens"])
+    pipe = KdaPipeline(q, k, v, beta, gate, w["cu_seqlens"])
+    pipe.build()
+    torch.cuda.synchronize()
+    for key in ("o", "S_seg", "P_hat", "log_decay"):
+        assert torch.equal(a[key], getattr(pipe, key)), key
