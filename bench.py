@@ -25,6 +25,7 @@ Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 """
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -548,6 +549,13 @@ def main():
         sys.exit(1)
     from paper_2607_01299_amd import _lib
     _lib.load()
+    # Python's cyclic collector stays off in the GPU legs, as timeit keeps it
+    # off: a full collection of the interpreter's objects stalls the host for
+    # 40-60 ms, and one such pause inside a timed loop of short launches lets
+    # the queue drain (the conv leg read 0.297 ms per call for an 88 us kernel)
+    gc.collect()
+    gc.freeze()
+    gc.disable()
     if args.families_only:
         print(json.dumps({"families": bench_families(torch, args.steps, args.warmup,
                                                      args.seam_w),
