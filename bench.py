@@ -57,13 +57,15 @@ TRAFFIC_FILE = os.path.join(HERE, "profiles", "hbm_traffic.json")
 KERNEL_SOURCES = {
     "scan_bf16": ["scan_bf16.hip", "mfma.hpp", "scan.hpp"],
     "compose": ["compose.hip", "mfma.hpp", "scan.hpp"],
-    "family_scalar_build": ["family.hip", "mfma.hpp", "family.hpp"],
-    "family_diagonal_build": ["family.hip", "mfma.hpp", "family.hpp"],
-    "family_scalar_compose": ["family.hip", "mfma.hpp", "family.hpp"],
-    "family_diagonal_compose": ["family.hip", "mfma.hpp", "family.hpp"],
+    "family_scalar_build": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
+    "family_diagonal_build": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
+    "family_scalar_compose": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
+    "family_diagonal_compose": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
+    "kda_build": ["kda.hip", "kda.hpp", "scan.hpp", "mfma.hpp", "frag_common.hpp"],
 }
 FAMILY_WORKLOAD = W.CONFIG_NAMES[2] + "; gates from workloads.family_gate (softplus)"
 FAMILY_BURST_WORKLOAD = W.CONFIG_NAMES[5] + " (family tuples)"
+KDA_WORKLOAD = W.CONFIG_NAMES[2] + "; per-channel gates from workloads.family_gate (diagonal, softplus)"
 
 
 def _code_only(src):
@@ -451,11 +453,12 @@ def bench_kda(torch, steps, warmup):
     flop = float(f_state + f_op) * T * h_v
     achieved = flop / (ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS
-    return {"workload": W.CONFIG_NAMES[2] + "; per-channel gates from workloads.family_gate "
-                        "(diagonal, softplus)",
+    return {"workload": KDA_WORKLOAD,
             "tokens_per_s": T / (ms * 1e-3), "build_ms": ms,
             "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                         "frac": achieved / peak, "traffic": None,
+                         "frac": achieved / peak,
+                         # both launches of one build
+                         "traffic": measured_traffic("kda_build", KDA_WORKLOAD),
                          "kernel": "kda_scan_kernel (state and operator launches)",
                          "flop_per_launch": flop,
                          "flop_split": {"state": float(f_state) * T * h_v,

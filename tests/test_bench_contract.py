@@ -78,3 +78,22 @@ def test_more_than_one_gpu_is_refused():
     assert res.returncode == 2
     assert "one GPU" in res.stderr
     assert res.stdout == ""
+
+
+def test_traffic_records_hash_every_header_their_kernels_include():
+    """A counter record is dropped when its kernel's code changes; the code is
+    the kernel file and every local header it reaches through #include."""
+    import re
+    csrc = os.path.join(ROOT, "paper_2607_01299_amd", "csrc")
+
+    def reach(name, seen):
+        if name in seen:
+            return seen
+        seen.add(name)
+        with open(os.path.join(csrc, name)) as f:
+            for inc in re.findall(r'#include "([^"]+)"', f.read()):
+                reach(inc, seen)
+        return seen
+
+    for kernel, files in bench.KERNEL_SOURCES.items():
+        assert set(files) == reach(files[0], set()), kernel
