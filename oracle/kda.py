@@ -13,12 +13,13 @@ Per head and token t (Eq. (2) with the Tab. 1 KDA row):
 with the gate ``g_t`` in R^{d_k} in natural-log units.  Tab. 3 stores the
 segment operator in full, ``T_C = prod_t (I - beta_t k_t k_t^T) diag(exp(g_t))``
 (later tokens on the left).  Here it is carried as ``T_C = exp(log_decay) P_hat``
-with a scalar ``log_decay`` chosen to keep ``P_hat`` within float32 range on
-long segments: the sum, over the segment's chunks of C tokens (chunks restart
-at the segment start), of the largest per-channel gate sum of the chunk.  This
-is a convention of the cache format, not part of the method; any scalar split
-gives the same ``T_C``, and the Eq. (6) composition of the GDN tuples applies
-unchanged.
+with a scalar ``log_decay`` that keeps ``P_hat`` in range on long segments.  The
+oracle factors each token's gate by its largest channel, m_t = max_c g_tc:
+``T_t = exp(m_t) (I - beta_t k_t k_t^T) diag(exp(g_t - m_t))``, so
+``log_decay = sum_t m_t`` and ``P_hat`` is the product of the rescaled factors.
+Tab. 3 fixes only ``T_C``; any scalar split gives the same operator, so a cache
+may choose another one, and comparisons are made on ``T_C`` (the Eq. (6)
+composition of the GDN tuples reads any split).
 
 All arithmetic is numpy float64; inputs are upcast exactly.
 """
@@ -67,26 +68,33 @@ def kda_transition_product(k, beta, gate):
     return T_C
 
 
-def kda_log_scale(gate, chunk=64):
-    """The scalar ``log_decay`` of the cached KDA operator: for each chunk of
-    ``chunk`` tokens from the segment start (the last one partial), the largest
-    over channels of the chunk's gate sum, summed over the chunks.  gate: [L, d_k]."""
-    gate = _f64(gate)
-    L = gate.shape[0]
-    total = 0.0
-    for lo in range(0, L, chunk):
-        total += float(np.max(np.sum(gate[lo:lo + chunk], axis=0)))
-    return total
+def kda_operator(k, beta, gate):
+    """``T_C`` of Tab. 3 as ``(log_decay, P_hat)`` with ``T_C = exp(log_decay) P_hat``:
+    each token's factor is split as ``exp(m_t) (I - beta_t k_t k_t^T) diag(exp(g_t - m_t))``
+    with ``m_t`` its largest gate, so ``P_hat`` is the ordered product of the
+    rescaled factors (later tokens on the left) and ``log_decay = sum_t m_t``.
+    k: [L, d_k]; beta: [L]; gate: [L, d_k]."""
+    k, beta, gate = _f64(k), _f64(beta), _f64(gate)
+    L, d_k = k.shape
+    P = np.eye(d_k)
+    ld = 0.0
+    for t in range(L):
+        m = float(np.max(gate[t]))
+        Pp = np.exp(gate[t] - m)[:, None] * P
+        P = Pp - beta[t] * np.outer(k[t], k[t] @ Pp)
+        ld += m
+    return ld, P
 
 
-def kda_build_segments(q, k, v, beta, gate, cu_seqlens, want_operator=True, chunk=64,
+def kda_build_segments(q, k, v, beta, gate, cu_seqlens, want_operator=True,
                        seg_head_pairs=None):
     """Zero-start build of every segment of a packed batch (Sec. 4.2 cache tuple).
 
     q, k: [T, h_qk, d_k]; v: [T, h_v, d_v]; beta: [T, h_v]; gate: [T, h_v, d_k].
     Returns dict with o [T, h_v, d_v], S_seg [n_seg, h_v, d_k, d_v],
     P_hat [n_seg, h_v, d_k, d_k] and log_decay [n_seg, h_v] with
-    ``T_C = exp(log_decay) P_hat``; pairs not listed stay NaN.
+    ``T_C = exp(log_decay) P_hat`` in the split of ``kda_operator``; pairs not
+    listed stay NaN.
     """
     T, h_qk, d_k = np.shape(k)
     h_v, d_v = np.shape(v)[1], np.shape(v)[2]
@@ -104,10 +112,8 @@ def kda_build_segments(q, k, v, beta, gate, cu_seqlens, want_operator=True, chun
         o[lo:hi, h], S_seg[s, h] = kda_recurrence(q[lo:hi, g], k[lo:hi, g], v[lo:hi, h],
                                                   beta[lo:hi, h], gate[lo:hi, h])
         if want_operator:
-            ld = kda_log_scale(gate[lo:hi, h], chunk) if hi > lo else 0.0
-            T_C = kda_transition_product(k[lo:hi, g], beta[lo:hi, h], gate[lo:hi, h])
-            P_hat[s, h] = np.exp(-ld) * T_C
-            log_decay[s, h] = ld
+            log_decay[s, h], P_hat[s, h] = kda_operator(k[lo:hi, g], beta[lo:hi, h],
+                                                        gate[lo:hi, h])
     return {"o": o, "S_seg": S_seg, "P_hat": P_hat, "log_decay": log_decay}
 
 

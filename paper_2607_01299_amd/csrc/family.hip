@@ -39,9 +39,12 @@
 //  * family_pipe_kernel (scalar family, bf16 inputs): four waves hold the
 //    state and make the outputs of chunk c while the other four stage and
 //    form chunk c + 1, double-buffered.
-// bf16 inputs use bf16 matrix-core products with float32 accumulation (every
-// decayed operand is rounded to bf16 once); float32 inputs use the float32
-// matrix cores.
+// bf16 inputs use bf16 matrix-core products with float32 accumulation; the
+// decayed operands of the state update and of the inter-chunk term are
+// rounded to bf16 once, while the diagonal family's tile-referred Q and K of
+// the intra-chunk scores A are kept as bf16 hi + lo pairs (three passes), so a
+// score whose q . k terms cancel keeps its float32 accuracy.  float32 inputs
+// use the float32 matrix cores.
 //
 // Composition (Eq. (6) with the compressed operators of Tab. 3) is
 // elementwise: S <- exp(log_decay_i) . S + S_seg_i, streamed 16 bytes per
@@ -77,8 +80,13 @@ struct FamLds {
   static constexpr int PAD = (sizeof(ST) == 2) ? 8 : 4;
   static constexpr int LDK = DK + PAD;  // Q, K rows (token-major)
   static constexpr int LDT = FC + PAD;  // rows of the token-minor operands and of A
-  ST q[FC * LDK];     // Q, then (diagonal) Q . exp(B - Bbar)
-  ST k[FC * LDK];     // K, then (diagonal) K . exp(Bbar - B)
+  // diagonal family, bf16 operands: the tile-referred Q and K are also kept as
+  // their bf16 remainders (lo), so the A tiles run on hi + lo operands
+  static constexpr bool SPL = DG && sizeof(ST) == 2;
+  alignas(16) ST q[FC * LDK];     // Q, then (diagonal) Q . exp(B - Bbar)
+  alignas(16) ST k[FC * LDK];     // K, then (diagonal) K . exp(Bbar - B)
+  alignas(16) ST qlo[SPL ? FC * LDK : 8];  // remainders of Q . exp(B - Bbar)
+  alignas(16) ST klo[SPL ? FC * LDK : 8];  // remainders of K . exp(Bbar - B)
   ST kdt[DK * LDT];   // (K . exp(B_last - B))^T: channel-major
   ST vt[FNC * LDT];   // V^T of this workgroup's columns: column-major
   ST a[FC * LDT];     // A (lower 16 x 16 tiles; the upper tiles read stay 0)
@@ -330,8 +338,13 @@ __global__ __launch_bounds__(kFT) void family_scan_kernel(FamArgs args) {
             const float kv = ldv(kp);
             const float e = __expf(pre[j]);      // exp(B_t - Bbar) <= 1
             const float ie = __expf(-pre[j]);    // >= 1, bounded by 16 tokens of decay
-            stv(qp, ldv(qp) * e);
-            stv(kp, kv * ie);
+            const float qs = ldv(qp) * e, ks = kv * ie;
+            stv(qp, qs);
+            stv(kp, ks);
+            if constexpr (L::SPL) {
+              stv(sm.qlo + t * LDK + pc, qs - bf16_round(qs));
+              stv(sm.klo + t * LDK + pc, ks - bf16_round(ks));
+            }
             kd[jj] = kv * (gdec * ie);           // K exp(B_last - B_t)
           }
           st8(sm.kdt + pc * LDT + t0 + j8, kd);
@@ -353,14 +366,28 @@ __global__ __launch_bounds__(kFT) void family_scan_kernel(FamArgs args) {
       const int tq = (tile < 1) ? 0 : ((tile < 3) ? 1 : ((tile < 6) ? 2 : 3));
       const int tk = tile - tq * (tq + 1) / 2;
       f32x4 acc = zero4();
+      if constexpr (L::SPL) {
+        // q_t . k_i exp(B_t - B_i) can nearly cancel; one bf16 rounding of the
+        // gate-scaled operands would then dominate the score, so both operands
+        // run as hi + lo (three passes)
 #pragma unroll
-      for (int kb = 0; kb < DK; kb += 32) {
-        Frag<ST> fa;
-        if (DIAG && tk < tq)
-          fa = frag_row_scaled(sm.q, LDK, tq * 16 + ln, kb, g, sm.fx + pair_idx(tq, tk) * DK);
-        else
-          fa = frag_row(sm.q, LDK, tq * 16 + ln, kb, g);
-        acc = mma(fa, frag_row(sm.k, LDK, tk * 16 + ln, kb, g), acc);
+        for (int kb = 0; kb < DK; kb += 32) {
+          const SplitFrag fa =
+              (tk < tq) ? frag_row_split_scaled(sm.q, sm.qlo, LDK, tq * 16 + ln, kb, g,
+                                                sm.fx + pair_idx(tq, tk) * DK)
+                        : frag_row_split(sm.q, sm.qlo, LDK, tq * 16 + ln, kb, g);
+          acc = mma3(fa, frag_row_split(sm.k, sm.klo, LDK, tk * 16 + ln, kb, g), acc);
+        }
+      } else {
+#pragma unroll
+        for (int kb = 0; kb < DK; kb += 32) {
+          Frag<ST> fa;
+          if (DIAG && tk < tq)
+            fa = frag_row_scaled(sm.q, LDK, tq * 16 + ln, kb, g, sm.fx + pair_idx(tq, tk) * DK);
+          else
+            fa = frag_row(sm.q, LDK, tq * 16 + ln, kb, g);
+          acc = mma(fa, frag_row(sm.k, LDK, tk * 16 + ln, kb, g), acc);
+        }
       }
       const int key = tk * 16 + ln;
 #pragma unroll

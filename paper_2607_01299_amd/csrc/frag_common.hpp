@@ -92,6 +92,63 @@ __device__ __forceinline__ Frag<ST> frag_row_scaled(const ST* M, int ld, int row
   return f;
 }
 
+// Split-bf16 operands: a float32 value x is carried as hi = bf16(x) and
+// lo = bf16(x - hi), about 2^-16 relative together, and a product of two such
+// operands runs as three bf16 passes (hi hi + hi lo + lo hi).  Used where one
+// bf16 rounding of a gate-scaled operand is too coarse: an intra-chunk score
+// q_t . k_i that nearly cancels.
+__device__ __forceinline__ float bf16_round(float x) {
+  return static_cast<float>(static_cast<__bf16>(x));
+}
+struct SplitFrag {
+  Frag<u16> h, l;
+};
+__device__ __forceinline__ f32x4 mma3(const SplitFrag& a, const SplitFrag& b, f32x4 c) {
+  c = mma(a.h, b.h, c);
+  c = mma(a.h, b.l, c);
+  return mma(a.l, b.h, c);
+}
+// slot j = M[row][kb + kap(g, j)] with M held as hi + lo arrays of one layout
+__device__ __forceinline__ SplitFrag frag_row_split(const u16* Mh, const u16* Ml, int ld, int row,
+                                                    int kb, int g) {
+  SplitFrag f;
+  f.h = frag_row(Mh, ld, row, kb, g);
+  f.l = frag_row(Ml, ld, row, kb, g);
+  return f;
+}
+// slot j = (Mh + Ml)[row][kb + kap(g, j)] * s[kb + kap(g, j)], split again
+__device__ __forceinline__ SplitFrag frag_row_split_scaled(const u16* Mh, const u16* Ml, int ld,
+                                                           int row, int kb, int g,
+                                                           const float* s) {
+  const Frag<u16> rh = frag_row(Mh, ld, row, kb, g), rl = frag_row(Ml, ld, row, kb, g);
+  const float4 s0 = *reinterpret_cast<const float4*>(s + kb + 4 * g);
+  const float4 s1 = *reinterpret_cast<const float4*>(s + kb + 16 + 4 * g);
+  const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+  SplitFrag f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float x = (static_cast<float>(rh.x[j]) + static_cast<float>(rl.x[j])) * sv[j];
+    const float xh = bf16_round(x);
+    f.h.set(j, xh);
+    f.l.set(j, x - xh);
+  }
+  return f;
+}
+// slot j = (Mh + Ml)[row][kb + kap(g, j)] * s[kb + kap(g, j)], rounded once
+__device__ __forceinline__ Frag<u16> frag_row_sum_scaled(const u16* Mh, const u16* Ml, int ld,
+                                                         int row, int kb, int g,
+                                                         const float* s) {
+  const Frag<u16> rh = frag_row(Mh, ld, row, kb, g), rl = frag_row(Ml, ld, row, kb, g);
+  const float4 s0 = *reinterpret_cast<const float4*>(s + kb + 4 * g);
+  const float4 s1 = *reinterpret_cast<const float4*>(s + kb + 16 + 4 * g);
+  const float sv[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+  Frag<u16> f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    f.set(j, (static_cast<float>(rh.x[j]) + static_cast<float>(rl.x[j])) * sv[j]);
+  return f;
+}
+
 // index of the tile pair (tq, tk), tk < tq, in fx
 __device__ __forceinline__ int pair_idx(int tq, int tk) { return tq * (tq - 1) / 2 + tk; }
 

@@ -36,9 +36,12 @@
 // 64-column block) chain over its chunks; each wave holds 16 columns x half the
 // d_k rows of the block's state in registers.  State columns use the input
 // precision on the matrix cores (bf16 operands with float32 accumulation for
-// bf16 inputs); operator columns always keep float32 operands in LDS and run
-// their products as three-pass split bf16, so that the normalised operator
-// does not pick up a one-pass bf16 rounding per chunk.  The 64 x 64 inverse
+// bf16 inputs), except the intra-chunk scores G and A, whose tile-referred
+// gate-scaled operands are kept as bf16 hi + lo pairs (three passes): a score
+// q_t . k_i that nearly cancels would otherwise be dominated by one bf16
+// rounding of its operands.  Operator columns always keep float32 operands in
+// LDS and run their products as three-pass split bf16, so that the
+// normalised operator does not pick up a one-pass bf16 rounding per chunk.  The 64 x 64 inverse
 // runs in float32: the four diagonal
 // 16 x 16 blocks by forward substitution (one lane per column), then block row
 // by block row, T_ij = -X_i sum_k L_ik T_kj, on the float32 matrix cores.
@@ -69,24 +72,28 @@ struct KdaLds {
   alignas(16) ST qk[KC * LDK];
   alignas(16) ST kk[KC * LDK];    // K, then K . exp(Bbar - B)
   alignas(16) float lt[KC * LTD]; // diag(beta) G (strict lower) -> its inverse T (in place) -> A
-  // state columns only: V^T of the block's columns; with bf16 operands (PRE)
-  // also K . exp(B) (Y), then Q . exp(B) (outputs), and (K . exp(B_last - B))^T
-  // channel-major (float32 operands form them on the fly: no LDS left for them)
+  // state columns only: V^T of the block's columns (read in stage 3 only;
+  // with bf16 operands the A tiles of stage 7 reuse it).  With bf16 operands
+  // (PRE) also (K . exp(B_last - B))^T channel-major (float32 operands form it
+  // on the fly: no LDS left for it), and (SPL) the bf16 remainders of the
+  // query-side and key-side operands, so that the scores G and A run on hi + lo
+  // operands: a q_t . k_i that nearly cancels keeps its float32 accuracy
   static constexpr bool PRE = !OP && sizeof(ST) == 2;
+  static constexpr bool SPL = PRE;
   alignas(16) ST vt[OP ? 1 : KNC * LDV];
-  alignas(16) ST kb[PRE ? KC * LDK : 1];
   alignas(16) ST kdt[PRE ? DK * LDV : 1];
+  alignas(16) ST qlo[SPL ? KC * LDK : 8];  // remainders of qk
+  alignas(16) ST klo[SPL ? KC * LDK : 8];  // remainders of kk
   // the off-diagonal 16 x 16 blocks of the inverse, kept apart from L (TB:
   // bf16 state columns and operator columns; float32 state columns write them
   // into lt, which takes a second barrier per block row)
   static constexpr bool TB = PRE || OP;
-  static constexpr int TBS = 20;  // row stride of a block
+  static constexpr int TBS = SPL ? 16 : 20;  // row stride of a block
   alignas(16) float tb[TB ? 6 * 16 * TBS : 4];
   // bf16 state columns (NS): N republished into a second fragment buffer and
-  // A formed into its own array, in one stage
+  // A formed into vt (free after stage 3), in one stage
   static constexpr bool NS = PRE;
   alignas(16) Frag<ST> rf2[NS ? NCG * 2 * 64 : 1];
-  alignas(16) ST la[NS ? KC * LDV : 1];
   // S0 as B fragments: column group, 32-row block, lane
   alignas(16) Frag<ST> s0f[NCG][DK / 32][64];
   alignas(16) Frag<ST> rf[NCG][2][64];         // diag(beta) R, then N, as B fragments over tokens
@@ -185,6 +192,50 @@ __device__ __forceinline__ Frag<ST> frag_T(const float* lt, const float* tb, int
   return f;
 }
 
+// One 16 x 16 score tile (query tile tq, key tile tk <= tq) over all d_k
+// channels from the tile-referred operands: sum_c qk[t][c] kk[i][c], with
+// the query side scaled by exp(Bbar_tq - Bbar_tk) for tk < tq.  SPL: both
+// operands as hi + lo, three bf16 passes.
+template <typename ST, int DK, bool OP, bool SPL>
+__device__ __forceinline__ f32x4 score_tile(const ST* qk, const ST* qlo, const ST* kk,
+                                            const ST* klo, const float* fx, int tq, int tk,
+                                            int g, int ln) {
+  constexpr int LDK = DK + ((sizeof(ST) == 2) ? 8 : 4);
+  f32x4 acc = zero4();
+  if constexpr (SPL) {
+#pragma unroll
+    for (int kb = 0; kb < DK; kb += 32) {
+      const SplitFrag fa =
+          (tk < tq) ? frag_row_split_scaled(qk, qlo, LDK, tq * 16 + ln, kb, g,
+                                            fx + pair_ix(tq, tk) * DK)
+                    : frag_row_split(qk, qlo, LDK, tq * 16 + ln, kb, g);
+      acc = mma3(fa, frag_row_split(kk, klo, LDK, tk * 16 + ln, kb, g), acc);
+    }
+  } else {
+#pragma unroll
+    for (int kb = 0; kb < DK; kb += 32) {
+      Frag<ST> fa;
+      if (tk < tq)
+        fa = frag_row_scaled(qk, LDK, tq * 16 + ln, kb, g, fx + pair_ix(tq, tk) * DK);
+      else
+        fa = frag_row(qk, LDK, tq * 16 + ln, kb, g);
+      acc = mmk<OP>(fa, frag_row(kk, LDK, tk * 16 + ln, kb, g), acc);
+    }
+  }
+  return acc;
+}
+
+// A-operand fragment of the query-side operand times exp(Bbar) of its tile
+// (K . exp(B) in stage 3, Q . exp(B) in stage 8); SPL: from hi + lo, rounded once
+template <typename ST, bool SPL>
+__device__ __forceinline__ Frag<ST> frag_decayed(const ST* qk, const ST* qlo, int ld, int row,
+                                                 int kb, int g, const float* s) {
+  if constexpr (SPL)
+    return frag_row_sum_scaled(qk, qlo, ld, row, kb, g, s);
+  else
+    return frag_row_scaled(qk, ld, row, kb, g, s);
+}
+
 __device__ __forceinline__ int kda_segment_of_rank(const KdaArgs& a, int rank) {
   return a.n_inline > 0 ? static_cast<int>(a.order_inline[rank]) : a.order[rank];
 }
@@ -204,11 +255,13 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
   static_assert(NQ >= 1 && NMH % 2 == 0 && NRG == 2, "tile split");
   static_assert(TPT == 16 || TPT == 8, "gate split");
   static_assert(sizeof(L) <= 160 * 1024, "LDS budget");
-  constexpr bool PRE = L::PRE, TB = L::TB, NS = L::NS;
+  constexpr bool PRE = L::PRE, TB = L::TB, NS = L::NS, SPL = L::SPL;
   constexpr int TBS = L::TBS;
+  static_assert(KNC == KC, "A reuses the V^T array");
 
   extern __shared__ __align__(16) unsigned char smem_raw[];
   L& sm = *reinterpret_cast<L*>(smem_raw);
+  ST* const la = sm.vt;  // A (NS): stages 7-8, after V^T's last read in stage 3
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -271,12 +324,11 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
     }
   }
 
-  // the upper 16 x 16 tiles of the 64 x 64 matrices read with their rows,
-  // (0, 1) and (2, 3), stay zero
+  // the upper 16 x 16 tiles of L read with its rows, (0, 1) and (2, 3), stay
+  // zero (those of A in vt are cleared per chunk, in stage 7)
   {
     const int t = tid >> 8, e = tid & 255;
     sm.lt[(32 * t + (e >> 4)) * LTD + 32 * t + 16 + (e & 15)] = 0.f;
-    if constexpr (NS) stv(sm.la + (32 * t + (e >> 4)) * LDV + 32 * t + 16 + (e & 15), 0.f);
   }
 
   // ---- register prefetch of one chunk ----
@@ -385,7 +437,7 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
       float base = 0.f;
       if constexpr (TPT == 8) base = (pt & 1) ? sm.part[(pt - 1) * DK + pc] : 0.f;
       const int t0 = TPT * pt;
-      const float hbt = hb[tile], ehb = __expf(hbt);
+      const float hbt = hb[tile];
 #pragma unroll
       for (int j8 = 0; j8 < TPT; j8 += 8) {
         float kd[8];
@@ -394,13 +446,14 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
           const int j = j8 + jj, t = t0 + j;
           const float rel = base + pre[j];  // B_t - Bbar of the token's tile, <= 0
           const float kv = ldv(sm.kk + t * LDK + pc);
-          const float e = __expf(rel);
-          stv(sm.qk + t * LDK + pc, kv * e);
-          stv(sm.kk + t * LDK + pc, kv * __expf(-rel));
-          if constexpr (PRE) {
-            stv(sm.kb + t * LDK + pc, kv * e * ehb);                 // K exp(B_t)
-            kd[jj] = kv * __expf(b_last - hbt - rel);                // K exp(B_last - B_t)
+          const float qs = kv * __expf(rel), ks = kv * __expf(-rel);
+          stv(sm.qk + t * LDK + pc, qs);
+          stv(sm.kk + t * LDK + pc, ks);
+          if constexpr (SPL) {
+            stv(sm.qlo + t * LDK + pc, qs - bf16_round(qs));
+            stv(sm.klo + t * LDK + pc, ks - bf16_round(ks));
           }
+          if constexpr (PRE) kd[jj] = kv * __expf(b_last - hbt - rel);  // K exp(B_last - B_t)
         }
         if constexpr (PRE) st8(sm.kdt + pc * LDV + t0 + j8, kd);
       }
@@ -426,16 +479,8 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
     for (int tile = wave; tile < 10; tile += 8) {
       const int tq = (tile < 1) ? 0 : ((tile < 3) ? 1 : ((tile < 6) ? 2 : 3));
       const int tk = tile - tq * (tq + 1) / 2;
-      f32x4 acc = zero4();
-#pragma unroll
-      for (int kb = 0; kb < DK; kb += 32) {
-        Frag<ST> fa;
-        if (tk < tq)
-          fa = frag_row_scaled(sm.qk, LDK, tq * 16 + ln, kb, g, sm.fx + pair_ix(tq, tk) * DK);
-        else
-          fa = frag_row(sm.qk, LDK, tq * 16 + ln, kb, g);
-        acc = mmk<OP>(fa, frag_row(sm.kk, LDK, tk * 16 + ln, kb, g), acc);
-      }
+      const f32x4 acc = score_tile<ST, DK, OP, SPL>(sm.qk, sm.qlo, sm.kk, sm.klo, sm.fx, tq,
+                                                    tk, g, ln);
       const int key = tk * 16 + ln;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -450,14 +495,10 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
         const int mt = 2 * rgrp + mh;  // token tile
         f32x4 acc = zero4();
 #pragma unroll
-        for (int kt = 0; kt < DK / 32; ++kt) {
-          Frag<ST> fa;
-          if constexpr (PRE)
-            fa = frag_row(sm.kb, LDK, mt * 16 + ln, 32 * kt, g);
-          else
-            fa = frag_row_scaled(sm.qk, LDK, mt * 16 + ln, 32 * kt, g, sm.hx + mt * DK);
-          acc = mmk<OP>(fa, sm.s0f[cg][kt][lane], acc);
-        }
+        for (int kt = 0; kt < DK / 32; ++kt)
+          acc = mmk<OP>(frag_decayed<ST, SPL>(sm.qk, sm.qlo, LDK, mt * 16 + ln, 32 * kt, g,
+                                              sm.hx + mt * DK),
+                        sm.s0f[cg][kt][lane], acc);
         const float4 bt = *reinterpret_cast<const float4*>(sm.beta + mt * 16 + 4 * g);
         float vv[4] = {0.f, 0.f, 0.f, 0.f};
         if constexpr (!OP) {
@@ -513,19 +554,13 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
     if constexpr (!OP) {
       float base = 0.f;
       if constexpr (TPT == 8) base = (pt & 1) ? sm.part[(pt - 1) * DK + pc] : 0.f;
-      float hbt = 0.f;  // Bbar of this thread's tile
-#pragma unroll
-      for (int p = 0; p < ((TPT == 16) ? pt : pt / 2); ++p)
-        hbt += (TPT == 16) ? sm.part[p * DK + pc]
-                           : sm.part[(2 * p) * DK + pc] + sm.part[(2 * p + 1) * DK + pc];
-      const float ehb = __expf(hbt);
 #pragma unroll
       for (int j = 0; j < TPT; ++j) {
         const int t = TPT * pt + j;
         ST* qp = sm.qk + t * LDK + pc;
         const float qv = ldv(qp) * __expf(base + pre[j]);
         stv(qp, qv);
-        if constexpr (PRE) stv(sm.kb + t * LDK + pc, qv * ehb);  // Q exp(B_t)
+        if constexpr (SPL) stv(sm.qlo + t * LDK + pc, qv - bf16_round(qv));
       }
     }
 #pragma unroll
@@ -606,26 +641,24 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
       for (int tile = wave; tile < 10; tile += 8) {
         const int tq = (tile < 1) ? 0 : ((tile < 3) ? 1 : ((tile < 6) ? 2 : 3));
         const int tk = tile - tq * (tq + 1) / 2;
-        f32x4 acc = zero4();
-#pragma unroll
-        for (int kb = 0; kb < DK; kb += 32) {
-          Frag<ST> fa;
-          if (tk < tq)
-            fa = frag_row_scaled(sm.qk, LDK, tq * 16 + ln, kb, g, sm.fx + pair_ix(tq, tk) * DK);
-          else
-            fa = frag_row(sm.qk, LDK, tq * 16 + ln, kb, g);
-          acc = mmk<OP>(fa, frag_row(sm.kk, LDK, tk * 16 + ln, kb, g), acc);
-        }
+        const f32x4 acc = score_tile<ST, DK, OP, SPL>(sm.qk, sm.qlo, sm.kk, sm.klo, sm.fx, tq,
+                                                      tk, g, ln);
         const int key = tk * 16 + ln;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int t = tq * 16 + 4 * g + i;
           const float x = (key <= t) ? acc[i] : 0.f;
           if constexpr (NS)
-            stv(sm.la + t * LDV + key, x);
+            stv(la + t * LDV + key, x);
           else
             sm.lt[t * LTD + key] = x;
         }
+      }
+      if constexpr (NS) {
+        // the upper tiles (0, 1) and (2, 3) read with A's rows are zero (vt
+        // held V^T there)
+        const int t = tid >> 8, e = tid & 255;
+        stv(la + (32 * t + (e >> 4)) * LDV + 32 * t + 16 + (e & 15), 0.f);
       }
     }
     lds_barrier();
@@ -642,19 +675,15 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
         const int mt = 2 * rgrp + mh;
         f32x4 acc = zero4();
 #pragma unroll
-        for (int kt = 0; kt < DK / 32; ++kt) {
-          Frag<ST> fa;
-          if constexpr (PRE)
-            fa = frag_row(sm.kb, LDK, mt * 16 + ln, 32 * kt, g);
-          else
-            fa = frag_row_scaled(sm.qk, LDK, mt * 16 + ln, 32 * kt, g, sm.hx + mt * DK);
-          acc = mmk<OP>(fa, sm.s0f[cg][kt][lane], acc);
-        }
+        for (int kt = 0; kt < DK / 32; ++kt)
+          acc = mmk<OP>(frag_decayed<ST, SPL>(sm.qk, sm.qlo, LDK, mt * 16 + ln, 32 * kt, g,
+                                              sm.hx + mt * DK),
+                        sm.s0f[cg][kt][lane], acc);
 #pragma unroll
         for (int kt = 0; kt < 2; ++kt)
           if (32 * kt < 16 * (mt + 1)) {
             if constexpr (NS)
-              acc = mmk<OP>(frag_row(sm.la, LDV, mt * 16 + ln, 32 * kt, g),
+              acc = mmk<OP>(frag_row(la, LDV, mt * 16 + ln, 32 * kt, g),
                             sm.rf2[(cg * 2 + kt) * 64 + lane], acc);
             else
               acc = mmk<OP>(frag_f32<ST>(sm.lt, LTD, mt * 16 + ln, 32 * kt, g),

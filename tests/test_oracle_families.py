@@ -391,7 +391,31 @@ def test_causal_conv_matches_numpy_convolve():
         assert np.allclose(y[:, c], ref, atol=1e-13, rtol=0)
     assert np.array_equal(tail, xx[-(K - 1):])
     ya, _ = F.causal_conv(x, w, conv_state=st)
-    assert np.allclose(ya, ref_silu := y / (1 + np.exp(-y)), atol=1e-14, rtol=0), ref_silu.shape
+    assert np.array_equal(ya, F.silu(y))  # the activation is applied to the conv output
+
+
+def test_silu_identities():
+    """SiLU pinned by properties its definition x sigmoid(x) implies, none of
+    which restates it: silu(0) = 0; the odd part silu(x) - silu(-x) = x
+    (because sigmoid(x) + sigmoid(-x) = 1); silu(x) -> x for large x and -> 0
+    for large negative x; at x = ln 3, sigmoid = 3/4 exactly; the minimum
+    near x = -1.2785 (where silu' = 0) has value -0.2784645...; a planted
+    mistake (tanh in place of sigmoid) breaks the odd-part identity."""
+    x = np.linspace(-30.0, 30.0, 6001)
+    assert F.silu(np.array([0.0]))[0] == 0.0
+    assert np.allclose(F.silu(x) - F.silu(-x), x, atol=1e-13, rtol=0)
+    assert abs(F.silu(np.array([40.0]))[0] - 40.0) < 1e-15 * 40 + 1e-15
+    assert abs(F.silu(np.array([-40.0]))[0]) < 1e-15
+    assert abs(F.silu(np.array([np.log(3.0)]))[0] - 0.75 * np.log(3.0)) < 1e-15
+    # the minimum of x sigmoid(x): silu' = 0 where 1 + x sigmoid(-x) = 0, i.e.
+    # x* = -1 - W(1/e) (W the Lambert function) = -1.27846454276107..., and there
+    # sigmoid(x*) = 1 + 1/x*, so silu(x*) = x* + 1
+    xs = np.linspace(-1.4, -1.1, 300001)
+    ys = F.silu(xs)
+    assert abs(xs[np.argmin(ys)] - (-1.27846454276107)) < 2e-6
+    assert abs(ys.min() - (-0.27846454276107)) < 1e-10
+    wrong = x * np.tanh(x)
+    assert not np.allclose(wrong - (-x) * np.tanh(-x), x, atol=1e-3)
 
 
 def test_conv_state_carries_across_windows():

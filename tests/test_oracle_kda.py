@@ -127,7 +127,7 @@ def test_kda_tuples_compose_to_the_concatenation():
     S0 = np.random.default_rng(9).standard_normal((6, 4))
     cu = [0, 70, 150]
     b = kda.kda_build_segments(q[:, None], k[:, None], v[:, None], beta[:, None], gate[:, None],
-                               cu, chunk=64)
+                               cu)
     S_out, S_inc = gdn.compose(b["P_hat"], b["log_decay"], b["S_seg"], [0, 1], [0, 2],
                                S_prefix=S0[None, None])
     o_full, S_full = kda.kda_recurrence(q, k, v, beta, gate, S0=S0)
@@ -141,18 +141,38 @@ def test_kda_tuples_compose_to_the_concatenation():
     assert _rel(b["S_seg"][0, 0] + b["S_seg"][1, 0], S_full) > 1e-2
 
 
-def test_kda_log_scale_is_the_sum_of_chunk_maxima():
-    """The cache-format scalar: chunks of 64 from the segment start, each
-    contributing its largest per-channel gate sum (hand-computed case)."""
-    gate = np.zeros((70, 3))
-    gate[:64, 0] = -1.0 / 64   # chunk 0 sums: -1, -2, -0.5
-    gate[:64, 1] = -2.0 / 64
-    gate[:64, 2] = -0.5 / 64
-    gate[64:, 0] = -0.3 / 6    # chunk 1 sums: -0.3, -0.1, -0.6
-    gate[64:, 1] = -0.1 / 6
-    gate[64:, 2] = -0.6 / 6
-    assert abs(kda.kda_log_scale(gate, 64) - (-0.5 - 0.1)) < 1e-14
-    b = kda.kda_build_segments(np.zeros((70, 1, 3)), np.eye(3)[np.arange(70) % 3][:, None],
-                               np.zeros((70, 1, 2)), np.full((70, 1), 0.5), gate[:, None], [0, 70])
-    T_C = kda.kda_transition_product(np.eye(3)[np.arange(70) % 3], np.full(70, 0.5), gate)
+def test_kda_operator_split_is_the_per_token_gate_maximum():
+    """The oracle's scalar split of T_C (Tab. 3 fixes only T_C): each token's
+    factor is divided by exp(max_c g_tc).  Hand-computed log_decay on a case
+    with known per-token maxima; exp(log_decay) P_hat equals the explicit
+    factor product; and P_hat stays in range where T_C itself underflows
+    float64 (the split can fail: without it the product is 0)."""
+    L, d = 70, 3
+    gate = np.zeros((L, d))
+    gate[:, 0] = -0.2
+    gate[:, 1] = -0.05          # the largest channel of every token
+    gate[:, 2] = -1.0
+    k = np.eye(d)[np.arange(L) % d]
+    beta = np.full(L, 0.5)
+    b = kda.kda_build_segments(np.zeros((L, 1, d)), k[:, None], np.zeros((L, 1, 2)),
+                               beta[:, None], gate[:, None], [0, L])
+    assert abs(b["log_decay"][0, 0] - L * -0.05) < 1e-13
+    T_C = kda.kda_transition_product(k, beta, gate)
     assert _rel(np.exp(b["log_decay"][0, 0]) * b["P_hat"][0, 0], T_C) < 1e-13
+    F = np.eye(d)
+    for t in range(L):
+        F = (np.eye(d) - beta[t] * np.outer(k[t], k[t])) @ np.diag(np.exp(gate[t])) @ F
+    assert _rel(T_C, F) < 1e-13
+    # 4000 tokens of channel-uniform gates near -0.3 and one fixed unit key:
+    # T_C ~ exp(-1200) underflows float64 (to zeros and denormals), while
+    # P_hat = I - (1 - (1 - beta)^L) k k^T in closed form
+    rng = np.random.default_rng(3)
+    Lh = 4000
+    gh = np.repeat(-0.3 + 0.01 * rng.standard_normal((Lh, 1)), d, axis=1)
+    kv = rng.standard_normal(d)
+    kv /= np.linalg.norm(kv)
+    kh = np.tile(kv, (Lh, 1))
+    ld, P = kda.kda_operator(kh, np.full(Lh, 0.5), gh)
+    assert np.max(np.abs(kda.kda_transition_product(kh, np.full(Lh, 0.5), gh))) < 1e-300
+    assert abs(ld - np.sum(gh[:, 0])) < 1e-9
+    assert _rel(P, np.eye(d) - (1.0 - 0.5 ** Lh) * np.outer(kv, kv)) < 1e-12
