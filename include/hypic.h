@@ -105,10 +105,11 @@ const char* hypic_status_str(int32_t status);
  *
  *   q, k        [T, h_qk, d_k] dtype    v [T, h_v, d_v] dtype
  *   beta        [T, h_v] f32            log_alpha [T, h_v] f32 (any finite values)
+ *   n_tokens    T, the rows of the packed token arrays (and of o).
  *   cu_seqlens  [n_seg + 1] int32 device; cu_seqlens_host the same values on the
- *               host: 0 = cu[0] <= cu[1] <= ... <= cu[n_seg] = T.  Segment s
- *               covers tokens [cu[s], cu[s+1]); a zero-length segment yields
- *               S_seg = 0, P_hat = I, log_decay = 0.
+ *               host: 0 = cu[0] <= cu[1] <= ... <= cu[n_seg] <= n_tokens, else
+ *               HYPIC_EINVAL.  Segment s covers tokens [cu[s], cu[s+1]); a
+ *               zero-length segment yields S_seg = 0, P_hat = I, log_decay = 0.
  *   o           [T, h_v, d_v] dtype, or NULL to skip the outputs.
  *   S_seg       [n_seg, h_v, d_k, d_v] f32: end state from S_0 = 0.
  *   P_hat       [n_seg, h_v, d_k, d_k] f32, or NULL to skip the operator path.
@@ -124,7 +125,8 @@ const char* hypic_status_str(int32_t status);
  */
 int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k,
                             const void* v, const float* beta,
-                            const float* log_alpha, const int32_t* cu_seqlens,
+                            const float* log_alpha, int32_t n_tokens,
+                            const int32_t* cu_seqlens,
                             const int32_t* cu_seqlens_host, int32_t n_seg,
                             void* o, float* S_seg, float* P_hat,
                             float* log_decay, void* workspace,
@@ -147,6 +149,7 @@ int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k
  *   S_prefix    [n_req, h_v, d_k, d_v] f32 or NULL.
  *   S_out       [n_req, h_v, d_k, d_v] f32.
  *   S_incoming  [nnz, h_v, d_k, d_v] f32 or NULL.
+ * P_hat, S_seg, S_prefix, S_out and S_incoming must be 16-byte aligned.
  * dims->dtype selects the arithmetic: F32 uses float32 matrix cores, BF16 uses
  * three-term split-bf16 products with float32 accumulation.  Workspace: none
  * (pass NULL, 0).  n_req == 0 enqueues nothing.
@@ -217,13 +220,14 @@ typedef enum hypic_family {
  * scalar- or diagonal-family layer (Sec. 4.2 cache tuple, Tab. 3 compressed
  * operator).
  *   q, k [T, h_qk, d_k] dtype; v [T, h_v, d_v] dtype; gate as above.
- *   cu_seqlens / cu_seqlens_host, o, S_seg, workspace: as in hypic_build_segment.
+ *   n_tokens, cu_seqlens / cu_seqlens_host, o, S_seg, workspace: as in
+ *   hypic_build_segment.
  *   log_decay   [n_seg, h_v] (scalar) or [n_seg, h_v, d_k] (diagonal) f32, or NULL.
  * A zero-length segment yields S_seg = 0 and log_decay = 0.
  * Returns HYPIC_EUNSUPPORTED for an unknown family.
  */
 int32_t hypic_family_build(const hypic_dims* dims, int32_t family, const void* q,
-                           const void* k, const void* v, const float* gate,
+                           const void* k, const void* v, const float* gate, int32_t n_tokens,
                            const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
                            int32_t n_seg, void* o, float* S_seg, float* log_decay,
                            void* workspace, size_t workspace_bytes, void* stream);
@@ -270,7 +274,7 @@ int32_t hypic_family_seam(const hypic_dims* dims, int32_t family, const void* q,
  * segment's chunks of 64 tokens from its start, of each chunk's largest
  * per-channel gate sum (a scale that keeps P_hat in float32 range); the tuple
  * (P_hat, log_decay, S_seg) composes with hypic_compose_segments unchanged.
- *   q, k, v, beta, cu_seqlens, o, S_seg  as in hypic_build_segment.
+ *   q, k, v, beta, n_tokens, cu_seqlens, o, S_seg  as in hypic_build_segment.
  *   gate      [T, h_v, d_k] float32: the per-channel log gates g_t (natural log).
  *   P_hat     [n_seg, h_v, d_k, d_k] float32 or NULL (no operator; then
  *             log_decay is not written).
@@ -282,8 +286,8 @@ int32_t hypic_family_seam(const hypic_dims* dims, int32_t family, const void* q,
  * longest-first order of more than 128 segments), as for the GDN build.
  */
 int32_t hypic_kda_build(const hypic_dims* dims, const void* q, const void* k, const void* v,
-                        const float* beta, const float* gate, const int32_t* cu_seqlens,
-                        const int32_t* cu_seqlens_host, int32_t n_seg, void* o, float* S_seg,
+                        const float* beta, const float* gate, int32_t n_tokens,
+                        const int32_t* cu_seqlens, const int32_t* cu_seqlens_host, int32_t n_seg, void* o, float* S_seg,
                         float* P_hat, float* log_decay, void* workspace, size_t workspace_bytes,
                         void* stream);
 

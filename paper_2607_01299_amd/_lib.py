@@ -84,7 +84,8 @@ def load():
     lib.hypic_status_str.argtypes = [_I32]
     lib.hypic_status_str.restype = ctypes.c_char_p
     lib.hypic_build_segment.argtypes = [
-        ctypes.POINTER(Dims), _P, _P, _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _P, _SZ, _P]
+        ctypes.POINTER(Dims), _P, _P, _P, _P, _P, _I32, _P, _P, _I32, _P, _P, _P, _P, _P, _SZ,
+        _P]
     lib.hypic_build_segment.restype = _I32
     lib.hypic_compose_segments.argtypes = [
         ctypes.POINTER(Dims), _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _SZ, _P]
@@ -94,7 +95,7 @@ def load():
         _P, _SZ, _P]
     lib.hypic_seam_rescan.restype = _I32
     lib.hypic_family_build.argtypes = [
-        ctypes.POINTER(Dims), _I32, _P, _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _SZ, _P]
+        ctypes.POINTER(Dims), _I32, _P, _P, _P, _P, _I32, _P, _P, _I32, _P, _P, _P, _P, _SZ, _P]
     lib.hypic_family_build.restype = _I32
     lib.hypic_family_compose.argtypes = [
         ctypes.POINTER(Dims), _I32, _P, _P, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _SZ, _P]
@@ -112,7 +113,8 @@ def load():
     lib.hypic_causal_conv.argtypes = [_I32, _I32, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _I32, _P]
     lib.hypic_causal_conv.restype = _I32
     lib.hypic_kda_build.argtypes = [
-        ctypes.POINTER(Dims), _P, _P, _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _P, _SZ, _P]
+        ctypes.POINTER(Dims), _P, _P, _P, _P, _P, _I32, _P, _P, _I32, _P, _P, _P, _P, _P, _SZ,
+        _P]
     lib.hypic_kda_build.restype = _I32
     lib.hypic_kda_seam.argtypes = [
         ctypes.POINTER(Dims), _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _I32, _P, _P, _P,

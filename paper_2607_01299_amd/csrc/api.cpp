@@ -33,6 +33,15 @@ int32_t check_dims(const hypic_dims* d) {
 
 int32_t hip_status(hipError_t e) { return e == hipSuccess ? HYPIC_OK : HYPIC_EHIP; }
 
+// Segment offsets of a build: 0 = cu[0] <= cu[1] <= ... <= cu[n_seg] <= n_tokens,
+// so every segment lies inside the packed token arrays.
+bool check_segment_offsets(const int32_t* cu_host, int32_t n_seg, int32_t n_tokens) {
+  if (cu_host[0] != 0) return false;
+  for (int32_t s = 0; s < n_seg; ++s)
+    if (cu_host[s + 1] < cu_host[s]) return false;
+  return cu_host[n_seg] <= n_tokens;
+}
+
 }  // namespace
 
 extern "C" {
@@ -57,21 +66,20 @@ size_t hypic_workspace_bytes(int32_t op, const hypic_dims* dims, int64_t n) {
 
 int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k,
                             const void* v, const float* beta, const float* log_alpha,
-                            const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                            int32_t n_tokens, const int32_t* cu_seqlens,
+                            const int32_t* cu_seqlens_host,
                             int32_t n_seg, void* o, float* S_seg, float* P_hat,
                             float* log_decay, void* workspace, size_t workspace_bytes,
                             void* stream) {
   int32_t st = check_dims(dims);
   if (st != HYPIC_OK) return st;
-  if (n_seg < 0) return HYPIC_EINVAL;
+  if (n_seg < 0 || n_tokens < 0) return HYPIC_EINVAL;
   if (n_seg == 0) return HYPIC_OK;
   if (!q || !k || !v || !beta || !log_alpha || !cu_seqlens || !cu_seqlens_host || !S_seg)
     return HYPIC_EINVAL;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || (o && !aligned16(o)))
     return HYPIC_EINVAL;
-  if (cu_seqlens_host[0] != 0) return HYPIC_EINVAL;
-  for (int32_t s = 0; s < n_seg; ++s)
-    if (cu_seqlens_host[s + 1] < cu_seqlens_host[s]) return HYPIC_EINVAL;
+  if (!check_segment_offsets(cu_seqlens_host, n_seg, n_tokens)) return HYPIC_EINVAL;
   const int64_t n_items = static_cast<int64_t>(n_seg) * dims->h_v * 4;
   if (n_items > 0x7fffffff) return HYPIC_EINVAL;
   const size_t need = hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg);
@@ -104,7 +112,7 @@ int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k
   a.h_qk = dims->h_qk;
   a.h_v = dims->h_v;
   a.group = dims->h_v / dims->h_qk;
-  a.n_tokens = cu_seqlens_host[n_seg];
+  a.n_tokens = n_tokens;
   a.mode = 0;
   a.n_roles = P_hat ? 2 : 1;
   a.cu_seqlens = cu_seqlens;
@@ -134,8 +142,12 @@ int32_t hypic_compose_segments(const hypic_dims* dims, const float* P_hat,
   for (int32_t r = 0; r < n_req; ++r)
     if (req_offsets_host[r + 1] < req_offsets_host[r]) return HYPIC_EINVAL;
   const int32_t nnz = req_offsets_host[n_req];
+  if (!aligned16(S_out) || (S_prefix && !aligned16(S_prefix)) ||
+      (S_incoming && !aligned16(S_incoming)))
+    return HYPIC_EINVAL;
   if (nnz > 0) {
     if (!P_hat || !log_decay || !S_seg || !seg_ids || !seg_ids_host) return HYPIC_EINVAL;
+    if (!aligned16(P_hat) || !aligned16(S_seg)) return HYPIC_EINVAL;
     for (int32_t j = 0; j < nnz; ++j)
       if (seg_ids_host[j] < 0 || seg_ids_host[j] >= n_pool) return HYPIC_EINVAL;
   }
@@ -209,20 +221,18 @@ int32_t hypic_seam_rescan(const hypic_dims* dims, const void* q, const void* k,
 // ---------------------------------------------------------------------------
 
 int32_t hypic_family_build(const hypic_dims* dims, int32_t family, const void* q,
-                           const void* k, const void* v, const float* gate,
+                           const void* k, const void* v, const float* gate, int32_t n_tokens,
                            const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
                            int32_t n_seg, void* o, float* S_seg, float* log_decay,
                            void* workspace, size_t workspace_bytes, void* stream) {
   int32_t st = check_dims(dims);
   if (st != HYPIC_OK) return st;
   if (family != HYPIC_FAMILY_SCALAR && family != HYPIC_FAMILY_DIAGONAL) return HYPIC_EUNSUPPORTED;
-  if (n_seg < 0) return HYPIC_EINVAL;
+  if (n_seg < 0 || n_tokens < 0) return HYPIC_EINVAL;
   if (n_seg == 0) return HYPIC_OK;
   if (!q || !k || !v || !gate || !cu_seqlens || !cu_seqlens_host || !S_seg) return HYPIC_EINVAL;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return HYPIC_EINVAL;
-  if (cu_seqlens_host[0] != 0) return HYPIC_EINVAL;
-  for (int32_t s = 0; s < n_seg; ++s)
-    if (cu_seqlens_host[s + 1] < cu_seqlens_host[s]) return HYPIC_EINVAL;
+  if (!check_segment_offsets(cu_seqlens_host, n_seg, n_tokens)) return HYPIC_EINVAL;
   if (static_cast<int64_t>(n_seg) * dims->h_v * 2 > 0x7fffffff) return HYPIC_EINVAL;
   const size_t need = hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return HYPIC_EWORKSPACE;
@@ -251,7 +261,7 @@ int32_t hypic_family_build(const hypic_dims* dims, int32_t family, const void* q
   a.h_qk = dims->h_qk;
   a.h_v = dims->h_v;
   a.group = dims->h_v / dims->h_qk;
-  a.n_tokens = cu_seqlens_host[n_seg];
+  a.n_tokens = n_tokens;
   a.mode = 0;
   a.cu_seqlens = cu_seqlens;
   a.o = o;
@@ -356,21 +366,19 @@ int32_t hypic_family_seam(const hypic_dims* dims, int32_t family, const void* q,
 // ---------------------------------------------------------------------------
 
 int32_t hypic_kda_build(const hypic_dims* dims, const void* q, const void* k, const void* v,
-                        const float* beta, const float* gate, const int32_t* cu_seqlens,
-                        const int32_t* cu_seqlens_host, int32_t n_seg, void* o, float* S_seg,
+                        const float* beta, const float* gate, int32_t n_tokens,
+                        const int32_t* cu_seqlens, const int32_t* cu_seqlens_host, int32_t n_seg, void* o, float* S_seg,
                         float* P_hat, float* log_decay, void* workspace, size_t workspace_bytes,
                         void* stream) {
   int32_t st = check_dims(dims);
   if (st != HYPIC_OK) return st;
-  if (n_seg < 0) return HYPIC_EINVAL;
+  if (n_seg < 0 || n_tokens < 0) return HYPIC_EINVAL;
   if (n_seg == 0) return HYPIC_OK;
   if (!q || !k || !v || !beta || !gate || !cu_seqlens || !cu_seqlens_host || !S_seg)
     return HYPIC_EINVAL;
   if (P_hat != nullptr && log_decay == nullptr) return HYPIC_EINVAL;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v)) return HYPIC_EINVAL;
-  if (cu_seqlens_host[0] != 0) return HYPIC_EINVAL;
-  for (int32_t s = 0; s < n_seg; ++s)
-    if (cu_seqlens_host[s + 1] < cu_seqlens_host[s]) return HYPIC_EINVAL;
+  if (!check_segment_offsets(cu_seqlens_host, n_seg, n_tokens)) return HYPIC_EINVAL;
   if (static_cast<int64_t>(n_seg) * dims->h_v * 2 > 0x7fffffff) return HYPIC_EINVAL;
   const size_t need = hypic_workspace_bytes(HYPIC_OP_BUILD, dims, n_seg);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return HYPIC_EWORKSPACE;
@@ -400,7 +408,7 @@ int32_t hypic_kda_build(const hypic_dims* dims, const void* q, const void* k, co
   a.h_qk = dims->h_qk;
   a.h_v = dims->h_v;
   a.group = dims->h_v / dims->h_qk;
-  a.n_tokens = cu_seqlens_host[n_seg];
+  a.n_tokens = n_tokens;
   a.mode = 0;
   a.cu_seqlens = cu_seqlens;
   a.o = o;

@@ -18,6 +18,7 @@ import ctypes
 import numpy as np
 import torch
 
+from . import _checks as C
 from . import _lib
 from ._lib import Dims
 
@@ -29,6 +30,26 @@ def _i32_pair(x, device):
 
 def _p(t):
     return ctypes.c_void_p(0 if t is None else t.data_ptr())
+
+
+def _check_tokens_against_pool(tokens, pool_dims, dev):
+    """Token arrays (q, k, v, beta, log_alpha) whose heads and widths match the
+    pool's (h_v, d_k, d_v) and whose per-token arrays are float32 [T, h_v]."""
+    q, k, v, beta, log_alpha = tokens
+    T, h_qk, h_v, d_k, d_v = C.token_arrays(q, k, v)
+    if (h_v, d_k, d_v) != tuple(pool_dims) or q.device != dev:
+        C.fail("token arrays (%d heads, %d x %d) do not match the pool (%d heads, %d x %d)"
+               % ((h_v, d_k, d_v) + tuple(pool_dims)))
+    C.per_token("beta", beta, T, h_v, dev)
+    C.per_token("log_alpha", log_alpha, T, h_v, dev)
+    return T
+
+
+def _check_csr(ids_h, off_h):
+    if len(off_h) < 1:
+        C.fail("req_offsets needs at least one value")
+    if int(off_h[-1]) != len(ids_h):
+        C.fail("req_offsets[-1] = %d but seg_ids holds %d ids" % (int(off_h[-1]), len(ids_h)))
 
 
 def _dtype_code(t):
@@ -44,8 +65,9 @@ class SegmentPipeline:
         self.device = dev
         self.stream = torch.cuda.current_stream(dev)
         sp = ctypes.c_void_p(self.stream.cuda_stream)
-        T, h_qk, d_k = q.shape
-        h_v, d_v = v.shape[1], v.shape[2]
+        T, h_qk, h_v, d_k, d_v = C.token_arrays(q, k, v)
+        C.per_token("beta", beta, T, h_v, dev)
+        C.per_token("log_alpha", log_alpha, T, h_v, dev)
         self.T, self.h_v, self.d_k, self.d_v = T, h_v, d_k, d_v
         self.dims = Dims(h_qk=h_qk, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_dtype_code(q), chunk=chunk)
         self.cdims = Dims(h_qk=h_v, h_v=h_v, d_k=d_k, d_v=d_v,
@@ -64,18 +86,20 @@ class SegmentPipeline:
                                                   n_seg)
         self.ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
         self._build_args = (
-            ctypes.byref(self.dims), _p(q), _p(k), _p(v), _p(beta), _p(log_alpha), _p(self.cu_d),
-            self.cu_h.ctypes.data_as(ctypes.c_void_p), n_seg, _p(self.o), _p(self.S_seg),
-            _p(self.P_hat), _p(self.log_decay), _p(self.ws), ws_bytes, sp)
+            ctypes.byref(self.dims), _p(q), _p(k), _p(v), _p(beta), _p(log_alpha), T,
+            _p(self.cu_d), self.cu_h.ctypes.data_as(ctypes.c_void_p), n_seg, _p(self.o),
+            _p(self.S_seg), _p(self.P_hat), _p(self.log_decay), _p(self.ws), ws_bytes, sp)
         # composition: one request of all segments in batch order by default
         if seg_ids is None:
             seg_ids = np.arange(n_seg, dtype=np.int32)
             req_offsets = np.array([0, n_seg], dtype=np.int32)
         self.ids_h, self.ids_d = _i32_pair(seg_ids, dev)
         self.off_h, self.off_d = _i32_pair(req_offsets, dev)
+        _check_csr(self.ids_h, self.off_h)
         n_req = len(self.off_h) - 1
         nnz = int(self.off_h[-1])
         self.n_req, self.nnz = n_req, nnz
+        C.state("S_prefix", S_prefix, n_req, h_v, d_k, d_v, dev)
         self.S_prefix = S_prefix
         self.S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=f32, device=dev)
         self.S_inc = torch.empty((nnz, h_v, d_k, d_v), dtype=f32, device=dev)
@@ -169,7 +193,8 @@ class ComposeBurst:
         dev = S_seg.device
         self.stream = torch.cuda.current_stream(dev)
         sp = ctypes.c_void_p(self.stream.cuda_stream)
-        n_pool, h_v, d_k, d_v = S_seg.shape
+        n_pool, h_v, d_k, d_v = C.pool(P_hat, log_decay, S_seg)
+        _check_tokens_against_pool(tokens, (h_v, d_k, d_v), dev)
         q, k, v, beta, log_alpha = tokens
         self.tokens = tokens
         self.pool = (P_hat, log_decay, S_seg)
@@ -180,8 +205,11 @@ class ComposeBurst:
                          chunk=chunk)
         self.ids_h, self.ids_d = _i32_pair(seg_ids, dev)
         self.off_h, self.off_d = _i32_pair(req_offsets, dev)
+        _check_csr(self.ids_h, self.off_h)
         n_req = len(self.off_h) - 1
         nnz = int(self.off_h[-1])
+        if len(tok_start) != nnz or len(tok_len) != nnz:
+            C.fail("tok_start and tok_len must hold one value per listed segment (%d)" % nnz)
         self.n_req, self.nnz, self.h_v, self.d_k, self.d_v = n_req, nnz, h_v, d_k, d_v
         f32 = torch.float32
         self.S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=f32, device=dev)
@@ -230,7 +258,8 @@ class SeamAdvanceBurst:
         self.lib = _lib.load()
         dev = S_seg.device
         self.stream = torch.cuda.current_stream(dev)
-        n_pool, h_v, d_k, d_v = S_seg.shape
+        n_pool, h_v, d_k, d_v = C.pool(P_hat, log_decay, S_seg)
+        _check_tokens_against_pool(tokens, (h_v, d_k, d_v), dev)
         q, k, v, beta, log_alpha = tokens
         self.tokens = tokens
         self.pool = (P_hat, log_decay, S_seg)
@@ -238,9 +267,13 @@ class SeamAdvanceBurst:
                          chunk=64)
         self.ss_h, self.ss_d = _i32_pair(seam_start, dev)
         self.sl_h, self.sl_d = _i32_pair(seam_len, dev)
+        if len(self.ss_h) != n_pool or len(self.sl_h) != n_pool:
+            C.fail("seam_start and seam_len must hold one value per pool entry (%d)" % n_pool)
         offs = np.asarray(req_offsets, dtype=np.int32)
+        _check_csr(np.asarray(seg_ids), offs)
         n_req = len(offs) - 1
-        nnz = int(offs[-1]) if n_req >= 0 else 0
+        nnz = int(offs[-1])
+        C.state("S_prefix", S_prefix, n_req, h_v, d_k, d_v, dev)
         self.n_req, self.nnz, self.h_v, self.d_k, self.d_v = n_req, nnz, h_v, d_k, d_v
         self.w = int(w)
         self.S_prefix = S_prefix
@@ -324,8 +357,8 @@ class FamilyPipeline:
         dev = q.device
         self.stream = torch.cuda.current_stream(dev)
         sp = ctypes.c_void_p(self.stream.cuda_stream)
-        T, h_qk, d_k = q.shape
-        h_v, d_v = v.shape[1], v.shape[2]
+        T, h_qk, h_v, d_k, d_v = C.token_arrays(q, k, v)
+        C.per_token("gate", gate, T, h_v, dev, None if family == "scalar" else d_k)
         self.T, self.h_v, self.d_k, self.d_v = T, h_v, d_k, d_v
         self.dims = Dims(h_qk=h_qk, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_dtype_code(q), chunk=64)
         self.cdims = Dims(h_qk=h_v, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_lib.HYPIC_F32, chunk=64)
@@ -342,7 +375,7 @@ class FamilyPipeline:
                                                   n_seg)
         self.ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
         self._build_args = (
-            ctypes.byref(self.dims), self.family, _p(q), _p(k), _p(v), _p(gate), _p(self.cu_d),
+            ctypes.byref(self.dims), self.family, _p(q), _p(k), _p(v), _p(gate), T, _p(self.cu_d),
             self.cu_h.ctypes.data_as(ctypes.c_void_p), n_seg, _p(self.o), _p(self.S_seg),
             _p(self.log_decay), _p(self.ws), ws_bytes, sp)
         if seg_ids is None:
@@ -350,9 +383,11 @@ class FamilyPipeline:
             req_offsets = np.array([0, n_seg], dtype=np.int32)
         self.ids_h, self.ids_d = _i32_pair(seg_ids, dev)
         self.off_h, self.off_d = _i32_pair(req_offsets, dev)
+        _check_csr(self.ids_h, self.off_h)
         n_req = len(self.off_h) - 1
         nnz = int(self.off_h[-1])
         self.n_req, self.nnz = n_req, nnz
+        C.state("S_prefix", S_prefix, n_req, h_v, d_k, d_v, dev)
         self.S_prefix = S_prefix
         self.S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=f32, device=dev)
         self.S_inc = torch.empty((nnz, h_v, d_k, d_v), dtype=f32, device=dev)
@@ -398,8 +433,9 @@ class KdaPipeline:
         dev = q.device
         self.stream = torch.cuda.current_stream(dev)
         sp = ctypes.c_void_p(self.stream.cuda_stream)
-        T, h_qk, d_k = q.shape
-        h_v, d_v = v.shape[1], v.shape[2]
+        T, h_qk, h_v, d_k, d_v = C.token_arrays(q, k, v)
+        C.per_token("beta", beta, T, h_v, dev)
+        C.per_token("gate", gate, T, h_v, dev, d_k)
         self.dims = Dims(h_qk=h_qk, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_dtype_code(q), chunk=64)
         self.inputs = (q, k, v, beta, gate)
         self.cu_h, self.cu_d = _i32_pair(cu_seqlens, dev)
@@ -415,7 +451,7 @@ class KdaPipeline:
                                                   n_seg)
         self.ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
         self._build_args = (
-            ctypes.byref(self.dims), _p(q), _p(k), _p(v), _p(beta), _p(gate), _p(self.cu_d),
+            ctypes.byref(self.dims), _p(q), _p(k), _p(v), _p(beta), _p(gate), T, _p(self.cu_d),
             self.cu_h.ctypes.data_as(ctypes.c_void_p), n_seg, _p(self.o), _p(self.S_seg),
             _p(self.P_hat), _p(self.log_decay), _p(self.ws), ws_bytes, sp)
 
@@ -434,11 +470,15 @@ class FamilyComposeBurst:
         dev = S_seg.device
         self.stream = torch.cuda.current_stream(dev)
         sp = ctypes.c_void_p(self.stream.cuda_stream)
-        n_pool, h_v, d_k, d_v = S_seg.shape
+        if not isinstance(S_seg, torch.Tensor) or S_seg.dim() != 4:
+            C.fail("S_seg must be a 4-d torch tensor")
+        n_pool, h_v, d_k, d_v = C.pool(None, log_decay, S_seg,
+                                       None if family == "scalar" else S_seg.shape[2])
         self.pool = (log_decay, S_seg)
         self.cdims = Dims(h_qk=h_v, h_v=h_v, d_k=d_k, d_v=d_v, dtype=_lib.HYPIC_F32, chunk=64)
         self.ids_h, self.ids_d = _i32_pair(seg_ids, dev)
         self.off_h, self.off_d = _i32_pair(req_offsets, dev)
+        _check_csr(self.ids_h, self.off_h)
         n_req = len(self.off_h) - 1
         nnz = int(self.off_h[-1])
         self.n_req, self.nnz, self.h_v, self.d_k, self.d_v = n_req, nnz, h_v, d_k, d_v

@@ -65,12 +65,13 @@ def test_workspace_sizes(lib):
 
 
 def _build(lib, dims, cu, n_seg=None, q=FAKE, S=FAKE, ws=FAKE, ws_bytes=1 << 20, o=FAKE,
-           cu_dev=FAKE):
+           cu_dev=FAKE, n_tokens=None):
     cu = np.asarray(cu, dtype=np.int32)
     n_seg = len(cu) - 1 if n_seg is None else n_seg
+    n_tokens = int(cu[-1]) if n_tokens is None else n_tokens
     return lib.hypic_build_segment(
-        ctypes.byref(dims) if dims is not None else None, q, FAKE, FAKE, FAKE, FAKE, cu_dev,
-        cu.ctypes.data_as(ctypes.c_void_p), n_seg, o, S, FAKE, FAKE, ws, ws_bytes, None)
+        ctypes.byref(dims) if dims is not None else None, q, FAKE, FAKE, FAKE, FAKE, n_tokens,
+        cu_dev, cu.ctypes.data_as(ctypes.c_void_p), n_seg, o, S, FAKE, FAKE, ws, ws_bytes, None)
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -104,13 +105,24 @@ def test_build_rejects_bad_arguments(lib):
     assert _build(lib, d, [0], n_seg=0) == _lib.HYPIC_OK
 
 
-def _compose(lib, dims, ids, offs, n_pool=8, S_out=FAKE, P=FAKE):
+def test_build_rejects_offsets_past_the_token_arrays(lib):
+    """The segments must lie inside the n_tokens rows of q, k, v (and o): an
+    offset past them is rejected on the host, before any launch."""
+    d = _dims()
+    assert _build(lib, d, [0, 10, 21], n_tokens=20) == _lib.HYPIC_EINVAL
+    assert _build(lib, d, [0, 10], n_tokens=-1) == _lib.HYPIC_EINVAL
+    assert _fbuild(lib, _lib.HYPIC_FAMILY_SCALAR, [0, 10, 21], n_tokens=20) == _lib.HYPIC_EINVAL
+    assert _kbuild(lib, [0, 10, 21], n_tokens=20) == _lib.HYPIC_EINVAL
+
+
+def _compose(lib, dims, ids, offs, n_pool=8, S_out=FAKE, P=FAKE, S_seg=FAKE, S_prefix=None,
+             S_inc=None):
     ids = np.asarray(ids, dtype=np.int32)
     offs = np.asarray(offs, dtype=np.int32)
     return lib.hypic_compose_segments(
-        ctypes.byref(dims), P, FAKE, FAKE, n_pool, FAKE, ids.ctypes.data_as(ctypes.c_void_p),
-        FAKE, offs.ctypes.data_as(ctypes.c_void_p), len(offs) - 1, None, S_out, None, None, 0,
-        None)
+        ctypes.byref(dims), P, FAKE, S_seg, n_pool, FAKE, ids.ctypes.data_as(ctypes.c_void_p),
+        FAKE, offs.ctypes.data_as(ctypes.c_void_p), len(offs) - 1, S_prefix, S_out, S_inc, None,
+        0, None)
 
 
 def test_compose_rejects_bad_arguments(lib):
@@ -123,6 +135,10 @@ def test_compose_rejects_bad_arguments(lib):
     assert _compose(lib, d, [0, 1], [0, 2], P=None) == _lib.HYPIC_EINVAL
     assert _compose(lib, _dims(d_k=32), [0], [0, 1]) == _lib.HYPIC_EUNSUPPORTED
     assert _compose(lib, d, [], [0]) == _lib.HYPIC_OK                  # no request
+    # the kernel reads and writes 16-byte pieces of every state and operator
+    for kw in (dict(P=FAKE_ODD), dict(S_seg=FAKE_ODD), dict(S_out=FAKE_ODD),
+               dict(S_prefix=FAKE_ODD), dict(S_inc=FAKE_ODD)):
+        assert _compose(lib, d, [0, 1], [0, 2], **kw) == _lib.HYPIC_EINVAL, kw
 
 
 def _seam(lib, dims, start, length, w=8, n_tokens=100, o=FAKE, S_in=FAKE):
@@ -153,12 +169,13 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
         _lib.load()
 
 
-def _fbuild(lib, family, cu, gate=FAKE, dims=None):
+def _fbuild(lib, family, cu, gate=FAKE, dims=None, n_tokens=None):
     cu = np.asarray(cu, dtype=np.int32)
     d = _dims() if dims is None else dims
+    n_tokens = int(cu[-1]) if n_tokens is None else n_tokens
     return lib.hypic_family_build(
-        ctypes.byref(d), family, FAKE, FAKE, FAKE, gate, FAKE, cu.ctypes.data_as(ctypes.c_void_p),
-        len(cu) - 1, FAKE, FAKE, FAKE, FAKE, 1 << 20, None)
+        ctypes.byref(d), family, FAKE, FAKE, FAKE, gate, n_tokens, FAKE,
+        cu.ctypes.data_as(ctypes.c_void_p), len(cu) - 1, FAKE, FAKE, FAKE, FAKE, 1 << 20, None)
 
 
 def _fcompose(lib, family, ids, offs, n_pool=8, S_out=FAKE, S_seg=FAKE):
@@ -202,12 +219,14 @@ def test_family_calls_reject_unknown_family(lib, family):
 
 
 def _kbuild(lib, cu, beta=FAKE, gate=FAKE, P_hat=FAKE, log_decay=FAKE, q=FAKE, dims=None,
-            ws_bytes=1 << 20):
+            ws_bytes=1 << 20, n_tokens=None):
     cu = np.asarray(cu, dtype=np.int32)
     d = _dims() if dims is None else dims
+    n_tokens = int(cu[-1]) if n_tokens is None else n_tokens
     return lib.hypic_kda_build(
-        ctypes.byref(d), q, FAKE, FAKE, beta, gate, FAKE, cu.ctypes.data_as(ctypes.c_void_p),
-        len(cu) - 1, FAKE, FAKE, P_hat, log_decay, FAKE, ws_bytes, None)
+        ctypes.byref(d), q, FAKE, FAKE, beta, gate, n_tokens, FAKE,
+        cu.ctypes.data_as(ctypes.c_void_p), len(cu) - 1, FAKE, FAKE, P_hat, log_decay, FAKE,
+        ws_bytes, None)
 
 
 def _kseam(lib, start, length, w=8, n_tokens=100, gate=FAKE, S_in=FAKE):

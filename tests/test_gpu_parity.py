@@ -328,6 +328,48 @@ def test_error_leaves_outputs_untouched(hy):
         hy.compose_segments(P, g, S, ids, offs)
 
 
+def test_build_rejects_offsets_past_the_tokens(hy):
+    """An offset past the n_tokens rows of q, k, v is rejected on the host: the
+    call returns HYPIC_EINVAL and enqueues nothing (pre-filled outputs keep
+    their values); the Python layer rejects mismatched tensors before the call."""
+    import ctypes
+    from paper_2607_01299_amd import _lib
+    _say("error path: cu_seqlens past the token arrays, mismatched tensors")
+    lib = _lib.load()
+    dev = "cuda"
+    T, d = 40, 64
+    q = torch.zeros(T, 1, d, device=dev, dtype=torch.bfloat16)
+    v = torch.zeros(T, 1, d, device=dev, dtype=torch.bfloat16)
+    beta = torch.zeros(T, 1, device=dev)
+    la = torch.zeros(T, 1, device=dev)
+    cu = np.array([0, 20, 48], dtype=np.int32)          # 48 > 40 rows
+    cu_d = torch.from_numpy(cu).to(dev)
+    o = torch.full((T, 1, d), 3.0, device=dev, dtype=torch.bfloat16)
+    S = torch.full((2, 1, d, d), 7.0, device=dev)
+    P = torch.full((2, 1, d, d), 7.0, device=dev)
+    ld = torch.full((2, 1), 7.0, device=dev)
+    dims = _lib.Dims(h_qk=1, h_v=1, d_k=d, d_v=d, dtype=_lib.HYPIC_BF16, chunk=64)
+    code = lib.hypic_build_segment(
+        ctypes.byref(dims), q.data_ptr(), q.data_ptr(), v.data_ptr(), beta.data_ptr(),
+        la.data_ptr(), T, cu_d.data_ptr(), cu.ctypes.data_as(ctypes.c_void_p), 2, o.data_ptr(),
+        S.data_ptr(), P.data_ptr(), ld.data_ptr(), None, 0, None)
+    torch.cuda.synchronize()
+    assert code == _lib.HYPIC_EINVAL
+    assert torch.all(o == 3.0) and torch.all(S == 7.0) and torch.all(P == 7.0)
+    assert torch.all(ld == 7.0)
+    with pytest.raises(hy.HypicError):
+        hy.build_segment(q, q, v, beta, la, cu)
+    ok = np.array([0, 20, 40], dtype=np.int32)
+    with pytest.raises(hy.HypicError):                  # bf16 beta
+        hy.build_segment(q, q, v, beta.to(torch.bfloat16), la, ok)
+    with pytest.raises(hy.HypicError):                  # float32 v next to bf16 q
+        hy.build_segment(q, q, v.float(), beta, la, ok)
+    with pytest.raises(hy.HypicError):                  # short incoming states
+        hy.seam_rescan(q, q, v, beta, la, [0, 20], [20, 20], 8, S[:1])
+    with pytest.raises(hy.HypicError):                  # short P_hat
+        hy.compose_segments(P[:1], ld, S, [0, 1], [0, 2])
+
+
 def test_chain_count_not_a_multiple_of_eight(hy):
     """21 chains x 2 column blocks: the first 16 chains take the XCD-grouped
     workgroup numbering, the last 5 the linear one; both must match the oracle."""
