@@ -38,6 +38,27 @@ def test_build_flops_are_the_chunk_products():
     assert bench.flop_per_token_head(128, 128, 64) == 245_760
 
 
+def test_build_flop_counts_the_gram_once_per_qk_head():
+    """Sec. 8(a): every v-head's chunk products, the K K^T and Q K^T Gram once
+    per q/k head of a grouped-head group.  Equal heads give the per-head count;
+    the long-context workload (16 q/k, 32 v heads, 131072 tokens) is 962 GFLOP."""
+    assert bench.build_flop(16384, 16, 16, 128, 128, 64) == 16384 * 16 * 245_760
+    C, d_k, d_v = 64, 128, 128
+    gram = 2 * (2 * C * C * d_k) // C          # K K^T and Q K^T per token of one q/k head
+    assert bench.gram_flop_per_token(d_k, C) == gram
+    full = bench.flop_per_token_head(d_k, d_v, C)
+    assert bench.build_flop(1, 16, 32, d_k, d_v, C) == 32 * (full - gram) + 16 * gram
+    assert abs(bench.build_flop(131072, 16, 32, 128, 128, 64) - 962.1e9) < 0.1e9
+
+
+def test_hbm_roofline_never_exceeds_the_counted_bytes():
+    """The reported HBM fraction divides the bytes the counters saw (when a record
+    exists) and never the larger algorithmic count of L2-served re-reads."""
+    r = bench.hbm_roofline(8e9, 1.0, None, "nothing")        # 8 GB in 1 ms, no record
+    assert abs(r["frac"] - 1.0) < 1e-12 and r["traffic"] is None
+    assert abs(r["frac_algorithmic"] - 1.0) < 1e-12
+
+
 def test_kda_flop_split_sums_to_the_build_count():
     for C, d_k, d_v in [(64, 128, 128), (64, 64, 128), (64, 128, 64)]:
         state, operator = bench.kda_flops(d_k, d_v, C)
