@@ -133,6 +133,29 @@ int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k
                             size_t workspace_bytes, void* stream);
 
 /*
+ * hypic_build_segment_noalloc -- hypic_build_segment for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.  Same arguments and results as
+ * hypic_build_segment without the workspace: the longest-first order of a
+ * build of more than 128 segments goes into a fixed device array of the
+ * library (one per GPU, HYPIC_NOALLOC_MAX_SEGMENTS int32 = 256 KiB, held until
+ * the process ends) instead.  Allocates nothing and calls no allocating
+ * routine.  n_seg > HYPIC_NOALLOC_MAX_SEGMENTS returns HYPIC_EWORKSPACE with
+ * nothing enqueued.  `stream` must belong to the current device.  Every call on
+ * a GPU shares that GPU's array: calls that overlap on one GPU (on different
+ * streams, or concurrent host threads) race on it and must be serialised by
+ * the caller; calls of up to 128 segments do not touch it.
+ */
+#define HYPIC_NOALLOC_MAX_SEGMENTS 65536
+int32_t hypic_build_segment_noalloc(const hypic_dims* dims, const void* q, const void* k,
+                                    const void* v, const float* beta,
+                                    const float* log_alpha, int32_t n_tokens,
+                                    const int32_t* cu_seqlens,
+                                    const int32_t* cu_seqlens_host, int32_t n_seg,
+                                    void* o, float* S_seg, float* P_hat,
+                                    float* log_decay, void* stream);
+
+/*
  * hypic_compose_segments -- Eq. (6): for each request r and v-head h, start
  * from S = S_prefix[r, h] (zero when S_prefix is NULL) and for each listed
  * segment i = seg_ids[j], j = req_offsets[r] .. req_offsets[r+1]-1 in order:

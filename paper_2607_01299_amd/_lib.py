@@ -40,7 +40,10 @@ EXPORTS = (
     "hypic_compose_with_seams",
     "hypic_kda_build",
     "hypic_kda_seam",
+    "hypic_build_segment_noalloc",
 )
+
+HYPIC_NOALLOC_MAX_SEGMENTS = 65536
 
 HYPIC_FAMILY_SCALAR = 1
 HYPIC_FAMILY_DIAGONAL = 2
@@ -87,6 +90,9 @@ def load():
         ctypes.POINTER(Dims), _P, _P, _P, _P, _P, _I32, _P, _P, _I32, _P, _P, _P, _P, _P, _SZ,
         _P]
     lib.hypic_build_segment.restype = _I32
+    lib.hypic_build_segment_noalloc.argtypes = [
+        ctypes.POINTER(Dims), _P, _P, _P, _P, _P, _I32, _P, _P, _I32, _P, _P, _P, _P, _P]
+    lib.hypic_build_segment_noalloc.restype = _I32
     lib.hypic_compose_segments.argtypes = [
         ctypes.POINTER(Dims), _P, _P, _P, _I32, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _SZ, _P]
     lib.hypic_compose_segments.restype = _I32

@@ -16,7 +16,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhypic.so")
 
 SOURCES = ["scan.hip", "scan_bf16.hip", "compose.hip", "family.hip", "kda.hip", "adjacent.hip",
-           "seam_advance.hip", "api.cpp"]
+           "seam_advance.hip", "noalloc.hip", "api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

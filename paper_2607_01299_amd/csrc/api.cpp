@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "../../include/hypic.h"
+#include "api_impl.hpp"
 #include "family.hpp"
 #include "kda.hpp"
 #include "scan.hpp"
@@ -71,6 +72,24 @@ int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k
                             int32_t n_seg, void* o, float* S_seg, float* P_hat,
                             float* log_decay, void* workspace, size_t workspace_bytes,
                             void* stream) {
+  return hypic::build_segment_impl(dims, q, k, v, beta, log_alpha, n_tokens, cu_seqlens,
+                                   cu_seqlens_host, n_seg, o, S_seg, P_hat, log_decay,
+                                   workspace, workspace_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace hypic {
+
+// The segment build behind hypic_build_segment and hypic_build_segment_noalloc:
+// host validation, then the longest-first order (in the kernel arguments, or
+// on the device into `workspace`) and the scan launch.
+int32_t build_segment_impl(const hypic_dims* dims, const void* q, const void* k,
+                           const void* v, const float* beta, const float* log_alpha,
+                           int32_t n_tokens, const int32_t* cu_seqlens,
+                           const int32_t* cu_seqlens_host, int32_t n_seg, void* o,
+                           float* S_seg, float* P_hat, float* log_decay, void* workspace,
+                           size_t workspace_bytes, void* stream) {
   int32_t st = check_dims(dims);
   if (st != HYPIC_OK) return st;
   if (n_seg < 0 || n_tokens < 0) return HYPIC_EINVAL;
@@ -123,6 +142,10 @@ int32_t hypic_build_segment(const hypic_dims* dims, const void* q, const void* k
   return hip_status(hypic::launch_scan(a, dims->dtype == HYPIC_BF16, dims->d_k, dims->d_v,
                                        dims->chunk, n_seg, s));
 }
+
+}  // namespace hypic
+
+extern "C" {
 
 int32_t hypic_compose_segments(const hypic_dims* dims, const float* P_hat,
                                const float* log_decay, const float* S_seg, int32_t n_pool,

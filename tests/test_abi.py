@@ -105,6 +105,19 @@ def test_build_rejects_bad_arguments(lib):
     assert _build(lib, d, [0], n_seg=0) == _lib.HYPIC_OK
 
 
+def test_noalloc_build_rejects_more_segments_than_its_scratch(lib):
+    """The no-allocation build holds at most HYPIC_NOALLOC_MAX_SEGMENTS orders;
+    beyond that it returns HYPIC_EWORKSPACE before touching the GPU."""
+    d = _dims()
+    n = _lib.HYPIC_NOALLOC_MAX_SEGMENTS + 1
+    cu = np.arange(n + 1, dtype=np.int32)
+    code = lib.hypic_build_segment_noalloc(
+        ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, n, FAKE,
+        cu.ctypes.data_as(ctypes.c_void_p), n, FAKE, FAKE, FAKE, FAKE, None)
+    assert code == _lib.HYPIC_EWORKSPACE
+    assert "HYPIC_NOALLOC_MAX_SEGMENTS 65536" in open(HEADER).read()
+
+
 def test_build_rejects_offsets_past_the_token_arrays(lib):
     """The segments must lie inside the n_tokens rows of q, k, v (and o): an
     offset past them is rejected on the host, before any launch."""
