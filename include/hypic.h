@@ -78,7 +78,8 @@ typedef enum hypic_dtype { HYPIC_F32 = 0, HYPIC_BF16 = 1 } hypic_dtype;
 typedef enum hypic_op {
   HYPIC_OP_BUILD = 0,
   HYPIC_OP_COMPOSE = 1,
-  HYPIC_OP_SEAM = 2
+  HYPIC_OP_SEAM = 2,
+  HYPIC_OP_COMPOSE_RESCAN = 3
 } hypic_op;
 
 typedef struct hypic_dims {
@@ -91,7 +92,7 @@ typedef struct hypic_dims {
 } hypic_dims;
 
 /* Bytes of device workspace `op` needs for `n` items (segments for BUILD,
- * requests for COMPOSE, entries for SEAM).  Returns 0 when none is needed, and
+ * requests for COMPOSE and COMPOSE_RESCAN, entries for SEAM).  Returns 0 when none is needed, and
  * 0 as well for invalid dims (the operation itself then reports the error). */
 size_t hypic_workspace_bytes(int32_t op, const hypic_dims* dims, int64_t n);
 
@@ -357,12 +358,48 @@ int32_t hypic_kda_seam(const hypic_dims* dims, const void* q, const void* k, con
  *              states per request and the per-step entry lists.
  * dims->dtype gives the token type and the composition arithmetic as in
  * hypic_seam_rescan and hypic_compose_segments.  Requests run longest first
- * (Eq. (9) list order); each step enqueues one seam and one composition launch
- * over the requests still running.
+ * (Eq. (9) list order).  With bf16 tokens, chunk 64 and w <= 64 the call is one
+ * launch in which each (request, head) keeps its running state on chip across
+ * its entries (seam, then Eq. (4) with the entry's tail tuple); otherwise each
+ * step enqueues one seam and one composition launch over the requests still
+ * running.
  */
 size_t hypic_seam_compose_workspace_bytes(const hypic_dims* dims, int32_t n_req,
                                           int32_t max_per_request);
 int32_t hypic_compose_with_seams(const hypic_dims* dims, const float* P_hat,
+                                 const float* log_decay, const float* S_seg, int32_t n_pool,
+                                 const void* q, const void* k, const void* v, const float* beta,
+                                 const float* log_alpha, int32_t n_tokens,
+                                 const int32_t* seam_start, const int32_t* seam_start_host,
+                                 const int32_t* seam_len, const int32_t* seam_len_host, int32_t w,
+                                 const int32_t* seg_ids, const int32_t* seg_ids_host,
+                                 const int32_t* req_offsets, const int32_t* req_offsets_host,
+                                 int32_t n_req, const float* S_prefix, float* S_out,
+                                 void* o_seam, void* workspace, size_t workspace_bytes,
+                                 void* stream);
+
+/*
+ * hypic_compose_and_rescan -- Eq. (6) composition with each listed segment's
+ * seam window rescanned from the state entering it, in one pass (Sec. 4.3;
+ * the cached tuples cover whole segments and the seam does not advance the
+ * composed state).  For each request r and v-head h, from S = S_prefix[r, h]
+ * (zero when NULL), each listed entry i = seg_ids[j] in order does
+ *     o_seam[j, 0 .. w_i - 1, h] = outputs of the recurrence of Eq. (2) over
+ *                                  the entry's first w_i tokens from S;
+ *     S <- exp(log_decay[i, h]) * P_hat[i, h] @ S + S_seg[i, h]        (Eq. (4))
+ * then S_out[r, h] = S: the results of hypic_compose_segments (S_out) and of
+ * hypic_seam_rescan on its incoming states (o_seam), without writing or
+ * reading the incoming states.  Each (request, head) keeps its state on chip.
+ *   Arguments as in hypic_compose_with_seams, except that the pool holds
+ *   whole-segment tuples and seam_start / seam_len give each pool entry's
+ *   first token and length (w_i = min(w, seam_len[i])).
+ *   Requires bf16 tokens (dims->dtype == HYPIC_BF16, split-bf16 composition),
+ *   chunk 64 and w <= 64, else HYPIC_EUNSUPPORTED.
+ *   workspace  hypic_workspace_bytes(HYPIC_OP_COMPOSE_RESCAN, dims, n_req) bytes:
+ *              0 up to 128 requests (their longest-first order travels in the
+ *              kernel arguments), else the order, computed on the device.
+ */
+int32_t hypic_compose_and_rescan(const hypic_dims* dims, const float* P_hat,
                                  const float* log_decay, const float* S_seg, int32_t n_pool,
                                  const void* q, const void* k, const void* v, const float* beta,
                                  const float* log_alpha, int32_t n_tokens,

@@ -11,7 +11,7 @@ def __getattr__(name):
     # library loader stay importable without it
     if name in ("build_segment", "compose_segments", "seam_rescan", "make_dims",
                 "family_build", "family_compose", "family_seam", "rope_shift_state",
-                "rope_rerotate_keys", "causal_conv", "compose_with_seams", "kda_build",
+                "rope_rerotate_keys", "causal_conv", "compose_with_seams", "compose_and_rescan", "kda_build",
                 "kda_seam"):
         from . import ops
         return getattr(ops, name)

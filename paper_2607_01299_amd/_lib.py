@@ -23,6 +23,7 @@ HYPIC_BF16 = 1
 HYPIC_OP_BUILD = 0
 HYPIC_OP_COMPOSE = 1
 HYPIC_OP_SEAM = 2
+HYPIC_OP_COMPOSE_RESCAN = 3
 
 EXPORTS = (
     "hypic_workspace_bytes",
@@ -41,6 +42,7 @@ EXPORTS = (
     "hypic_kda_build",
     "hypic_kda_seam",
     "hypic_build_segment_noalloc",
+    "hypic_compose_and_rescan",
 )
 
 HYPIC_NOALLOC_MAX_SEGMENTS = 65536
@@ -132,6 +134,8 @@ def load():
         ctypes.POINTER(Dims), _P, _P, _P, _I32, _P, _P, _P, _P, _P, _I32, _P, _P, _P, _P, _I32,
         _P, _P, _P, _P, _I32, _P, _P, _P, _P, _SZ, _P]
     lib.hypic_compose_with_seams.restype = _I32
+    lib.hypic_compose_and_rescan.argtypes = lib.hypic_compose_with_seams.argtypes
+    lib.hypic_compose_and_rescan.restype = _I32
     _lib = lib
     return lib
 

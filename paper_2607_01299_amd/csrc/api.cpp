@@ -60,7 +60,7 @@ const char* hypic_status_str(int32_t status) {
 
 size_t hypic_workspace_bytes(int32_t op, const hypic_dims* dims, int64_t n) {
   if (check_dims(dims) != HYPIC_OK || n <= 0) return 0;
-  if (op == HYPIC_OP_BUILD && n > hypic::kInlineOrder)
+  if ((op == HYPIC_OP_BUILD || op == HYPIC_OP_COMPOSE_RESCAN) && n > hypic::kInlineOrder)
     return round_up(static_cast<size_t>(n) * sizeof(int32_t));
   return 0;
 }
@@ -511,23 +511,19 @@ SeamComposeLayout seam_compose_layout(const hypic_dims* d, int64_t n_req, int64_
 
 }  // namespace
 
-size_t hypic_seam_compose_workspace_bytes(const hypic_dims* dims, int32_t n_req,
-                                          int32_t max_per_request) {
-  if (check_dims(dims) != HYPIC_OK || n_req <= 0 || max_per_request < 0) return 0;
-  return seam_compose_layout(dims, n_req, max_per_request).total;
-}
+namespace {
 
-int32_t hypic_compose_with_seams(const hypic_dims* dims, const float* P_hat,
-                                 const float* log_decay, const float* S_seg, int32_t n_pool,
-                                 const void* q, const void* k, const void* v, const float* beta,
-                                 const float* log_alpha, int32_t n_tokens,
-                                 const int32_t* seam_start, const int32_t* seam_start_host,
-                                 const int32_t* seam_len, const int32_t* seam_len_host, int32_t w,
-                                 const int32_t* seg_ids, const int32_t* seg_ids_host,
-                                 const int32_t* req_offsets, const int32_t* req_offsets_host,
-                                 int32_t n_req, const float* S_prefix, float* S_out,
-                                 void* o_seam, void* workspace, size_t workspace_bytes,
-                                 void* stream) {
+// Host validation shared by the two seam-composition calls; max_n gets the
+// longest request's entry count.
+int32_t check_seam_compose(const hypic_dims* dims, const float* P_hat, const float* log_decay,
+                           const float* S_seg, int32_t n_pool, const void* q, const void* k,
+                           const void* v, const float* beta, const float* log_alpha,
+                           int32_t n_tokens, const int32_t* seam_start,
+                           const int32_t* seam_start_host, const int32_t* seam_len,
+                           const int32_t* seam_len_host, int32_t w, const int32_t* seg_ids,
+                           const int32_t* seg_ids_host, const int32_t* req_offsets,
+                           const int32_t* req_offsets_host, int32_t n_req,
+                           const float* S_prefix, float* S_out, void* o_seam, int32_t* max_n_out) {
   int32_t st = check_dims(dims);
   if (st != HYPIC_OK) return st;
   if (n_req < 0 || n_pool < 0 || n_tokens < 0 || w < 1) return HYPIC_EINVAL;
@@ -547,7 +543,9 @@ int32_t hypic_compose_with_seams(const hypic_dims* dims, const float* P_hat,
     if (!P_hat || !log_decay || !S_seg || !seg_ids || !seg_ids_host || !q || !k || !v || !beta ||
         !log_alpha || !seam_start || !seam_start_host || !seam_len || !seam_len_host || !o_seam)
       return HYPIC_EINVAL;
-    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o_seam)) return HYPIC_EINVAL;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o_seam) ||
+        !aligned16(P_hat) || !aligned16(S_seg))
+      return HYPIC_EINVAL;
     for (int32_t j = 0; j < nnz; ++j)
       if (seg_ids_host[j] < 0 || seg_ids_host[j] >= n_pool) return HYPIC_EINVAL;
     for (int32_t i = 0; i < n_pool; ++i) {
@@ -559,11 +557,105 @@ int32_t hypic_compose_with_seams(const hypic_dims* dims, const float* P_hat,
   if (static_cast<int64_t>(n_req) * dims->h_v * 4 > 0x7fffffff ||
       static_cast<int64_t>(max_n) * n_req > 0x7fffffff)
     return HYPIC_EINVAL;
+  *max_n_out = max_n;
+  return HYPIC_OK;
+}
+
+// The one-pass composition with seams runs on the bf16 chunk-64 scan: bf16
+// tokens, chunk 64, a seam of at most one chunk.
+bool fusable(const hypic_dims* dims, int32_t w) {
+  return dims->dtype == HYPIC_BF16 && dims->chunk == 64 && w <= 64;
+}
+
+// One launch: requests longest first (Eq. (9) list order, ties by index; in
+// the kernel arguments up to kInlineOrder requests, else on the device into
+// order_ws), one workgroup per (request, head).
+int32_t launch_fused(const hypic_dims* dims, const float* P_hat, const float* log_decay,
+                     const float* S_seg, const void* q, const void* k, const void* v,
+                     const float* beta, const float* log_alpha, int32_t n_tokens,
+                     const int32_t* seam_start, const int32_t* seam_len, int32_t w,
+                     const int32_t* seg_ids, const int32_t* req_offsets,
+                     const int32_t* req_offsets_host, int32_t n_req, const float* S_prefix,
+                     float* S_out, void* o_seam, int32_t advance, int32_t* order_ws,
+                     hipStream_t s) {
+  hypic::ScanArgs a{};
+  if (n_req <= hypic::kInlineOrder) {
+    int32_t idx[hypic::kInlineOrder];
+    for (int32_t i = 0; i < n_req; ++i) idx[i] = i;
+    std::stable_sort(idx, idx + n_req, [&](int32_t x, int32_t y) {
+      return req_offsets_host[x + 1] - req_offsets_host[x] >
+             req_offsets_host[y + 1] - req_offsets_host[y];
+    });
+    for (int32_t i = 0; i < n_req; ++i) a.order_inline[i] = static_cast<uint16_t>(idx[i]);
+    a.n_inline = n_req;
+  } else {
+    const int32_t st = hip_status(hypic::launch_lpt_order(req_offsets, n_req, order_ws, s));
+    if (st != HYPIC_OK) return st;
+    a.order = order_ws;
+  }
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.beta = beta;
+  a.log_alpha = log_alpha;
+  a.h_qk = dims->h_qk;
+  a.h_v = dims->h_v;
+  a.group = dims->h_v / dims->h_qk;
+  a.n_tokens = n_tokens;
+  a.mode = 2;
+  a.n_roles = 1;
+  a.tok_start = seam_start;
+  a.tok_len = seam_len;
+  a.w = w;
+  a.o = o_seam;
+  a.seg_ids = seg_ids;
+  a.req_offsets = req_offsets;
+  a.pool_P = P_hat;
+  a.pool_ld = log_decay;
+  a.pool_S = S_seg;
+  a.S_prefix = S_prefix;
+  a.S_final = S_out;
+  a.advance = advance;
+  return hip_status(hypic::launch_seam_compose_fused(a, dims->d_k, dims->d_v, n_req, s));
+}
+
+}  // namespace
+
+size_t hypic_seam_compose_workspace_bytes(const hypic_dims* dims, int32_t n_req,
+                                          int32_t max_per_request) {
+  if (check_dims(dims) != HYPIC_OK || n_req <= 0 || max_per_request < 0) return 0;
+  return seam_compose_layout(dims, n_req, max_per_request).total;
+}
+
+int32_t hypic_compose_with_seams(const hypic_dims* dims, const float* P_hat,
+                                 const float* log_decay, const float* S_seg, int32_t n_pool,
+                                 const void* q, const void* k, const void* v, const float* beta,
+                                 const float* log_alpha, int32_t n_tokens,
+                                 const int32_t* seam_start, const int32_t* seam_start_host,
+                                 const int32_t* seam_len, const int32_t* seam_len_host, int32_t w,
+                                 const int32_t* seg_ids, const int32_t* seg_ids_host,
+                                 const int32_t* req_offsets, const int32_t* req_offsets_host,
+                                 int32_t n_req, const float* S_prefix, float* S_out,
+                                 void* o_seam, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  int32_t max_n = 0;
+  int32_t st = check_seam_compose(dims, P_hat, log_decay, S_seg, n_pool, q, k, v, beta,
+                                  log_alpha, n_tokens, seam_start, seam_start_host, seam_len,
+                                  seam_len_host, w, seg_ids, seg_ids_host, req_offsets,
+                                  req_offsets_host, n_req, S_prefix, S_out, o_seam, &max_n);
+  if (st != HYPIC_OK || n_req == 0) return st;
   const SeamComposeLayout l = seam_compose_layout(dims, n_req, max_n);
   if (workspace == nullptr || workspace_bytes < l.total) return HYPIC_EWORKSPACE;
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   unsigned char* ws = static_cast<unsigned char*>(workspace);
+  if (fusable(dims, w)) {
+    // one pass: each (request, head) keeps its running state on chip across
+    // its entries (seam, then the tail tuple)
+    return launch_fused(dims, P_hat, log_decay, S_seg, q, k, v, beta, log_alpha, n_tokens,
+                        seam_start, seam_len, w, seg_ids, req_offsets, req_offsets_host, n_req,
+                        S_prefix, S_out, o_seam, 1, reinterpret_cast<int32_t*>(ws + l.order), s);
+  }
   const long state_floats = static_cast<long>(dims->h_v) * dims->d_k * dims->d_v;
   float* cur = reinterpret_cast<float*>(ws + l.states);
   float* tmp = cur + static_cast<long>(n_req) * state_floats;
@@ -626,6 +718,32 @@ int32_t hypic_compose_with_seams(const hypic_dims* dims, const float* P_hat,
   if (st == HYPIC_OK)
     st = hip_status(hypic::launch_permute_states(cur, S_out, order, n_req, state_floats, 1, s));
   return st;
+}
+
+int32_t hypic_compose_and_rescan(const hypic_dims* dims, const float* P_hat,
+                                 const float* log_decay, const float* S_seg, int32_t n_pool,
+                                 const void* q, const void* k, const void* v, const float* beta,
+                                 const float* log_alpha, int32_t n_tokens,
+                                 const int32_t* seam_start, const int32_t* seam_start_host,
+                                 const int32_t* seam_len, const int32_t* seam_len_host, int32_t w,
+                                 const int32_t* seg_ids, const int32_t* seg_ids_host,
+                                 const int32_t* req_offsets, const int32_t* req_offsets_host,
+                                 int32_t n_req, const float* S_prefix, float* S_out,
+                                 void* o_seam, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  int32_t max_n = 0;
+  int32_t st = check_seam_compose(dims, P_hat, log_decay, S_seg, n_pool, q, k, v, beta,
+                                  log_alpha, n_tokens, seam_start, seam_start_host, seam_len,
+                                  seam_len_host, w, seg_ids, seg_ids_host, req_offsets,
+                                  req_offsets_host, n_req, S_prefix, S_out, o_seam, &max_n);
+  if (st != HYPIC_OK || n_req == 0) return st;
+  if (!fusable(dims, w)) return HYPIC_EUNSUPPORTED;
+  const size_t need = hypic_workspace_bytes(HYPIC_OP_COMPOSE_RESCAN, dims, n_req);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return HYPIC_EWORKSPACE;
+  return launch_fused(dims, P_hat, log_decay, S_seg, q, k, v, beta, log_alpha, n_tokens,
+                      seam_start, seam_len, w, seg_ids, req_offsets, req_offsets_host, n_req,
+                      S_prefix, S_out, o_seam, 0, static_cast<int32_t*>(workspace),
+                      static_cast<hipStream_t>(stream));
 }
 
 // ---------------------------------------------------------------------------

@@ -37,6 +37,19 @@ struct ScanArgs {
   int32_t n_inline;          // build: > 0 when the order is held in order_inline
   uint16_t order_inline[kInlineOrder];
   const int32_t* out_entry;  // seam: output entry of each entry (NULL: the same)
+  // mode 2, composition with seams in one pass: a chain is one (request, head);
+  // chunk c is the request's c-th listed pool entry, whose seam tokens are
+  // tok_start[i], min(w, tok_len[i]) with i = seg_ids[req_offsets[r] + c]; after
+  // the seam the state composes with that entry's tuple.  The request order
+  // (longest first) is held in order / order_inline.
+  const int32_t* seg_ids;      // [nnz] pool entry of each listed segment
+  const int32_t* req_offsets;  // [n_req + 1] CSR offsets
+  const float* pool_P;         // [n_pool, h_v, d_k, d_k]
+  const float* pool_ld;        // [n_pool, h_v]
+  const float* pool_S;         // [n_pool, h_v, d_k, d_v]
+  const float* S_prefix;       // [n_req, h_v, d_k, d_v] or NULL (zero)
+  float* S_final;              // [n_req, h_v, d_k, d_v]
+  int32_t advance;             // 1: the seam advances the state (Sec. 4.3); 0: it does not
 };
 
 // Entry of the seam output o[n, w, h_v, d_v] that seam entry e writes.
@@ -69,6 +82,10 @@ hipError_t launch_scan(const ScanArgs& a, int bf16, int d_k, int d_v, int chunk,
 // Workgroups per (chain, head) of the bf16 chunk-64 scan.
 int scan_bf16_items_per_head(int d_k, int d_v, int with_operator);
 hipError_t launch_scan_bf16(const ScanArgs& a, int d_k, int d_v, int n_items, hipStream_t s);
+// Mode 2 (bf16 tokens, seam w <= 64, no operator): one workgroup per (request,
+// head), n_req x h_v workgroups.
+hipError_t launch_seam_compose_fused(const ScanArgs& a, int d_k, int d_v, int n_req,
+                                     hipStream_t s);
 hipError_t launch_compose(const ComposeArgs& a, int f32, int d_k, int d_v, int n_req,
                           hipStream_t s);
 

@@ -221,11 +221,16 @@ struct Chain {
   int e0, w, n_tok;
   const int32_t* tok_start;
   const int32_t* tok_len;
+  const int32_t* ids;  // fused composition: pool entry of listed segment e0 + c
 };
 
+// token range of seam entry e0 + c (through the request's pool ids when fused)
+__device__ __forceinline__ int entry_of(const Chain& ch, int c) {
+  return ch.ids != nullptr ? ch.ids[ch.e0 + c] : ch.e0 + c;
+}
 __device__ __forceinline__ int chunk_start(const Chain& ch, int c) {
   if (!ch.batched) return ch.lo + c * C;
-  const int t = ch.tok_start[ch.e0 + c];
+  const int t = ch.tok_start[entry_of(ch, c)];
   return (t < 0) ? 0 : ((t >= ch.n_tok) ? ch.n_tok - 1 : t);
 }
 __device__ __forceinline__ int chunk_len(const Chain& ch, int c) {
@@ -234,7 +239,7 @@ __device__ __forceinline__ int chunk_len(const Chain& ch, int c) {
     return (r < C) ? r : C;
   }
   const int t = chunk_start(ch, c);
-  const int l = ch.tok_len[ch.e0 + c];
+  const int l = ch.tok_len[entry_of(ch, c)];
   int n = (l < ch.w) ? l : ch.w;
   n = (n > ch.n_tok - t) ? ch.n_tok - t : n;
   return (n < 1) ? 1 : n;
@@ -758,7 +763,53 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
 // =============================================================================
 // waves 0-3: the chain update of chunk c
 // =============================================================================
+
+// One Eq. (4) step of a state wave's 32 columns (all d_k rows, order rho):
+// S <- exp(g) P S + S_i.  The A operand streams P's rows from HBM in float32:
+// lane (g2, r) of step u needs true row rho^-1(32 m + r), true columns
+// 16 u + 8 g2 .. +7 (the slot order of a state B fragment maps back to 8
+// contiguous columns), split into bf16 hi + lo; the B operand is exp(g) S from
+// the accumulators, split likewise; three passes; the accumulators start from
+// S_i, so no extra pass adds it.
 template <int DK, int DV>
+__device__ __forceinline__ void compose_entry(f32x16 (&st)[DK / 32], const float* P,
+                                              const float* Si, float e, int col0, int lane) {
+  constexpr int NM = DK / 32, NU = DK / 16;
+  const int g2 = lane >> 5, n32 = lane & 31;
+  f32x16 acc[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int x = 0; x < 16; ++x) acc[m][x] = Si[true_row(m, x, g2) * DV + col0 + n32];
+  const int prow = (n32 & ~12) | ((n32 & 4) << 1) | ((n32 & 8) >> 1);  // rho -> true row
+  const float* pr = P + prow * DK + 8 * g2;
+#pragma unroll
+  for (int u = 0; u < NU; ++u) {
+    bf16x8 bh, bl;
+    {
+      f32x16 es = st[u >> 1] * e;
+      split_of(es, u & 1, bh, bl);
+    }
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      const float* src = pr + (32 * m) * DK + 16 * u;
+      const float4 a0 = *reinterpret_cast<const float4*>(src);
+      const float4 a1 = *reinterpret_cast<const float4*>(src + 4);
+      f32x16 a;
+      a[0] = a0.x; a[1] = a0.y; a[2] = a0.z; a[3] = a0.w;
+      a[4] = a1.x; a[5] = a1.y; a[6] = a1.z; a[7] = a1.w;
+      bf16x8 ah, al;
+      split_of(a, 0, ah, al);
+      acc[m] = mma32(ah, bh, acc[m]);
+      acc[m] = mma32(ah, bl, acc[m]);
+      acc[m] = mma32(al, bh, acc[m]);
+    }
+  }
+#pragma unroll
+  for (int m = 0; m < NM; ++m) st[m] = acc[m];
+}
+
+template <int DK, int DV, bool FUSED>
 __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch,
                                            unsigned char* smem, int lane, int col0, int wslot) {
   using LP = Lds<DK>;
@@ -775,8 +826,9 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
   f32x16 st[NM];
 #pragma unroll
   for (int m = 0; m < NM; ++m) st[m] = zero16();
-  if (args.mode == 1) {
-    const float* s_in = args.S_in + ch.sh * DK * DV + col0 + n32;
+  const float* s_first = FUSED ? args.S_prefix : (args.mode == 1 ? args.S_in : nullptr);
+  if (s_first != nullptr) {
+    const float* s_in = s_first + ch.sh * DK * DV + col0 + n32;
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
@@ -901,7 +953,9 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
       }
     }
     lds_barrier();
-    if (active) {
+    // the seam advances the state, except in a fused composition that reads
+    // the seam from the incoming state only
+    if (active && (!FUSED || args.advance)) {
       const u16* fKt = reinterpret_cast<const u16*>(smem + LP::O_KT + par * LP::NKT * LP::FB);
       const float b_last = gb[C - 1];  // log2 units
       log_decay += b_last * 0.693147180559945309f;
@@ -914,7 +968,15 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
         st[m] = acc;
       }
     }
-    if (active && ch.batched) {
+    if constexpr (FUSED) {
+      // Eq. (4) with the listed segment's tuple
+      if (active) {
+        const long ih = static_cast<long>(entry_of(ch, c)) * args.h_v + ch.h;
+        const float e = __expf(args.pool_ld[ih]);
+        compose_entry<DK, DV>(st, args.pool_P + ih * DK * DK, args.pool_S + ih * DK * DV, e,
+                              col0, lane);
+      }
+    } else if (active && ch.batched) {
       // one seam entry per chunk: its state after the seam, then the state
       // entering the next entry
       const long eh = static_cast<long>(ch.e0 + c) * args.h_v + ch.h;
@@ -944,8 +1006,9 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
     lds_barrier();
   }
 
-  if (args.S_out != nullptr && !ch.batched) {
-    float* so = args.S_out + ch.sh * DK * DV + col0 + n32;
+  float* s_last = FUSED ? args.S_final : (ch.batched ? nullptr : args.S_out);
+  if (s_last != nullptr) {
+    float* so = s_last + ch.sh * DK * DV + col0 + n32;
 #pragma unroll
     for (int m = 0; m < NM; ++m)
 #pragma unroll
@@ -1035,7 +1098,8 @@ __device__ __forceinline__ void idle_wave(const Chain& ch, unsigned char* smem, 
   }
 }
 
-template <int DK, int DV>
+// FUSED: mode 2, composition with seams (no operator columns)
+template <int DK, int DV, bool FUSED>
 __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   extern __shared__ __align__(16) unsigned char smem[];
   const int tid = threadIdx.x;
@@ -1071,7 +1135,16 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   ch.tok_start = args.tok_start;
   ch.tok_len = args.tok_len;
   ch.e0 = 0;
-  if (args.mode == 0) {
+  ch.ids = nullptr;
+  if (FUSED) {
+    // one (request, head): the request's listed segments, one seam each
+    const int r = segment_of_rank(args, rank);
+    ch.batched = true;
+    ch.ids = args.seg_ids;
+    ch.e0 = args.req_offsets[r];
+    ch.seg = r;
+    lo = hi = 0;
+  } else if (args.mode == 0) {
     ch.seg = segment_of_rank(args, rank);
     lo = args.cu_seqlens[ch.seg];
     hi = args.cu_seqlens[ch.seg + 1];
@@ -1089,7 +1162,9 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   hi = (hi < lo) ? lo : ((hi > args.n_tokens) ? args.n_tokens : hi);
   ch.lo = lo;
   ch.hi = hi;
-  if (ch.batched) {
+  if (FUSED) {
+    ch.nc = args.req_offsets[ch.seg + 1] - ch.e0;
+  } else if (ch.batched) {
     const int e1 = ch.e0 + args.group_e;
     ch.nc = ((e1 < args.n_entries) ? e1 : args.n_entries) - ch.e0;
   } else {
@@ -1113,7 +1188,7 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
       col0 = cb * 2 * NCOL + 32 * wave;
     }
     if (state_role && col0 < DV)
-      state_wave<DK, DV>(args, ch, smem, lane, col0, wave);
+      state_wave<DK, DV, FUSED>(args, ch, smem, lane, col0, wave);
     else if (!state_role && ch.need_op)
       operator_wave<DK, DV>(args, ch, smem, lane, col0, wave);
     else
@@ -1129,15 +1204,16 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   }
 }
 
-template <int DK, int DV>
+template <int DK, int DV, bool FUSED = false>
 hipError_t launch_t(const ScanArgs& a, int n_items, hipStream_t s) {
   constexpr int bytes = Lds<DK>::TOTAL;
   // one-time (thread-safe static initialisation) opt-in to more than 64 KiB of LDS
   static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(&scan_bf16_kernel<DK, DV>),
+      reinterpret_cast<const void*>(&scan_bf16_kernel<DK, DV, FUSED>),
       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((scan_bf16_kernel<DK, DV>), dim3(n_items), dim3(kThreads), bytes, s, a);
+  hipLaunchKernelGGL((scan_bf16_kernel<DK, DV, FUSED>), dim3(n_items), dim3(kThreads), bytes, s,
+                     a);
   return hipGetLastError();
 }
 
@@ -1147,6 +1223,19 @@ int scan_bf16_items_per_head(int d_k, int d_v, int with_operator) {
   const int ns = d_v / NCOL, np = d_k / NCOL;
   if (!with_operator) return (d_v + 2 * NCOL - 1) / (2 * NCOL);
   return (np > ns) ? np : ns;
+}
+
+hipError_t launch_seam_compose_fused(const ScanArgs& a, int d_k, int d_v, int n_req,
+                                     hipStream_t s) {
+  // no operator columns: one workgroup carries every state column of a head
+  const int64_t n_items = static_cast<int64_t>(n_req) * a.h_v * scan_bf16_items_per_head(d_k, d_v, 0);
+  if (n_items <= 0) return hipSuccess;
+  if (n_items > 0x7fffffff || a.n_roles != 1 || a.mode != 2 || a.w > C) return hipErrorInvalidValue;
+  const int n = static_cast<int>(n_items);
+  if (d_k == 64 && d_v == 64) return launch_t<64, 64, true>(a, n, s);
+  if (d_k == 64 && d_v == 128) return launch_t<64, 128, true>(a, n, s);
+  if (d_k == 128 && d_v == 64) return launch_t<128, 64, true>(a, n, s);
+  return launch_t<128, 128, true>(a, n, s);
 }
 
 hipError_t launch_scan_bf16(const ScanArgs& a, int d_k, int d_v, int n_items, hipStream_t s) {

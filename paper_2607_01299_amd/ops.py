@@ -418,12 +418,28 @@ def causal_conv(x, weight, cu_seqlens, state_in=None, *, silu=True, want_state=T
 # reuse with seam windows that advance the state (Sec. 4.3)
 # ---------------------------------------------------------------------------
 
+def compose_and_rescan(P_hat, log_decay, S_seg, q, k, v, beta, log_alpha, seam_start, seam_len,
+                       w, seg_ids, req_offsets, S_prefix=None):
+    """Eq. (6) composition of whole-segment pool tuples with each listed entry's
+    first min(w, seam_len) tokens rescanned from the state entering it, in one
+    pass (see include/hypic.h; bf16 tokens, w <= 64).
+    Returns (S_out [n_req, h_v, d_k, d_v], o_seam [nnz, w, h_v, d_v])."""
+    return _seam_compose("hypic_compose_and_rescan", P_hat, log_decay, S_seg, q, k, v, beta,
+                         log_alpha, seam_start, seam_len, w, seg_ids, req_offsets, S_prefix)
+
+
 def compose_with_seams(P_hat, log_decay, S_seg, q, k, v, beta, log_alpha, seam_start, seam_len,
                        w, seg_ids, req_offsets, S_prefix=None):
     """Tail tuples of the pool composed with each entry's seam run from the
     running state first (see include/hypic.h).  Token dtype gives the
     composition arithmetic (bf16: split bf16; f32: float32 matrix cores).
     Returns (S_out [n_req, h_v, d_k, d_v], o_seam [nnz, w, h_v, d_v])."""
+    return _seam_compose("hypic_compose_with_seams", P_hat, log_decay, S_seg, q, k, v, beta,
+                         log_alpha, seam_start, seam_len, w, seg_ids, req_offsets, S_prefix)
+
+
+def _seam_compose(entry, P_hat, log_decay, S_seg, q, k, v, beta, log_alpha, seam_start, seam_len,
+                  w, seg_ids, req_offsets, S_prefix):
     lib = _lib.load()
     n_pool, h_v, d_k, d_v = C.pool(P_hat, log_decay, S_seg)
     dev = S_seg.device
@@ -452,9 +468,12 @@ def compose_with_seams(P_hat, log_decay, S_seg, q, k, v, beta, log_alpha, seam_s
     max_n = int(np.max(np.diff(off_h))) if n_req > 0 else 0
     S_out = torch.empty((n_req, h_v, d_k, d_v), dtype=torch.float32, device=dev)
     o_seam = torch.empty((nnz, w, h_v, d_v), dtype=q.dtype, device=dev)
-    need = lib.hypic_seam_compose_workspace_bytes(ctypes.byref(dims), n_req, max_n)
+    if entry == "hypic_compose_with_seams":
+        need = lib.hypic_seam_compose_workspace_bytes(ctypes.byref(dims), n_req, max_n)
+    else:
+        need = lib.hypic_workspace_bytes(_lib.HYPIC_OP_COMPOSE_RESCAN, ctypes.byref(dims), n_req)
     ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
-    _lib.check(lib.hypic_compose_with_seams(
+    _lib.check(getattr(lib, entry)(
         ctypes.byref(dims), _ptr(P_hat), _ptr(log_decay), _ptr(S_seg), n_pool, _ptr(q), _ptr(k),
         _ptr(v), _ptr(beta), _ptr(log_alpha), q.shape[0], _ptr(ss_d), _hptr(ss_h), _ptr(sl_d),
         _hptr(sl_h), int(w), _ptr(ids_d), _hptr(ids_h), _ptr(off_d), _hptr(off_h), n_req,
