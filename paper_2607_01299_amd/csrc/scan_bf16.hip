@@ -222,27 +222,37 @@ struct Chain {
   const int32_t* tok_start;
   const int32_t* tok_len;
   const int32_t* ids;  // fused composition: pool entry of listed segment e0 + c
+  // batched entries: lane l holds the first token and token count of entry
+  // e0 + l (l < 64), read once per workgroup, so that no iteration waits on a
+  // chain of dependent loads for its token range
+  int pre_t, pre_n;
+  int pre_id;  // fused: lane l holds the pool entry of listed segment e0 + l
 };
 
 // token range of seam entry e0 + c (through the request's pool ids when fused)
 __device__ __forceinline__ int entry_of(const Chain& ch, int c) {
   return ch.ids != nullptr ? ch.ids[ch.e0 + c] : ch.e0 + c;
 }
-__device__ __forceinline__ int chunk_start(const Chain& ch, int c) {
-  if (!ch.batched) return ch.lo + c * C;
+__device__ __forceinline__ int entry_start(const Chain& ch, int c) {
   const int t = ch.tok_start[entry_of(ch, c)];
   return (t < 0) ? 0 : ((t >= ch.n_tok) ? ch.n_tok - 1 : t);
+}
+__device__ __forceinline__ int entry_len(const Chain& ch, int c, int t) {
+  const int l = ch.tok_len[entry_of(ch, c)];
+  int n = (l < ch.w) ? l : ch.w;
+  n = (n > ch.n_tok - t) ? ch.n_tok - t : n;
+  return (n < 1) ? 1 : n;
+}
+__device__ __forceinline__ int chunk_start(const Chain& ch, int c) {
+  if (!ch.batched) return ch.lo + c * C;
+  return (c < 64) ? __builtin_amdgcn_readlane(ch.pre_t, c) : entry_start(ch, c);
 }
 __device__ __forceinline__ int chunk_len(const Chain& ch, int c) {
   if (!ch.batched) {
     const int r = ch.hi - (ch.lo + c * C);
     return (r < C) ? r : C;
   }
-  const int t = chunk_start(ch, c);
-  const int l = ch.tok_len[entry_of(ch, c)];
-  int n = (l < ch.w) ? l : ch.w;
-  n = (n > ch.n_tok - t) ? ch.n_tok - t : n;
-  return (n < 1) ? 1 : n;
+  return (c < 64) ? __builtin_amdgcn_readlane(ch.pre_n, c) : entry_len(ch, c, entry_start(ch, c));
 }
 
 // raw 16-byte loads of the 32x32-layout fragments of one token tile of a
@@ -765,48 +775,69 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
 // =============================================================================
 
 // One Eq. (4) step of a state wave's 32 columns (all d_k rows, order rho):
-// S <- exp(g) P S + S_i.  The A operand streams P's rows from HBM in float32:
-// lane (g2, r) of step u needs true row rho^-1(32 m + r), true columns
-// 16 u + 8 g2 .. +7 (the slot order of a state B fragment maps back to 8
-// contiguous columns), split into bf16 hi + lo; the B operand is exp(g) S from
-// the accumulators, split likewise; three passes; the accumulators start from
-// S_i, so no extra pass adds it.
+// S <- exp(g) P S + S_i.  The B operand is exp(g) S from the accumulators,
+// split once into bf16 hi + lo.  The A operand streams P's rows from HBM in
+// float32: lane (g2, r) of step u needs true row rho^-1(32 m + r), true
+// columns 16 u + 8 g2 .. +7 (the slot order of a state B fragment maps back to
+// 8 contiguous columns), split into hi + lo; three passes.  Output tile m is
+// produced from two half-batches of four steps (8 x 16-byte loads per lane
+// each); the loads of the next half-batch, and of S_i's tile with the first
+// half of a tile, are issued before the current one computes, so one batch is
+// always in flight.  The accumulators start from S_i.
 template <int DK, int DV>
 __device__ __forceinline__ void compose_entry(f32x16 (&st)[DK / 32], const float* P,
                                               const float* Si, float e, int col0, int lane) {
-  constexpr int NM = DK / 32, NU = DK / 16;
+  constexpr int NM = DK / 32, NU = DK / 16, NB = 2 * NM;  // tiles, steps, half-batches
   const int g2 = lane >> 5, n32 = lane & 31;
-  f32x16 acc[NM];
-#pragma unroll
-  for (int m = 0; m < NM; ++m)
-#pragma unroll
-    for (int x = 0; x < 16; ++x) acc[m][x] = Si[true_row(m, x, g2) * DV + col0 + n32];
-  const int prow = (n32 & ~12) | ((n32 & 4) << 1) | ((n32 & 8) >> 1);  // rho -> true row
-  const float* pr = P + prow * DK + 8 * g2;
+  bf16x8 bh[NU], bl[NU];
 #pragma unroll
   for (int u = 0; u < NU; ++u) {
-    bf16x8 bh, bl;
-    {
-      f32x16 es = st[u >> 1] * e;
-      split_of(es, u & 1, bh, bl);
-    }
+    const f32x16 es = st[u >> 1] * e;
+    split_of(es, u & 1, bh[u], bl[u]);
+  }
+  const int prow = (n32 & ~12) | ((n32 & 4) << 1) | ((n32 & 8) >> 1);  // rho -> true row
+  const float* pr = P + prow * DK + 8 * g2;
+  const float* sr = Si + col0 + n32;
+  float4 buf[2][8];
+  f32x16 acc[2];
+  auto load_half = [&](int b) __attribute__((always_inline)) {
+    const float* src = pr + (32 * (b >> 1)) * DK + 64 * (b & 1);
 #pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      const float* src = pr + (32 * m) * DK + 16 * u;
-      const float4 a0 = *reinterpret_cast<const float4*>(src);
-      const float4 a1 = *reinterpret_cast<const float4*>(src + 4);
+    for (int uu = 0; uu < 4; ++uu) {
+      buf[b & 1][2 * uu] = *reinterpret_cast<const float4*>(src + 16 * uu);
+      buf[b & 1][2 * uu + 1] = *reinterpret_cast<const float4*>(src + 16 * uu + 4);
+    }
+  };
+  auto load_tile = [&](int m) __attribute__((always_inline)) {
+#pragma unroll
+    for (int x = 0; x < 16; ++x) acc[m & 1][x] = sr[true_row(m, x, g2) * DV];
+  };
+  load_tile(0);
+  load_half(0);
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const int m = b >> 1;
+    if (b + 1 < NB) {
+      if (((b + 1) & 1) == 0) load_tile(m + 1);
+      load_half(b + 1);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int uu = 0; uu < 4; ++uu) {
+      const int u = 4 * (b & 1) + uu;
+      const float4 a0 = buf[b & 1][2 * uu], a1 = buf[b & 1][2 * uu + 1];
       f32x16 a;
       a[0] = a0.x; a[1] = a0.y; a[2] = a0.z; a[3] = a0.w;
       a[4] = a1.x; a[5] = a1.y; a[6] = a1.z; a[7] = a1.w;
       bf16x8 ah, al;
       split_of(a, 0, ah, al);
-      acc[m] = mma32(ah, bh, acc[m]);
-      acc[m] = mma32(ah, bl, acc[m]);
-      acc[m] = mma32(al, bh, acc[m]);
+      acc[m & 1] = mma32(ah, bh[u], acc[m & 1]);
+      acc[m & 1] = mma32(ah, bl[u], acc[m & 1]);
+      acc[m & 1] = mma32(al, bh[u], acc[m & 1]);
     }
+    if (b & 1) st[m] = acc[m & 1];
+    __builtin_amdgcn_sched_barrier(0);
   }
-#pragma unroll
-  for (int m = 0; m < NM; ++m) st[m] = acc[m];
 }
 
 template <int DK, int DV, bool FUSED>
@@ -971,7 +1002,8 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
     if constexpr (FUSED) {
       // Eq. (4) with the listed segment's tuple
       if (active) {
-        const long ih = static_cast<long>(entry_of(ch, c)) * args.h_v + ch.h;
+        const int id = (c < 64) ? __builtin_amdgcn_readlane(ch.pre_id, c) : entry_of(ch, c);
+        const long ih = static_cast<long>(id) * args.h_v + ch.h;
         const float e = __expf(args.pool_ld[ih]);
         compose_entry<DK, DV>(st, args.pool_P + ih * DK * DK, args.pool_S + ih * DK * DV, e,
                               col0, lane);
@@ -1174,6 +1206,12 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   ch.sh = static_cast<long>(ch.seg) * args.h_v + ch.h;
   ch.qk_stride = static_cast<long>(args.h_qk) * DK;
   ch.v_stride = static_cast<long>(args.h_v) * DV;
+  ch.pre_t = ch.pre_n = ch.pre_id = 0;
+  if (ch.batched && lane < ch.nc) {
+    ch.pre_t = entry_start(ch, lane);
+    ch.pre_n = entry_len(ch, lane, ch.pre_t);
+    ch.pre_id = entry_of(ch, lane);
+  }
   ch.need_state = ch.with_op ? (cb * NCOL < DV) : true;
   ch.need_op = ch.with_op && (cb * NCOL < DK);
 

@@ -244,17 +244,21 @@ class ComposeBurst:
 
 class SeamAdvanceBurst:
     """Requests composed from a pool of tail tuples with each entry's seam run
-    from the running state first (hypic_compose_with_seams), pre-bound.
+    from the running state first (hypic_compose_with_seams), pre-bound.  With
+    advance=False the pool holds whole-segment tuples and each seam runs from
+    the state entering its entry without advancing it
+    (hypic_compose_and_rescan): the composition and seams of ComposeBurst in
+    one pass.
 
     lanes > 1 splits the requests, dealt longest first, over that many calls on
-    streams of their own (default priority), so that one lane's seam steps
-    (matrix-core work) overlap another's compositions (HBM streams).  Each lane
-    then holds its requests' S_out and o_seam in its own request order;
-    outputs() assembles them in the caller's order.
+    streams of their own (default priority).  Each lane then holds its
+    requests' S_out and o_seam in its own request order; outputs() assembles
+    them in the caller's order.
     """
 
     def __init__(self, P_hat, log_decay, S_seg, seg_ids, req_offsets, tokens, seam_start,
-                 seam_len, w, *, S_prefix=None, lanes=1):
+                 seam_len, w, *, S_prefix=None, lanes=1, advance=True):
+        self.entry = "hypic_compose_with_seams" if advance else "hypic_compose_and_rescan"
         self.lib = _lib.load()
         dev = S_seg.device
         self.stream = torch.cuda.current_stream(dev)
@@ -302,7 +306,12 @@ class SeamAdvanceBurst:
         S_out = torch.empty((n_req, self.h_v, self.d_k, self.d_v), dtype=torch.float32,
                             device=dev)
         o_seam = torch.empty((nnz, self.w, self.h_v, self.d_v), dtype=q.dtype, device=dev)
-        need = self.lib.hypic_seam_compose_workspace_bytes(ctypes.byref(self.dims), n_req, max_n)
+        if self.entry == "hypic_compose_with_seams":
+            need = self.lib.hypic_seam_compose_workspace_bytes(ctypes.byref(self.dims), n_req,
+                                                               max_n)
+        else:
+            need = self.lib.hypic_workspace_bytes(_lib.HYPIC_OP_COMPOSE_RESCAN,
+                                                  ctypes.byref(self.dims), n_req)
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
         args = (
             ctypes.byref(self.dims), _p(P_hat), _p(log_decay), _p(S_seg), n_pool, _p(q), _p(k),
@@ -316,14 +325,15 @@ class SeamAdvanceBurst:
                                                                    S_prefix), "args": args}
 
     def run(self):
+        call = getattr(self.lib, self.entry)
         if len(self.lanes) == 1:
-            _lib.check(self.lib.hypic_compose_with_seams(*self.lanes[0]["args"]))
+            _lib.check(call(*self.lanes[0]["args"]))
             return
         start = torch.cuda.Event()
         start.record(self.stream)
         for lane, st in zip(self.lanes, self.streams):
             st.wait_event(start)
-            _lib.check(self.lib.hypic_compose_with_seams(*lane["args"]))
+            _lib.check(call(*lane["args"]))
         for st in self.streams:
             done = torch.cuda.Event()
             done.record(st)
