@@ -1142,16 +1142,22 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   ch.with_op = args.n_roles == 2;
   constexpr int NP = DK / NCOL, NS = DV / NCOL;
   const int n_cb = ch.with_op ? ((NP > NS) ? NP : NS) : (DV + 2 * NCOL - 1) / (2 * NCOL);
-  // Workgroups are dealt to the 8 XCDs round-robin; the n_cb column blocks of a
-  // chain are numbered so that they land on one XCD back to back and share its
-  // L2 for q and k.  Chains past the last full group of 8 keep linear order.
+  // Workgroups are dealt to the 8 XCDs round-robin.  A unit is every
+  // workgroup that reads one q/k head's tokens: the n_cb column blocks of each
+  // of the group's v-head chains (chains G u .. G u + G - 1, G = h_v / h_qk).
+  // A unit's workgroups are numbered to land on one XCD back to back, so they
+  // share its L2 for q and k; units past the last full group of 8 keep linear
+  // order.
   const int n_chains = static_cast<int>(gridDim.x) / n_cb;
-  const int full = (n_chains / 8) * 8 * n_cb;
+  const int G = args.group;
+  const int U = G * n_cb;
+  const int full = (n_chains / G / 8) * 8 * U;
   int chain, cb;
   if (static_cast<int>(blockIdx.x) < full) {
     const int slot = blockIdx.x / 8;
-    chain = (slot / n_cb) * 8 + blockIdx.x % 8;
-    cb = slot % n_cb;
+    const int within = slot % U;
+    chain = ((slot / U) * 8 + blockIdx.x % 8) * G + within / n_cb;
+    cb = within % n_cb;
   } else {
     const int b = blockIdx.x - full;
     chain = full / n_cb + b / n_cb;
