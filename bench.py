@@ -181,6 +181,13 @@ def hbm_roofline(alg_bytes, ms, kernel, workload, record_key=None):
     counted = alg_bytes if traffic is None else min(alg_bytes, traffic)
     out["achieved"] = counted / (ms * 1e-3) / 1e9
     out["frac"] = out["achieved"] / PEAK_HBM_GBS
+    if traffic is None and out["frac"] > 1.0:
+        # more algorithmic bytes than HBM can deliver in this time: caches serve
+        # re-reads, and without a counter record of this kernel code the HBM
+        # share is unknown
+        out["achieved"] = out["frac"] = None
+        out["note_frac"] = ("algorithmic bytes above the HBM peak (re-reads served by the "
+                            "caches); no counter record of the current kernel code")
     return out
 
 

@@ -57,6 +57,9 @@ def test_hbm_roofline_never_exceeds_the_counted_bytes():
     r = bench.hbm_roofline(8e9, 1.0, None, "nothing")        # 8 GB in 1 ms, no record
     assert abs(r["frac"] - 1.0) < 1e-12 and r["traffic"] is None
     assert abs(r["frac_algorithmic"] - 1.0) < 1e-12
+    # above the peak with no counter record: no HBM fraction is claimed
+    r = bench.hbm_roofline(9e9, 1.0, None, "nothing")
+    assert r["frac"] is None and r["achieved"] is None and r["frac_algorithmic"] > 1.0
 
 
 def test_kda_flop_split_sums_to_the_build_count():
