@@ -467,8 +467,9 @@ def bench_compose_burst(torch, steps, warmup):
     seam_ms = float(np.median([e[1].elapsed_time(e[2]) for e in ev]))
     nnz, h_v = burst.nnz, burst.h_v
     name = W.CONFIG_NAMES[5]
-    # Sec. 8(d)'s unit: read P_hat_i, S_i and log_decay_i per head-step (131,076 B);
-    # this kernel also writes the incoming state for the separate seam launch
+    # the composition's own bytes: P_hat_i, S_i and log_decay_i read per
+    # head-step (131,076 B at d = 128); this launch also writes the incoming
+    # state that the separate seam launch reads
     alg = float(compose_bytes_per_head_step(burst.d_k, burst.d_v, False)) * nnz * h_v
     alg_inc = float(compose_bytes_per_head_step(burst.d_k, burst.d_v, True)) * nnz * h_v
     roof = hbm_roofline(alg, comp_ms, None, name)
@@ -483,6 +484,15 @@ def bench_compose_burst(torch, steps, warmup):
     two_launch = {"ms_per_burst": dt / steps * 1e3, "compositions_per_s": nnz / (dt / steps),
                   "compose_ms": comp_ms, "seam_ms": seam_ms, "roofline": roof,
                   "note": "compose_kernel writing the incoming states, then the seam launch"}
+    # the composition alone (S_out, no incoming states: the launch a caller
+    # that needs no seam makes), the same kernel
+    states_ms = _events_ms(torch, stream, burst.compose_states, max(steps // 2, 4))
+    states_roof = hbm_roofline(alg, states_ms, None, name)
+    states_roof["kernel"] = "compose_kernel (S_incoming = NULL)"
+    two_launch["compose_states_only"] = {
+        "ms": states_ms, "compositions_per_s": nnz / (states_ms * 1e-3), "roofline": states_roof,
+        "note": "Eq. (6) to S_out without the incoming-state writes; frac by the composition's "
+                "131,076 B per head-step"}
     # the same burst in one pass (hypic_compose_and_rescan): each (request,
     # head) keeps its state on chip; the seam of each entry from its incoming
     # state, then Eq. (4)

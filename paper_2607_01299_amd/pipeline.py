@@ -234,6 +234,13 @@ class ComposeBurst:
     def compose(self):
         _lib.check(self.lib.hypic_compose_segments(*self._compose_args))
 
+    def compose_states(self):
+        """Eq. (6) to S_out alone: the same launch without the incoming states
+        (S_incoming = NULL), as a caller that needs no seam issues it."""
+        a = list(self._compose_args)
+        a[12] = None
+        _lib.check(self.lib.hypic_compose_segments(*a))
+
     def seam(self):
         _lib.check(self.lib.hypic_seam_rescan(*self._seam_args))
 

@@ -39,7 +39,7 @@ def test_build_flops_are_the_chunk_products():
 
 
 def test_build_flop_counts_the_gram_once_per_qk_head():
-    """Sec. 8(a): every v-head's chunk products, the K K^T and Q K^T Gram once
+    """The algorithmic count: every v-head's chunk products, the K K^T and Q K^T Gram once
     per q/k head of a grouped-head group.  Equal heads give the per-head count;
     the long-context workload (16 q/k, 32 v heads, 131072 tokens) is 962 GFLOP."""
     assert bench.build_flop(16384, 16, 16, 128, 128, 64) == 16384 * 16 * 245_760

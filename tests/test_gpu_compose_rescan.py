@@ -82,6 +82,13 @@ def test_compose_and_rescan_serve_burst_equals_two_launches(hy):
     two = ComposeBurst(*pool, p["seg_ids"], p["req_offsets"], toks, p["tok_start"], p["tok_len"],
                        p["w"])
     two.run()
+    # the composition alone (no incoming states written) gives the same S_out,
+    # bit for bit: the same kernel with its incoming-state stores skipped
+    S_two = two.S_out.clone()
+    two.S_out.fill_(float("nan"))
+    two.compose_states()
+    torch.cuda.synchronize()
+    assert torch.equal(two.S_out, S_two)
     S_out, o_seam = hy.compose_and_rescan(*pool, *toks, p["tok_start_pool"], p["seam_len_pool"],
                                           p["w"], p["seg_ids"], p["req_offsets"])
     torch.cuda.synchronize()
