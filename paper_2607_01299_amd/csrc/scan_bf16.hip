@@ -226,7 +226,8 @@ struct Chain {
   // e0 + l (l < 64), read once per workgroup, so that no iteration waits on a
   // chain of dependent loads for its token range
   int pre_t, pre_n;
-  int pre_id;  // fused: lane l holds the pool entry of listed segment e0 + l
+  int pre_id;    // fused: lane l holds the pool entry of listed segment e0 + l
+  float pre_ld;  // fused: lane l holds that entry's log_decay (this head)
 };
 
 // token range of seam entry e0 + c (through the request's pool ids when fused)
@@ -253,6 +254,113 @@ __device__ __forceinline__ int chunk_len(const Chain& ch, int c) {
     return (r < C) ? r : C;
   }
   return (c < 64) ? __builtin_amdgcn_readlane(ch.pre_n, c) : entry_len(ch, c, entry_start(ch, c));
+}
+
+// The fused composition (mode 2) adds DK / 32 - 1 barriers to every iteration
+// that composes an entry (compose_entry): the four producer waves stage P_hat's
+// A operands into LDS one output tile at a time, the first before the
+// iteration's first barrier and each later one before a barrier of its own
+// (producer_compose_first, producer_compose), and a wave without a part in it
+// passes the same barriers after its own work.
+template <int DK>
+__device__ __forceinline__ int compose_barriers(const ScanArgs& args) {
+  return args.mode == 2 ? DK / 32 - 1 : 0;
+}
+__device__ __forceinline__ void pass_barriers(const Chain& ch, int it, int n) {
+  if (it >= 0 && it < ch.nc)
+    for (int i = 0; i < n; ++i) lds_barrier();
+}
+
+// A producer wave's share of one entry's P_hat A operands: for every output
+// tile m (32 rows, order rho) the steps u = US p .. US p + US - 1 (p = wave -
+// 4, US = d_k / 64) of lane (g2, r): true row rho^-1(32 m + r), true columns
+// 16 u + 8 g2 .. +7 in float32.  A ring of D tiles: the first D are loaded an
+// iteration before they are staged, each later one D rounds before.
+template <int DK>
+struct PShare {
+  static constexpr int NM = DK / 32, US = DK / 64, D = (NM < 2) ? NM : 2;
+  float4 p[D][US][2];
+  const float* pr;  // this lane's first element of the entry's share
+};
+
+template <int DK>
+__device__ __forceinline__ void share_load_tile(PShare<DK>& sh, int m) {
+  constexpr int US = PShare<DK>::US, D = PShare<DK>::D;
+#pragma unroll
+  for (int k = 0; k < US; ++k) {
+    sh.p[m % D][k][0] = *reinterpret_cast<const float4*>(sh.pr + 32 * m * DK + 16 * k);
+    sh.p[m % D][k][1] = *reinterpret_cast<const float4*>(sh.pr + 32 * m * DK + 16 * k + 4);
+  }
+}
+
+template <int DK>
+__device__ __forceinline__ void share_load(PShare<DK>& sh, const ScanArgs& args, const Chain& ch,
+                                           int c, int pslot, int lane) {
+  constexpr int US = PShare<DK>::US, D = PShare<DK>::D;
+  const int id = (c < 64) ? __builtin_amdgcn_readlane(ch.pre_id, c) : entry_of(ch, c);
+  const int g2 = lane >> 5, n32 = lane & 31;
+  const int prow = (n32 & ~12) | ((n32 & 4) << 1) | ((n32 & 8) >> 1);  // rho -> true row
+  sh.pr = args.pool_P + (static_cast<long>(id) * args.h_v + ch.h) * DK * DK + prow * DK +
+          8 * g2 + 16 * US * pslot;
+#pragma unroll
+  for (int m = 0; m < D; ++m) share_load_tile<DK>(sh, m);
+}
+
+// Stage output tile m's share, split into bf16 hi + lo, as fragments 2u (hi)
+// and 2u + 1 (lo) of buffer m % 2, then load the share of tile m + D into the
+// ring.  The buffers are regions idle during a fused composition: W lo (no
+// operator columns) and the Q fragments of chunk c (free once the iteration's
+// first barrier has passed, so tile 0, staged before it, goes to W lo).
+template <int DK>
+__device__ __forceinline__ void share_stage(PShare<DK>& sh, unsigned char* smem, int par, int m,
+                                            int pslot, int lane) {
+  using LP = Lds<DK>;
+  constexpr int NM = PShare<DK>::NM, US = PShare<DK>::US, D = PShare<DK>::D;
+  u16* buf = reinterpret_cast<u16*>((m & 1) ? smem + LP::O_Q + par * LP::NW * LP::FB
+                                            : smem + LP::O_WL);
+#pragma unroll
+  for (int k = 0; k < US; ++k) {
+    const float4 p0 = sh.p[m % D][k][0], p1 = sh.p[m % D][k][1];
+    f32x16 a;
+    a[0] = p0.x; a[1] = p0.y; a[2] = p0.z; a[3] = p0.w;
+    a[4] = p1.x; a[5] = p1.y; a[6] = p1.z; a[7] = p1.w;
+    bf16x8 ah, al;
+    split_of(a, 0, ah, al);
+    const int u = US * pslot + k;
+    stf(buf, 2 * u, lane, ah);
+    stf(buf, 2 * u + 1, lane, al);
+  }
+  if (m + D < NM) share_load_tile<DK>(sh, m + D);
+}
+
+// A producer wave's part of the fused composition of entry it: tile 0 at the
+// start of the iteration (before its first barrier, so the state waves can
+// multiply it as soon as they reach it) ...
+template <int DK, bool FUSED>
+__device__ __forceinline__ void producer_compose_first(PShare<DK>& sh, const Chain& ch,
+                                                       unsigned char* smem, int it, int pslot,
+                                                       int lane) {
+  if constexpr (FUSED) {
+    if (it >= 0 && it < ch.nc) share_stage<DK>(sh, smem, it & 1, 0, pslot, lane);
+  }
+}
+
+// ... and at its end the later tiles, one per barrier, then the loads of entry
+// it + 1's first tiles.
+template <int DK, bool FUSED>
+__device__ __forceinline__ void producer_compose(PShare<DK>& sh, const ScanArgs& args,
+                                                 const Chain& ch, unsigned char* smem, int it,
+                                                 int pslot, int lane) {
+  if constexpr (FUSED) {
+    if (it >= 0 && it < ch.nc) {
+#pragma unroll
+      for (int m = 1; m < PShare<DK>::NM; ++m) {
+        share_stage<DK>(sh, smem, it & 1, m, pslot, lane);
+        lds_barrier();
+      }
+    }
+    if (it + 1 >= 0 && it + 1 < ch.nc) share_load<DK>(sh, args, ch, it + 1, pslot, lane);
+  }
 }
 
 // raw 16-byte loads of the 32x32-layout fragments of one token tile of a
@@ -305,10 +413,11 @@ __device__ __forceinline__ f32x4 transpose16(const Split4& x, const s16x4& eye) 
   return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(x.l, eye, c, 0, 0, 0);
 }
 
-template <int DK, int DV>
+template <int DK, int DV, bool FUSED>
 __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& ch,
                                              unsigned char* smem, int lane) {
   using LP = Lds<DK>;
+  PShare<DK> psh;  // fused composition: this wave's share of the next entry's P_hat
   constexpr int KTD = DK / 32;
   const int g = lane >> 4, n16 = lane & 15;
   float* bs = reinterpret_cast<float*>(smem + LP::O_BS);
@@ -356,6 +465,7 @@ __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& 
   }
 
   for (int it = -2; it < ch.nc; ++it) {
+    producer_compose_first<DK, FUSED>(psh, ch, smem, it, 0, lane);
     const int c = it + 2;
     const bool active = c < ch.nc;
     f32x4 gu[6];      // upper Gram tiles (k, i), k < i: rows of L_ik once scaled by beta
@@ -459,6 +569,7 @@ __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& 
       emit(af, 3, 1, -mma16_x3(T31, R3, zero4()));
       emit(af, 3, 0, -mma16_x3(T30, R3, zero4()));
     }
+    producer_compose<DK, FUSED>(psh, args, ch, smem, it, 0, lane);
     lds_barrier();
   }
 }
@@ -537,10 +648,11 @@ __device__ __forceinline__ u16x4 pack4(float a, float b, float c, float d) {
 
 // Wave 5: loads all of K and Q of the chunk (one copy per workgroup) and the
 // gates; forms K Q^T masked with Gamma, the Q fragments and its share of W.
-template <int DK, int DV>
+template <int DK, int DV, bool FUSED>
 __device__ __forceinline__ void producer_qk_wave(const ScanArgs& args, const Chain& ch,
                                                  unsigned char* smem, int lane) {
   using LP = Lds<DK>;
+  PShare<DK> psh;  // fused composition: this wave's share of the next entry's P_hat
   constexpr int NU = DK / 16;
   constexpr int KTD = DK / 32;
   const int g = lane >> 4, n16 = lane & 15;
@@ -570,6 +682,7 @@ __device__ __forceinline__ void producer_qk_wave(const ScanArgs& args, const Cha
   if (ch.nc > 0) prefetch(0);
 
   for (int it = -2; it < ch.nc; ++it) {
+    producer_compose_first<DK, FUSED>(psh, ch, smem, it, 1, lane);
     const int p = it + 1;
     const bool active = p >= 0 && p < ch.nc;
     const int par = p & 1;
@@ -651,16 +764,18 @@ __device__ __forceinline__ void producer_qk_wave(const ScanArgs& args, const Cha
         }
       }
     }
+    producer_compose<DK, FUSED>(psh, args, ch, smem, it, 1, lane);
     lds_barrier();
   }
 }
 
 // Waves 6, 7: load one d_k half of K (HALF = 0, 1) and form its K^T
 // fragments; then (A1 . Gamma) diag(beta) and a share of W.
-template <int DK, int DV, int HALF>
+template <int DK, int DV, int HALF, bool FUSED>
 __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Chain& ch,
                                                  unsigned char* smem, int lane) {
   using LP = Lds<DK>;
+  PShare<DK> psh;  // fused composition: this wave's share of the next entry's P_hat
   constexpr int NH = DK / 64;  // 32-wide d_k blocks of this half
   const int g = lane >> 4, n16 = lane & 15;
   const int g2 = lane >> 5, n32 = lane & 31;
@@ -687,6 +802,7 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
   if (ch.nc > 0) prefetch(0);
 
   for (int it = -2; it < ch.nc; ++it) {
+    producer_compose_first<DK, FUSED>(psh, ch, smem, it, 2 + HALF, lane);
     const int p = it + 1;
     const bool active = p >= 0 && p < ch.nc;
     const int par = p & 1;
@@ -766,6 +882,7 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
       }
       emit_w<DK>(ch, smem, lane, par, 1 + 2 * HALF);
     }
+    producer_compose<DK, FUSED>(psh, args, ch, smem, it, 2 + HALF, lane);
     lds_barrier();
   }
 }
@@ -774,69 +891,47 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
 // waves 0-3: the chain update of chunk c
 // =============================================================================
 
-// One Eq. (4) step of a state wave's 32 columns (all d_k rows, order rho):
-// S <- exp(g) P S + S_i.  The B operand is exp(g) S from the accumulators,
-// split once into bf16 hi + lo.  The A operand streams P's rows from HBM in
-// float32: lane (g2, r) of step u needs true row rho^-1(32 m + r), true
-// columns 16 u + 8 g2 .. +7 (the slot order of a state B fragment maps back to
-// 8 contiguous columns), split into hi + lo; three passes.  Output tile m is
-// produced from two half-batches of four steps (8 x 16-byte loads per lane
-// each); the loads of the next half-batch, and of S_i's tile with the first
-// half of a tile, are issued before the current one computes, so one batch is
-// always in flight.  The accumulators start from S_i.
+// One Eq. (4) step of the fused composition, S <- exp(g) P S + S_i, for a
+// state wave's 32 columns (all d_k rows, order rho).  P's A operands (lane
+// (g2, r) of step u: true row rho^-1(32 m + r), true columns 16 u + 8 g2 ..
+// +7, the slot order of a state B fragment mapped back to 8 contiguous
+// columns, split into bf16 hi + lo) are staged once per workgroup by the four
+// producer waves into two LDS buffers in turn, tile 0 before the iteration's
+// first barrier and each later tile before a barrier of its own; the producers
+// load them ahead.  The B operand is exp(g) S from the accumulators, split
+// once; S_i's tiles are loaded at the start and added to each tile's product;
+// three passes.  d_k / 32 - 1 barriers.
 template <int DK, int DV>
-__device__ __forceinline__ void compose_entry(f32x16 (&st)[DK / 32], const float* P,
-                                              const float* Si, float e, int col0, int lane) {
-  constexpr int NM = DK / 32, NU = DK / 16, NB = 2 * NM;  // tiles, steps, half-batches
-  const int g2 = lane >> 5, n32 = lane & 31;
+__device__ __forceinline__ void compose_entry(f32x16 (&st)[DK / 32], const float* Si, float e,
+                                              int col0, int lane, const u16* buf0,
+                                              const u16* buf1) {
+  constexpr int NM = DK / 32, NU = DK / 16;
+  const int g2 = lane >> 5;
   bf16x8 bh[NU], bl[NU];
 #pragma unroll
   for (int u = 0; u < NU; ++u) {
     const f32x16 es = st[u >> 1] * e;
     split_of(es, u & 1, bh[u], bl[u]);
   }
-  const int prow = (n32 & ~12) | ((n32 & 4) << 1) | ((n32 & 8) >> 1);  // rho -> true row
-  const float* pr = P + prow * DK + 8 * g2;
-  const float* sr = Si + col0 + n32;
-  float4 buf[2][8];
-  f32x16 acc[2];
-  auto load_half = [&](int b) __attribute__((always_inline)) {
-    const float* src = pr + (32 * (b >> 1)) * DK + 64 * (b & 1);
+  // S_i's tiles of this wave's columns (the state registers are free now)
+  const float* sr = Si + col0 + (lane & 31);
 #pragma unroll
-    for (int uu = 0; uu < 4; ++uu) {
-      buf[b & 1][2 * uu] = *reinterpret_cast<const float4*>(src + 16 * uu);
-      buf[b & 1][2 * uu + 1] = *reinterpret_cast<const float4*>(src + 16 * uu + 4);
+  for (int m = 0; m < NM; ++m)
+#pragma unroll
+    for (int x = 0; x < 16; ++x) st[m][x] = sr[true_row(m, x, g2) * DV];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) {
+    if (m > 0) lds_barrier();  // tile m is staged (tile 0 before the iteration's first barrier)
+    const u16* cur = (m & 1) ? buf1 : buf0;
+    f32x16 acc = zero16();
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const bf16x8 ah = ldf(cur, 2 * u, lane), al = ldf(cur, 2 * u + 1, lane);
+      acc = mma32(ah, bh[u], acc);
+      acc = mma32(ah, bl[u], acc);
+      acc = mma32(al, bh[u], acc);
     }
-  };
-  auto load_tile = [&](int m) __attribute__((always_inline)) {
-#pragma unroll
-    for (int x = 0; x < 16; ++x) acc[m & 1][x] = sr[true_row(m, x, g2) * DV];
-  };
-  load_tile(0);
-  load_half(0);
-#pragma unroll
-  for (int b = 0; b < NB; ++b) {
-    const int m = b >> 1;
-    if (b + 1 < NB) {
-      if (((b + 1) & 1) == 0) load_tile(m + 1);
-      load_half(b + 1);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int uu = 0; uu < 4; ++uu) {
-      const int u = 4 * (b & 1) + uu;
-      const float4 a0 = buf[b & 1][2 * uu], a1 = buf[b & 1][2 * uu + 1];
-      f32x16 a;
-      a[0] = a0.x; a[1] = a0.y; a[2] = a0.z; a[3] = a0.w;
-      a[4] = a1.x; a[5] = a1.y; a[6] = a1.z; a[7] = a1.w;
-      bf16x8 ah, al;
-      split_of(a, 0, ah, al);
-      acc[m & 1] = mma32(ah, bh[u], acc[m & 1]);
-      acc[m & 1] = mma32(ah, bl[u], acc[m & 1]);
-      acc[m & 1] = mma32(al, bh[u], acc[m & 1]);
-    }
-    if (b & 1) st[m] = acc[m & 1];
-    __builtin_amdgcn_sched_barrier(0);
+    st[m] += acc;
   }
 }
 
@@ -1004,9 +1099,11 @@ __device__ __forceinline__ void state_wave(const ScanArgs& args, const Chain& ch
       if (active) {
         const int id = (c < 64) ? __builtin_amdgcn_readlane(ch.pre_id, c) : entry_of(ch, c);
         const long ih = static_cast<long>(id) * args.h_v + ch.h;
-        const float e = __expf(args.pool_ld[ih]);
-        compose_entry<DK, DV>(st, args.pool_P + ih * DK * DK, args.pool_S + ih * DK * DV, e,
-                              col0, lane);
+        const float ld = (c < 64) ? __builtin_amdgcn_readlane(__float_as_int(ch.pre_ld), c)
+                                  : __float_as_int(args.pool_ld[ih]);
+        compose_entry<DK, DV>(st, args.pool_S + ih * DK * DV, __expf(__int_as_float(ld)), col0,
+                              lane, reinterpret_cast<const u16*>(smem + LP::O_WL),
+                              reinterpret_cast<const u16*>(smem + LP::O_Q + par * LP::NW * LP::FB));
       }
     } else if (active && ch.batched) {
       // one seam entry per chunk: its state after the seam, then the state
@@ -1122,9 +1219,10 @@ __device__ __forceinline__ void operator_wave(const ScanArgs& args, const Chain&
 // a consumer slot without columns still forms its share of W
 template <int DK, int DV>
 __device__ __forceinline__ void idle_wave(const Chain& ch, unsigned char* smem, int lane,
-                                          int wslot) {
+                                          int wslot, int xb) {
   for (int it = -2; it < ch.nc; ++it) {
     lds_barrier();
+    pass_barriers(ch, it, xb);
     if (it + 1 >= 0 && it + 1 < ch.nc) emit_w<DK>(ch, smem, lane, (it + 1) & 1, w_tile(wslot));
     lds_barrier();
   }
@@ -1213,10 +1311,12 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
   ch.qk_stride = static_cast<long>(args.h_qk) * DK;
   ch.v_stride = static_cast<long>(args.h_v) * DV;
   ch.pre_t = ch.pre_n = ch.pre_id = 0;
+  ch.pre_ld = 0.f;
   if (ch.batched && lane < ch.nc) {
     ch.pre_t = entry_start(ch, lane);
     ch.pre_n = entry_len(ch, lane, ch.pre_t);
     ch.pre_id = entry_of(ch, lane);
+    if (FUSED) ch.pre_ld = args.pool_ld[static_cast<long>(ch.pre_id) * args.h_v + ch.h];
   }
   ch.need_state = ch.with_op ? (cb * NCOL < DV) : true;
   ch.need_op = ch.with_op && (cb * NCOL < DK);
@@ -1236,15 +1336,15 @@ __global__ __launch_bounds__(kThreads, 1) void scan_bf16_kernel(ScanArgs args) {
     else if (!state_role && ch.need_op)
       operator_wave<DK, DV>(args, ch, smem, lane, col0, wave);
     else
-      idle_wave<DK, DV>(ch, smem, lane, wave);
+      idle_wave<DK, DV>(ch, smem, lane, wave, compose_barriers<DK>(args));
   } else if (wave == 4) {
-    inverse_wave<DK, DV>(args, ch, smem, lane);
+    inverse_wave<DK, DV, FUSED>(args, ch, smem, lane);
   } else if (wave == 5) {
-    producer_qk_wave<DK, DV>(args, ch, smem, lane);
+    producer_qk_wave<DK, DV, FUSED>(args, ch, smem, lane);
   } else if (wave == 6) {
-    producer_kt_wave<DK, DV, 0>(args, ch, smem, lane);
+    producer_kt_wave<DK, DV, 0, FUSED>(args, ch, smem, lane);
   } else {
-    producer_kt_wave<DK, DV, 1>(args, ch, smem, lane);
+    producer_kt_wave<DK, DV, 1, FUSED>(args, ch, smem, lane);
   }
 }
 
