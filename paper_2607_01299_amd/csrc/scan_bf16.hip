@@ -257,7 +257,7 @@ __device__ __forceinline__ int chunk_len(const Chain& ch, int c) {
 }
 
 // The fused composition (mode 2) adds DK / 32 - 1 barriers to every iteration
-// that composes an entry (compose_entry): the four producer waves stage P_hat's
+// that composes an entry (compose_entry): three producer waves stage P_hat's
 // A operands into LDS one output tile at a time, the first before the
 // iteration's first barrier and each later one before a barrier of its own
 // (producer_compose_first, producer_compose), and a wave without a part in it
@@ -271,21 +271,27 @@ __device__ __forceinline__ void pass_barriers(const Chain& ch, int it, int n) {
     for (int i = 0; i < n; ++i) lds_barrier();
 }
 
-// A producer wave's share of one entry's P_hat A operands: for every output
-// tile m (32 rows, order rho) the steps u = US p .. US p + US - 1 (p = wave -
-// 4, US = d_k / 64) of lane (g2, r): true row rho^-1(32 m + r), true columns
-// 16 u + 8 g2 .. +7 in float32.  A ring of D tiles: the first D are loaded an
-// iteration before they are staged, each later one D rounds before.
-template <int DK>
+// A stager's share of one entry's P_hat A operands: for every output tile m
+// (32 rows, order rho) the steps u = FIRST .. FIRST + US - 1 of lane (g2, r):
+// true row rho^-1(32 m + r), true columns 16 u + 8 g2 .. +7 in float32.  The
+// stagers are the Q K producer (SLOT 0) and the two K^T producers (SLOT 1, 2);
+// the inverse wave, the one with no registers to spare, takes no share.  A
+// ring of D tiles: the first D are loaded an iteration before they are staged,
+// each later one D rounds before.
+template <int DK, int SLOT>
 struct PShare {
-  static constexpr int NM = DK / 32, US = DK / 64, D = (NM < 2) ? NM : 2;
+  static constexpr int NM = DK / 32, NU = DK / 16, D = (NM < 2) ? NM : 2;
+  // steps per stager: 2, 3, 3 at d_k = 128; 1, 2, 1 at d_k = 64
+  static constexpr int US = (NU == 8) ? (SLOT == 0 ? 2 : 3) : (SLOT == 1 ? 2 : 1);
+  static constexpr int FIRST = (NU == 8) ? (SLOT == 0 ? 0 : (SLOT == 1 ? 2 : 5))
+                                         : (SLOT == 0 ? 0 : (SLOT == 1 ? 1 : 3));
   float4 p[D][US][2];
   const float* pr;  // this lane's first element of the entry's share
 };
 
-template <int DK>
-__device__ __forceinline__ void share_load_tile(PShare<DK>& sh, int m) {
-  constexpr int US = PShare<DK>::US, D = PShare<DK>::D;
+template <int DK, int SLOT>
+__device__ __forceinline__ void share_load_tile(PShare<DK, SLOT>& sh, int m) {
+  constexpr int US = PShare<DK, SLOT>::US, D = PShare<DK, SLOT>::D;
 #pragma unroll
   for (int k = 0; k < US; ++k) {
     sh.p[m % D][k][0] = *reinterpret_cast<const float4*>(sh.pr + 32 * m * DK + 16 * k);
@@ -293,17 +299,17 @@ __device__ __forceinline__ void share_load_tile(PShare<DK>& sh, int m) {
   }
 }
 
-template <int DK>
-__device__ __forceinline__ void share_load(PShare<DK>& sh, const ScanArgs& args, const Chain& ch,
-                                           int c, int pslot, int lane) {
-  constexpr int US = PShare<DK>::US, D = PShare<DK>::D;
+template <int DK, int SLOT>
+__device__ __forceinline__ void share_load(PShare<DK, SLOT>& sh, const ScanArgs& args,
+                                           const Chain& ch, int c, int lane) {
+  constexpr int D = PShare<DK, SLOT>::D, FIRST = PShare<DK, SLOT>::FIRST;
   const int id = (c < 64) ? __builtin_amdgcn_readlane(ch.pre_id, c) : entry_of(ch, c);
   const int g2 = lane >> 5, n32 = lane & 31;
   const int prow = (n32 & ~12) | ((n32 & 4) << 1) | ((n32 & 8) >> 1);  // rho -> true row
   sh.pr = args.pool_P + (static_cast<long>(id) * args.h_v + ch.h) * DK * DK + prow * DK +
-          8 * g2 + 16 * US * pslot;
+          8 * g2 + 16 * FIRST;
 #pragma unroll
-  for (int m = 0; m < D; ++m) share_load_tile<DK>(sh, m);
+  for (int m = 0; m < D; ++m) share_load_tile<DK, SLOT>(sh, m);
 }
 
 // Stage output tile m's share, split into bf16 hi + lo, as fragments 2u (hi)
@@ -311,11 +317,12 @@ __device__ __forceinline__ void share_load(PShare<DK>& sh, const ScanArgs& args,
 // ring.  The buffers are regions idle during a fused composition: W lo (no
 // operator columns) and the Q fragments of chunk c (free once the iteration's
 // first barrier has passed, so tile 0, staged before it, goes to W lo).
-template <int DK>
-__device__ __forceinline__ void share_stage(PShare<DK>& sh, unsigned char* smem, int par, int m,
-                                            int pslot, int lane) {
+template <int DK, int SLOT>
+__device__ __forceinline__ void share_stage(PShare<DK, SLOT>& sh, unsigned char* smem, int par,
+                                            int m, int lane) {
   using LP = Lds<DK>;
-  constexpr int NM = PShare<DK>::NM, US = PShare<DK>::US, D = PShare<DK>::D;
+  constexpr int NM = PShare<DK, SLOT>::NM, US = PShare<DK, SLOT>::US, D = PShare<DK, SLOT>::D;
+  constexpr int FIRST = PShare<DK, SLOT>::FIRST;
   u16* buf = reinterpret_cast<u16*>((m & 1) ? smem + LP::O_Q + par * LP::NW * LP::FB
                                             : smem + LP::O_WL);
 #pragma unroll
@@ -326,40 +333,38 @@ __device__ __forceinline__ void share_stage(PShare<DK>& sh, unsigned char* smem,
     a[4] = p1.x; a[5] = p1.y; a[6] = p1.z; a[7] = p1.w;
     bf16x8 ah, al;
     split_of(a, 0, ah, al);
-    const int u = US * pslot + k;
-    stf(buf, 2 * u, lane, ah);
-    stf(buf, 2 * u + 1, lane, al);
+    stf(buf, 2 * (FIRST + k), lane, ah);
+    stf(buf, 2 * (FIRST + k) + 1, lane, al);
   }
-  if (m + D < NM) share_load_tile<DK>(sh, m + D);
+  if (m + D < NM) share_load_tile<DK, SLOT>(sh, m + D);
 }
 
-// A producer wave's part of the fused composition of entry it: tile 0 at the
-// start of the iteration (before its first barrier, so the state waves can
-// multiply it as soon as they reach it) ...
-template <int DK, bool FUSED>
-__device__ __forceinline__ void producer_compose_first(PShare<DK>& sh, const Chain& ch,
-                                                       unsigned char* smem, int it, int pslot,
-                                                       int lane) {
+// A stager's part of the fused composition of entry it: tile 0 at the start of
+// the iteration (before its first barrier, so the state waves can multiply it
+// as soon as they reach it) ...
+template <int DK, int SLOT, bool FUSED>
+__device__ __forceinline__ void producer_compose_first(PShare<DK, SLOT>& sh, const Chain& ch,
+                                                       unsigned char* smem, int it, int lane) {
   if constexpr (FUSED) {
-    if (it >= 0 && it < ch.nc) share_stage<DK>(sh, smem, it & 1, 0, pslot, lane);
+    if (it >= 0 && it < ch.nc) share_stage<DK, SLOT>(sh, smem, it & 1, 0, lane);
   }
 }
 
 // ... and at its end the later tiles, one per barrier, then the loads of entry
 // it + 1's first tiles.
-template <int DK, bool FUSED>
-__device__ __forceinline__ void producer_compose(PShare<DK>& sh, const ScanArgs& args,
+template <int DK, int SLOT, bool FUSED>
+__device__ __forceinline__ void producer_compose(PShare<DK, SLOT>& sh, const ScanArgs& args,
                                                  const Chain& ch, unsigned char* smem, int it,
-                                                 int pslot, int lane) {
+                                                 int lane) {
   if constexpr (FUSED) {
     if (it >= 0 && it < ch.nc) {
 #pragma unroll
-      for (int m = 1; m < PShare<DK>::NM; ++m) {
-        share_stage<DK>(sh, smem, it & 1, m, pslot, lane);
+      for (int m = 1; m < PShare<DK, SLOT>::NM; ++m) {
+        share_stage<DK, SLOT>(sh, smem, it & 1, m, lane);
         lds_barrier();
       }
     }
-    if (it + 1 >= 0 && it + 1 < ch.nc) share_load<DK>(sh, args, ch, it + 1, pslot, lane);
+    if (it + 1 >= 0 && it + 1 < ch.nc) share_load<DK, SLOT>(sh, args, ch, it + 1, lane);
   }
 }
 
@@ -417,7 +422,6 @@ template <int DK, int DV, bool FUSED>
 __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& ch,
                                              unsigned char* smem, int lane) {
   using LP = Lds<DK>;
-  PShare<DK> psh;  // fused composition: this wave's share of the next entry's P_hat
   constexpr int KTD = DK / 32;
   const int g = lane >> 4, n16 = lane & 15;
   float* bs = reinterpret_cast<float*>(smem + LP::O_BS);
@@ -465,7 +469,6 @@ __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& 
   }
 
   for (int it = -2; it < ch.nc; ++it) {
-    producer_compose_first<DK, FUSED>(psh, ch, smem, it, 0, lane);
     const int c = it + 2;
     const bool active = c < ch.nc;
     f32x4 gu[6];      // upper Gram tiles (k, i), k < i: rows of L_ik once scaled by beta
@@ -569,7 +572,7 @@ __device__ __forceinline__ void inverse_wave(const ScanArgs& args, const Chain& 
       emit(af, 3, 1, -mma16_x3(T31, R3, zero4()));
       emit(af, 3, 0, -mma16_x3(T30, R3, zero4()));
     }
-    producer_compose<DK, FUSED>(psh, args, ch, smem, it, 0, lane);
+    pass_barriers(ch, it, compose_barriers<DK>(args));
     lds_barrier();
   }
 }
@@ -652,7 +655,7 @@ template <int DK, int DV, bool FUSED>
 __device__ __forceinline__ void producer_qk_wave(const ScanArgs& args, const Chain& ch,
                                                  unsigned char* smem, int lane) {
   using LP = Lds<DK>;
-  PShare<DK> psh;  // fused composition: this wave's share of the next entry's P_hat
+  PShare<DK, 0> psh;  // fused composition: this wave's share of the next entry's P_hat
   constexpr int NU = DK / 16;
   constexpr int KTD = DK / 32;
   const int g = lane >> 4, n16 = lane & 15;
@@ -682,7 +685,7 @@ __device__ __forceinline__ void producer_qk_wave(const ScanArgs& args, const Cha
   if (ch.nc > 0) prefetch(0);
 
   for (int it = -2; it < ch.nc; ++it) {
-    producer_compose_first<DK, FUSED>(psh, ch, smem, it, 1, lane);
+    producer_compose_first<DK, 0, FUSED>(psh, ch, smem, it, lane);
     const int p = it + 1;
     const bool active = p >= 0 && p < ch.nc;
     const int par = p & 1;
@@ -764,7 +767,7 @@ __device__ __forceinline__ void producer_qk_wave(const ScanArgs& args, const Cha
         }
       }
     }
-    producer_compose<DK, FUSED>(psh, args, ch, smem, it, 1, lane);
+    producer_compose<DK, 0, FUSED>(psh, args, ch, smem, it, lane);
     lds_barrier();
   }
 }
@@ -775,7 +778,7 @@ template <int DK, int DV, int HALF, bool FUSED>
 __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Chain& ch,
                                                  unsigned char* smem, int lane) {
   using LP = Lds<DK>;
-  PShare<DK> psh;  // fused composition: this wave's share of the next entry's P_hat
+  PShare<DK, 1 + HALF> psh;  // fused composition: this wave's share of the next entry's P_hat
   constexpr int NH = DK / 64;  // 32-wide d_k blocks of this half
   const int g = lane >> 4, n16 = lane & 15;
   const int g2 = lane >> 5, n32 = lane & 31;
@@ -802,7 +805,7 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
   if (ch.nc > 0) prefetch(0);
 
   for (int it = -2; it < ch.nc; ++it) {
-    producer_compose_first<DK, FUSED>(psh, ch, smem, it, 2 + HALF, lane);
+    producer_compose_first<DK, 1 + HALF, FUSED>(psh, ch, smem, it, lane);
     const int p = it + 1;
     const bool active = p >= 0 && p < ch.nc;
     const int par = p & 1;
@@ -882,7 +885,7 @@ __device__ __forceinline__ void producer_kt_wave(const ScanArgs& args, const Cha
       }
       emit_w<DK>(ch, smem, lane, par, 1 + 2 * HALF);
     }
-    producer_compose<DK, FUSED>(psh, args, ch, smem, it, 2 + HALF, lane);
+    producer_compose<DK, 1 + HALF, FUSED>(psh, args, ch, smem, it, lane);
     lds_barrier();
   }
 }
