@@ -134,3 +134,36 @@ def test_kda_build_mixed_dims(hy, d_k, d_v):
     ref = K.kda_build_segments(w["q"], w["k"], w["v"], w["beta"], gate, w["cu"])
     _compare(res, ref, w["cu"], ("o", "S_seg", "P_hat", "log_decay"), TOL[W.BF16],
              "kda %dx%d" % (d_k, d_v), kda_gate=gate)
+
+
+@pytest.mark.parametrize("d_k,d_v", DIMS)
+def test_compose_and_rescan_mixed_dims(hy, d_k, d_v):
+    """The one-pass composition with seams (Sec. 4.3, Eq. (6)) at unequal
+    widths: d_v = 64 leaves two of the four column slots idle (they pass the
+    composition's barriers), d_k = 64 stages two output tiles instead of four."""
+    import oracle
+    _say("compose and rescan bf16 d_k=%d d_v=%d" % (d_k, d_v))
+    w, dev = _tokens(d_k, d_v, W.BF16, 46)
+    cu = w["cu"]
+    res = hy.build_segment(dev["q"], dev["k"], dev["v"], dev["beta"], dev["log_alpha"], cu)
+    ids = np.array([1, 0, 2, 1, 2, 0], dtype=np.int32)
+    offs = np.array([0, 2, 2, 6], dtype=np.int32)  # the second request is empty
+    seam_w = 64
+    S_out, o_seam = hy.compose_and_rescan(res["P_hat"], res["log_decay"], res["S_seg"], dev["q"],
+                                          dev["k"], dev["v"], dev["beta"], dev["log_alpha"],
+                                          cu[:-1], np.diff(cu), seam_w, ids, offs)
+    torch.cuda.synchronize()
+    P, ld, S = _np(res["P_hat"]), _np(res["log_decay"]), _np(res["S_seg"])
+    R_out, R_inc = oracle.compose(P, ld, S, ids, offs)
+    R_o, _ = oracle.seam(w["q"], w["k"], w["v"], w["beta"], w["log_alpha"], cu[:-1][ids],
+                         np.diff(cu)[ids], seam_w, R_inc)
+    So, og = _np(S_out), _np(o_seam)
+    ws = max(rel(So[r, h], R_out[r, h]) for r in range(3) for h in range(4))
+    wo = 0.0
+    for j in range(len(ids)):
+        wj = min(seam_w, LENGTHS[ids[j]])
+        for h in range(4):
+            wo = max(wo, rel(og[j, :wj, h], R_o[j, :wj, h]))
+    print("compose and rescan %dx%d: state %.2e, seam outputs %.2e" % (d_k, d_v, ws, wo),
+          flush=True)
+    assert ws <= 1e-4 and wo <= 1e-2
