@@ -15,8 +15,8 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhypic.so")
 
-SOURCES = ["scan.hip", "scan_bf16.hip", "compose.hip", "family.hip", "kda.hip", "adjacent.hip",
-           "seam_advance.hip", "noalloc.hip", "api.cpp"]
+SOURCES = ["scan.hip", "scan_bf16.hip", "compose.hip", "family.hip", "kda.hip", "gated_pipe.hip",
+           "adjacent.hip", "seam_advance.hip", "noalloc.hip", "api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

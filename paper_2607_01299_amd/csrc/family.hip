@@ -921,6 +921,8 @@ hipError_t launch_family_scan(const FamArgs& a, int family, int bf16, int d_k, i
   const int64_t n_items = static_cast<int64_t>(n_chains) * a.h_v * (d_v / fnc);
   if (n_items > 0x7fffffff) return hipErrorInvalidValue;
   const int n = static_cast<int>(n_items);
+  if (family == FAM_DIAGONAL && diag_pipe_supported(bf16, d_k, d_v, a.mode))
+    return launch_diag_pipe(a, d_v, n_chains, s);
   // scalar family, bf16 inputs: the software-pipelined kernel (64-column blocks)
   if (family == FAM_DIAGONAL)
     return bf16 ? launch_fscan_d<FAM_DIAGONAL, uint16_t>(a, d_k, d_v, n, s)

@@ -81,6 +81,7 @@ CASES = [
     ("diagonal", W.F32, 64, (1, 2), "softplus"),
     ("diagonal", W.BF16, 128, (2, 4), "softplus"),
     ("diagonal", W.BF16, 64, (2, 2), "logsigmoid"),
+    ("diagonal", W.BF16, 128, (2, 2), "logsigmoid"),
     ("diagonal", W.F32, 128, (2, 2), "logsigmoid"),
 ]
 
