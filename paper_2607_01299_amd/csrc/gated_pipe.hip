@@ -27,20 +27,23 @@
 // Organisation.  One workgroup of 8 waves runs one (segment, v-head,
 // 64-column block) chain, software-pipelined two deep:
 //   waves 0-1  state columns (32 each) of chunk c: outputs and the state update
-//   waves 2-3  HBM loads: the q, k and gate rows of chunk c + 2, staged into
-//              LDS for the producers once they are done with chunk c + 1's
-//   waves 4-7  chunk c + 1, one 32-channel slice of d_k each: gate prefix (DPP
-//              row scans), the exponentials, the gate-scaled operands, their
+//   waves 2-3  HBM loads, half a chunk each: the q, k and gate rows of chunk
+//              c + 2, staged into LDS once the producers hold chunk c + 1's;
+//              the gates are turned into their in-tile prefix on the way, and
+//              the segment's log_decay summed
+//   waves 4-7  chunk c + 1, one 32-channel slice of d_k each: the exponentials
+//              of the staged gate prefix, the gate-scaled operands, their
 //              share of the score tiles (one 32-deep contraction step each),
 //              (Q . exp(B)) and (K . exp(B_last - B))^T of their channels, and
 //              the row decays exp(B_last).  Each leaves its partial score
 //              tiles in an LDS slab; after R1 each sums a quarter of the tiles.
-// One barrier before the loop (chunk 0 staged), then three LDS-only barriers
-// per iteration: R1 (partial scores written, staging free), B1 (the
-// state waves are done with chunk c), B2 (chunk c + 1's operands written).
-// The state waves read the outputs' operands (Q . exp(B), A) before R1 and the
-// state update's between R1 and B1; the producers write chunk c + 1's after
-// R1 and after B1 respectively, so every operand buffer is single.
+// One barrier before the loop (chunk 0 staged), three LDS-only barriers per
+// iteration: R0 (the producers hold chunk c + 1's staged rows in registers, so
+// the staging area takes chunk c + 2's), R1 (partial scores written; the
+// state waves are done with chunk c's operands), B2 (chunk c + 1's operands
+// written), and one after the loop.  Every operand buffer is single: the
+// state waves read chunk c's before R1, the producers write chunk c + 1's
+// after it.
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -138,25 +141,15 @@ __device__ __forceinline__ void producer_wave(const FamArgs& args, const Chain& 
   }
 
   lds_barrier();  // P0: chunk 0 is staged
-  float lsum[8];  // this lane row's channel gate sums over the segment (log2 units)
-#pragma unroll
-  for (int j = 0; j < 8; ++j) lsum[j] = 0.f;
 
   for (int it = -1; it < ch.nc; ++it) {
     const int p = it + 1;
     const bool active = p < ch.nc;
-    uint4 qe[4];        // Q . exp(B) of tile t, bf16
-    u16x4 kd[4][2];     // (K . exp(B_last - B))^T tiles (token tile t, rho half h)
-    float rdv[8];       // exp(B_last) of this lane row's channels
+    // lane (g, r) of tile t: token 16t + r, channels 32u + 8g .. +7, from
+    // the staged rows (rows past the chunk hold a repeated row: masked)
+    uint4 kr[4], qr[4];
+    float4 gr[4][2];
     if (active) {
-      const int n = chunk_len(ch, p);
-      bool keep[4];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) keep[t] = 16 * t + r < n;
-      // lane (g, r) of tile t: token 16t + r, channels 32u + 8g .. +7, from
-      // the staged rows (rows past the chunk hold a repeated row: masked)
-      uint4 kr[4], qr[4];
-      float4 gr[4][2];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const int tok = 16 * t + r;
@@ -165,10 +158,21 @@ __device__ __forceinline__ void producer_wave(const FamArgs& args, const Chain& 
         gr[t][0] = *reinterpret_cast<const float4*>(sgt + tok * LP::RG);
         gr[t][1] = *reinterpret_cast<const float4*>(sgt + tok * LP::RG + 16);
       }
-      // Per tile: the in-tile inclusive prefix x of the gate (log2 units;
-      // tokens past the chunk carry no gate), exp(x) for the query side, the
-      // key side referred to the tile's start, k_i exp(-x_i), and the tile
-      // factor F_t = exp(s_{t+1} - s_t), exp(x) of the tile's last token
+    }
+    lds_barrier();  // R0: the staged rows are in registers
+    uint4 qe[4];        // Q . exp(B) of tile t, bf16
+    u16x4 kd[4][2];     // (K . exp(B_last - B))^T tiles (token tile t, rho half h)
+    float rdv[8];       // exp(B_last) of this lane row's channels
+    if (active) {
+      const int n = chunk_len(ch, p);
+      bool keep[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) keep[t] = 16 * t + r < n;
+
+      // Per tile, from the staged in-tile prefix x of the gate (log2 units):
+      // exp(x) for the query side, the key side referred to the tile's start,
+      // k_i exp(-x_i), and the tile factor F_t = exp(s_{t+1} - s_t), exp(x) of
+      // the tile's last token
       float E[4][8], kk[4][8];
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
@@ -179,11 +183,9 @@ __device__ __forceinline__ void producer_wave(const FamArgs& args, const Chain& 
         unpack8(mask4(kr[t], keep[t]), kf);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const float x = row_scan16(keep[t] ? gv[j] * kLog2e : 0.f);
-          E[t][j] = __builtin_amdgcn_exp2f(x);
-          kk[t][j] = kf[j] * __builtin_amdgcn_exp2f(-x);
+          E[t][j] = __builtin_amdgcn_exp2f(gv[j]);
+          kk[t][j] = kf[j] * __builtin_amdgcn_exp2f(-gv[j]);
           F[j] = row_last(E[t][j]);
-          lsum[j] += row_last(x);
         }
         if (r == 0) {
           *reinterpret_cast<float4*>(tf + 8 * t) = make_float4(F[0], F[1], F[2], F[3]);
@@ -261,7 +263,7 @@ __device__ __forceinline__ void producer_wave(const FamArgs& args, const Chain& 
       for (int j = 0; j < 8; ++j) rdv[j] = d[j];  // exp(B_last)
     }
     lds_barrier();  // R1: the partial score tiles are written; the state
-                    // waves are done with chunk c's Q . exp(B) and A
+                    // waves are done with chunk c's operands
     if (active) {
       // Q . exp(B) fragments: the 16 bytes of lane (g, r) of tile (t, u) are
       // slot group g%2 of lane 16(t%2) + r of fragment (t/2, 2u + g/2)
@@ -289,9 +291,6 @@ __device__ __forceinline__ void producer_wave(const FamArgs& args, const Chain& 
           *reinterpret_cast<u16x4*>(fQK + scatter_off(tri_idx(tq >> 1, tk), tq & 1, lane)) =
               pack4(v[0], v[1], v[2], v[3]);
         }
-    }
-    lds_barrier();  // B1: the state waves are done with chunk c
-    if (active) {
       // the transposed decayed keys: fragment (rho tile u, token step t)
 #pragma unroll
       for (int t = 0; t < 4; ++t)
@@ -306,11 +305,7 @@ __device__ __forceinline__ void producer_wave(const FamArgs& args, const Chain& 
     }
     lds_barrier();  // B2
   }
-  if (args.log_decay != nullptr && ch.cb == 0 && r == 0) {
-    float* ld = args.log_decay + ch.sh * DK + 32 * u + 8 * g;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) ld[j] = lsum[j] * kLn2;
-  }
+  lds_barrier();  // E0
 }
 
 // =============================================================================
@@ -354,6 +349,7 @@ __device__ __forceinline__ void state_wave(const FamArgs& args, const Chain& ch,
   for (int it = -1; it < ch.nc; ++it) {
     const int c = it;
     const bool active = c >= 0;
+    lds_barrier();  // R0
     bf16x8 vB[4];  // V (this wave's columns) as fragments over tokens
     if (active) {
       const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
@@ -395,7 +391,6 @@ __device__ __forceinline__ void state_wave(const FamArgs& args, const Chain& ch,
         }
       }
     }
-    lds_barrier();  // R1
     if (active) {
       // S <- exp(B_last) . S0 + (K . exp(B_last - B))^T V
 #pragma unroll
@@ -415,9 +410,10 @@ __device__ __forceinline__ void state_wave(const FamArgs& args, const Chain& ch,
         st[m] = acc;
       }
     }
-    lds_barrier();  // B1
+    lds_barrier();  // R1
     lds_barrier();  // B2
   }
+  lds_barrier();  // E0
 
   if (args.S_out != nullptr) {
     float* so = args.S_out + ch.sh * DK * DV + col0 + n32;
@@ -429,77 +425,112 @@ __device__ __forceinline__ void state_wave(const FamArgs& args, const Chain& ch,
 }
 
 // =============================================================================
-// waves 2-3: HBM loads two chunks ahead, staged into LDS one chunk ahead
+// waves 2-3: HBM loads, staged into LDS
 // =============================================================================
-// Loads of one chunk's rows into registers and their staging into LDS.
-// QK: the q and k rows of the chain's q/k head, 4 rows of 256 bytes per
-// instruction; otherwise the gate rows of its v-head, 2 rows of 512 bytes.
-template <bool QK>
+// Loader w takes tokens 32w .. 32w + 31 of a chunk: its q and k rows (4 rows
+// of 256 bytes per instruction) and its gate rows, lanes 0-31 tile 2w and
+// lanes 32-63 tile 2w + 1 (one token of each per instruction, 4 channels a
+// lane), so that every load reads whole rows and each lane holds whole tiles
+// of its channels.
 __device__ __forceinline__ void loader_load(u32x4 (&buf)[32], const FamArgs& args,
-                                            const Chain& ch, int c, int lane) {
+                                            const Chain& ch, int c, int lane, int w) {
   const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
-  if constexpr (QK) {
-    const u16* kb = static_cast<const u16*>(args.k) + ch.hk * DK + 8 * (lane & 15);
-    const u16* qb = static_cast<const u16*>(args.q) + ch.hk * DK + 8 * (lane & 15);
+  const u16* kb = static_cast<const u16*>(args.k) + ch.hk * DK + 8 * (lane & 15);
+  const u16* qb = static_cast<const u16*>(args.q) + ch.hk * DK + 8 * (lane & 15);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int tok = 4 * i + (lane >> 4);
-      const long row = c0 + ((tok < n) ? tok : n - 1);
-      buf[i] = *reinterpret_cast<const u32x4*>(kb + row * ch.qk_stride);
-      buf[16 + i] = *reinterpret_cast<const u32x4*>(qb + row * ch.qk_stride);
-    }
-  } else {
-    const float* gb = args.gate + static_cast<long>(ch.h) * DK + 4 * (lane & 31);
-    const long gs = static_cast<long>(args.h_v) * DK;
-#pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const int tok = 2 * i + (lane >> 5);
-      const long row = c0 + ((tok < n) ? tok : n - 1);
-      buf[i] = *reinterpret_cast<const u32x4*>(gb + row * gs);
-    }
+  for (int i = 0; i < 8; ++i) {
+    const int tok = 32 * w + 4 * i + (lane >> 4);
+    const long row = c0 + ((tok < n) ? tok : n - 1);
+    buf[i] = *reinterpret_cast<const u32x4*>(kb + row * ch.qk_stride);
+    buf[8 + i] = *reinterpret_cast<const u32x4*>(qb + row * ch.qk_stride);
   }
-}
-template <bool QK>
-__device__ __forceinline__ void loader_stage(const u32x4 (&buf)[32], unsigned char* smem,
-                                             int lane) {
-  using LP = Lds;
-  if constexpr (QK) {
+  const float* gb = args.gate + static_cast<long>(ch.h) * DK + 4 * (lane & 31);
+  const long gs = static_cast<long>(args.h_v) * DK;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int off = (4 * i + (lane >> 4)) * LP::RQK + 16 * (lane & 15);
-      *reinterpret_cast<u32x4*>(smem + LP::O_SK + off) = buf[i];
-      *reinterpret_cast<u32x4*>(smem + LP::O_SQ + off) = buf[16 + i];
-    }
-  } else {
-#pragma unroll
-    for (int i = 0; i < 32; ++i) {
-      const int off = (2 * i + (lane >> 5)) * LP::RG + 16 * (lane & 31);
-      *reinterpret_cast<u32x4*>(smem + LP::O_SG + off) = buf[i];
-    }
+  for (int i = 0; i < 16; ++i) {
+    const int tok = 32 * w + 16 * (lane >> 5) + i;
+    const long row = c0 + ((tok < n) ? tok : n - 1);
+    buf[16 + i] = *reinterpret_cast<const u32x4*>(gb + row * gs);
   }
 }
 
-// Wave 2 moves the q and k rows (QK), wave 3 the gate rows: every load
-// instruction reads whole rows.  Chunk c + 2's rows are loaded at the start of
-// iteration c, while the producers work on chunk c + 1 (a load can wait at
-// issue while the memory system is busy; this wave has nothing else to do),
-// staged once they have read chunk c + 1's (after R1) and read by them after
-// B2.
-template <bool QK>
+// The gate rows in place as the in-tile inclusive prefix of the gate (log2
+// units; tokens past the chunk carry none), and the tile's channel sums added
+// to lsum.
+__device__ __forceinline__ void gate_prefix(u32x4 (&buf)[32], float (&lsum)[4], int n, int lane,
+                                            int w) {
+  float run[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const bool keep = 32 * w + 16 * (lane >> 5) + i < n;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      run[e] += keep ? __uint_as_float(buf[16 + i][e]) * kLog2e : 0.f;
+      buf[16 + i][e] = __float_as_uint(run[e]);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) lsum[e] += run[e];
+}
+
+__device__ __forceinline__ void loader_stage(const u32x4 (&buf)[32], unsigned char* smem,
+                                             int lane, int w) {
+  using LP = Lds;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int off = (32 * w + 4 * i + (lane >> 4)) * LP::RQK + 16 * (lane & 15);
+    *reinterpret_cast<u32x4*>(smem + LP::O_SK + off) = buf[i];
+    *reinterpret_cast<u32x4*>(smem + LP::O_SQ + off) = buf[8 + i];
+  }
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int off = (32 * w + 16 * (lane >> 5) + i) * LP::RG + 16 * (lane & 31);
+    *reinterpret_cast<u32x4*>(smem + LP::O_SG + off) = buf[16 + i];
+  }
+}
+
+// A chunk's rows are loaded an iteration before they are staged (a load can
+// wait at issue while the memory system is busy; this wave has nothing else to
+// do) and their gate prefix formed between R1 and B2, when the producers'
+// own arithmetic is done.  Chunk c + 2 is staged in iteration c once the
+// producers have moved chunk c + 1's rows into registers (R0), and read by
+// them after B2.
 __device__ __forceinline__ void loader_wave(const FamArgs& args, const Chain& ch,
-                                            unsigned char* smem, int lane) {
+                                            unsigned char* smem, int lane, int w) {
   u32x4 buf[32];
+  float lsum[4] = {0.f, 0.f, 0.f, 0.f};  // this lane's tile of its channels, summed (log2 units)
   if (ch.nc > 0) {
-    loader_load<QK>(buf, args, ch, 0, lane);
-    loader_stage<QK>(buf, smem, lane);
+    loader_load(buf, args, ch, 0, lane, w);
+    gate_prefix(buf, lsum, chunk_len(ch, 0), lane, w);
+    loader_stage(buf, smem, lane, w);
+    if (ch.nc > 1) loader_load(buf, args, ch, 1, lane, w);
   }
   lds_barrier();  // P0
+  if (ch.nc > 1) gate_prefix(buf, lsum, chunk_len(ch, 1), lane, w);
   for (int it = -1; it < ch.nc; ++it) {
-    if (it + 2 < ch.nc) loader_load<QK>(buf, args, ch, it + 2, lane);
-    lds_barrier();  // R1: the producers are done with the staged chunk it + 1
-    if (it + 2 < ch.nc) loader_stage<QK>(buf, smem, lane);
-    lds_barrier();  // B1
+    lds_barrier();  // R0: the producers hold chunk it + 1's rows
+    if (it + 2 < ch.nc) {
+      loader_stage(buf, smem, lane, w);
+      if (it + 3 < ch.nc) loader_load(buf, args, ch, it + 3, lane, w);
+    }
+    lds_barrier();  // R1
+    // the gate prefix of the rows just loaded, while the producers store
+    if (it + 3 < ch.nc) gate_prefix(buf, lsum, chunk_len(ch, it + 3), lane, w);
     lds_barrier();  // B2
+  }
+  // the segment's per-channel gate sums: lanes l and l + 32 of the two
+  // loaders hold the four tiles of channels 4(l % 32) .. +3
+  float* part = reinterpret_cast<float*>(smem + Lds::O_SL);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) lsum[e] += __shfl_xor(lsum[e], 32, 64);
+  if (w == 1 && lane < 32)
+    *reinterpret_cast<float4*>(part + 4 * lane) = make_float4(lsum[0], lsum[1], lsum[2], lsum[3]);
+  lds_barrier();  // E0
+  if (w == 0 && lane < 32 && args.log_decay != nullptr && ch.cb == 0) {
+    const float4 o = *reinterpret_cast<const float4*>(part + 4 * lane);
+    float* ld = args.log_decay + ch.sh * DK + 4 * lane;
+    *reinterpret_cast<float4*>(ld) = make_float4((lsum[0] + o.x) * kLn2, (lsum[1] + o.y) * kLn2,
+                                                 (lsum[2] + o.z) * kLn2, (lsum[3] + o.w) * kLn2);
   }
 }
 
@@ -552,10 +583,8 @@ __global__ __launch_bounds__(kThreads, 1) void diag_pipe_kernel(FamArgs args) {
 
   if (wave < 2)
     state_wave<DV>(args, ch, smem, lane, cb * NCOL + 32 * wave);
-  else if (wave == 2)
-    loader_wave<true>(args, ch, smem, lane);
-  else if (wave == 3)
-    loader_wave<false>(args, ch, smem, lane);
+  else if (wave < 4)
+    loader_wave(args, ch, smem, lane, wave - 2);
   else
     producer_wave<DV>(args, ch, smem, lane, wave - 4);
 }
