@@ -85,7 +85,7 @@ KERNEL_SOURCES = {
     "scan_bf16": ["scan_bf16.hip", "mfma.hpp", "scan.hpp"],
     "compose": ["compose.hip", "mfma.hpp", "scan.hpp"],
     "family_scalar_build": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
-    "family_diagonal_build": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
+    "family_diagonal_build": ["gated_pipe.hip", "frag32.hpp", "mfma.hpp", "family.hpp", "scan.hpp"],
     "family_scalar_compose": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
     "family_diagonal_compose": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
     "kda_build": ["kda.hip", "kda.hpp", "scan.hpp", "mfma.hpp", "frag_common.hpp"],
@@ -603,7 +603,7 @@ def bench_families(torch, steps, warmup, seam_w):
                               "to frac_algorithmic"})
         broof = hbm_roofline(byts, build_ms, "family_%s_build" % family, FAMILY_WORKLOAD)
         broof["kernel"] = ("family_pipe_kernel (build)" if family == "scalar"
-                           else "family_scan_kernel (build)")
+                           else "diag_pipe_kernel (build)")
         out[family] = {
             "tokens_per_s": T / dt,
             "ms_per_step": dt * 1e3,

@@ -667,27 +667,41 @@ __global__ __launch_bounds__(512) void family_pipe_kernel(FamArgs args) {
     // 2 rp + 1 of one 8-column group, items running over the groups fastest
     // (whole rows per load), so the token-minor copies are written as pairs
     const int rpv = ptid / 8, cvv = ptid % 8;  // V: one item
-    auto prefetch = [&](int c0, int n) __attribute__((always_inline)) {
+    // the next chunk's loads, each issued as soon as its registers are free,
+    // so that no single burst waits long at issue
+    auto pf_q = [&](int c0, int n) __attribute__((always_inline)) {
       const auto rsq = rsrc(qg + static_cast<long>(c0) * qk_stride, n * qk_stride * 2);
-      const auto rsk = rsrc(kg + static_cast<long>(c0) * qk_stride, n * qk_stride * 2);
-      const auto rsv = rsrc(vg + static_cast<long>(c0) * v_stride, n * v_stride * 2);
 #pragma unroll
       for (int u = 0; u < NQ; ++u) {
         const int idx = u * PT + ptid;
         const int r = idx / (DK / 8), cv = idx % (DK / 8);
         rq[u] = bload16(rsq, static_cast<int>((r * qk_stride + cv * 8) * 2));
       }
+    };
+    auto pf_k = [&](int c0, int n) __attribute__((always_inline)) {
+      const auto rsk = rsrc(kg + static_cast<long>(c0) * qk_stride, n * qk_stride * 2);
 #pragma unroll
       for (int u = 0; u < NQ; ++u) {
         const int idx = (u >> 1) * PT + ptid;
         const int r = 2 * (idx / (DK / 8)) + (u & 1), cv = idx % (DK / 8);
         rk[u] = bload16(rsk, static_cast<int>((r * qk_stride + cv * 8) * 2));
       }
+    };
+    auto pf_v = [&](int c0, int n) __attribute__((always_inline)) {
+      const auto rsv = rsrc(vg + static_cast<long>(c0) * v_stride, n * v_stride * 2);
 #pragma unroll
       for (int u = 0; u < NV; ++u)
         rv[u] = bload16(rsv, static_cast<int>(((2 * rpv + u) * v_stride + cvv * 8) * 2));
+    };
+    auto pf_g = [&](int c0, int n) __attribute__((always_inline)) {
       const auto rsg = rsrc(args.gate + static_cast<long>(c0) * args.h_v, n * args.h_v * 4);
       rg = bload4(rsg, (lane * args.h_v + h) * 4);
+    };
+    auto prefetch = [&](int c0, int n) __attribute__((always_inline)) {
+      pf_q(c0, n);
+      pf_k(c0, n);
+      pf_v(c0, n);
+      pf_g(c0, n);
     };
     if (nc > 0) prefetch(lo, (hi - lo < FC) ? hi - lo : FC);
     float ld_acc = 0.f;  // log_decay: sum of the chunk gate totals
@@ -696,14 +710,16 @@ __global__ __launch_bounds__(512) void family_pipe_kernel(FamArgs args) {
       const int c0 = lo + p * FC;
       const bool active = p < nc;
       // ---- stage A: stage chunk p, its gate prefix and decayed keys;
-      // prefetch chunk p + 1 ----
+      // prefetch chunk p + 1, part by part ----
       if (active) {
+        const int c1 = c0 + FC, n1 = (hi - c1 < FC) ? hi - c1 : FC;
 #pragma unroll
         for (int u = 0; u < NQ; ++u) {
           const int idx = u * PT + ptid;
           const int r = idx / (DK / 8), cv = idx % (DK / 8);
           *reinterpret_cast<uint4*>(sm.q[buf] + r * LDK + cv * 8) = rq[u];
         }
+        pf_q(c1, n1);
 #pragma unroll
         for (int u = 0; u < NQ; ++u) {
           const int idx = (u >> 1) * PT + ptid;
@@ -715,7 +731,9 @@ __global__ __launch_bounds__(512) void family_pipe_kernel(FamArgs args) {
           *reinterpret_cast<uint32_t*>(sm.vt[buf] + (cvv * 8 + e) * LDT +
                                        ((2 * rpv) ^ (SWV * (cvv >> 1)))) =
               pair_raw(rv[0], rv[1], e);
+        pf_v(c1, n1);
         const float b = wave_inclusive_sum(rg);
+        pf_g(c1, n1);
         const float b_last = __builtin_bit_cast(
             float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, b), 63));
         const float dec = __expf(b_last - b);
@@ -736,8 +754,7 @@ __global__ __launch_bounds__(512) void family_pipe_kernel(FamArgs args) {
                 pack_bf16(elem(rk[2 * j], e, static_cast<const u16*>(nullptr)) * d0,
                           elem(rk[2 * j + 1], e, static_cast<const u16*>(nullptr)) * d1);
         }
-        const int c1 = c0 + FC;
-        prefetch(c1, (hi - c1 < FC) ? hi - c1 : FC);
+        pf_k(c1, n1);
       }
       lds_barrier();
       // ---- stage C: the lower 16 x 16 tiles of A for chunk p ----
