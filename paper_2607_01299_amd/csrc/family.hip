@@ -940,6 +940,8 @@ hipError_t launch_family_scan(const FamArgs& a, int family, int bf16, int d_k, i
   const int n = static_cast<int>(n_items);
   if (family == FAM_DIAGONAL && diag_pipe_supported(bf16, d_k, d_v, a.mode))
     return launch_diag_pipe(a, d_v, n_chains, s);
+  if (family == FAM_SCALAR && diag_pipe_supported(bf16, d_k, d_v, a.mode))
+    return launch_scalar_pipe(a, d_v, n_chains, s);
   // scalar family, bf16 inputs: the software-pipelined kernel (64-column blocks)
   if (family == FAM_DIAGONAL)
     return bf16 ? launch_fscan_d<FAM_DIAGONAL, uint16_t>(a, d_k, d_v, n, s)

@@ -47,10 +47,11 @@ struct FamComposeArgs {
   int32_t h_v;
 };
 
-// The software-pipelined build of the diagonal family (gated_pipe.hip): bf16
-// inputs, d_k = 128, d_v = 64 or 128, segment build only.
+// The software-pipelined builds of the diagonal and scalar families
+// (gated_pipe.hip): bf16 inputs, d_k = 128, d_v = 64 or 128, segment build only.
 bool diag_pipe_supported(int bf16, int d_k, int d_v, int mode);
 hipError_t launch_diag_pipe(const FamArgs& a, int d_v, int n_chains, hipStream_t s);
+hipError_t launch_scalar_pipe(const FamArgs& a, int d_v, int n_chains, hipStream_t s);
 
 hipError_t launch_family_scan(const FamArgs& a, int family, int bf16, int d_k, int d_v,
                               int n_chains, hipStream_t s);

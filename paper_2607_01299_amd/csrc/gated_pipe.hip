@@ -538,19 +538,15 @@ __device__ __forceinline__ int segment_of(const FamArgs& a, int rank) {
   return a.n_inline > 0 ? static_cast<int>(a.order_inline[rank]) : a.order[rank];
 }
 
+// The chain of workgroup blockIdx.x, n_cb workgroups (64-column blocks) per
+// (segment, v-head).  Workgroups are dealt to the 8 XCDs round-robin.  A unit
+// is every workgroup that reads one q/k head's tokens (the column blocks of the
+// group's v-head chains); a unit's workgroups are numbered to land on one XCD
+// back to back, so they share its L2 for q and k; units past the last full
+// group of 8 keep linear order.
 template <int DV>
-__global__ __launch_bounds__(kThreads, 1) void diag_pipe_kernel(FamArgs args) {
-  extern __shared__ __align__(16) unsigned char smem[];
-  const int tid = threadIdx.x;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
-  const int lane = tid & 63;
-
+__device__ __forceinline__ Chain make_chain(const FamArgs& args) {
   constexpr int n_cb = DV / NCOL;
-  // Workgroups are dealt to the 8 XCDs round-robin.  A unit is every
-  // workgroup that reads one q/k head's tokens (the column blocks of the
-  // group's v-head chains); a unit's workgroups are numbered to land on one
-  // XCD back to back, so they share its L2 for q and k; units past the last
-  // full group of 8 keep linear order.
   const int n_chains = static_cast<int>(gridDim.x) / n_cb;
   const int G = args.group;
   const int U = G * n_cb;
@@ -580,6 +576,17 @@ __global__ __launch_bounds__(kThreads, 1) void diag_pipe_kernel(FamArgs args) {
   ch.sh = static_cast<long>(ch.seg) * args.h_v + ch.h;
   ch.qk_stride = static_cast<long>(args.h_qk) * DK;
   ch.v_stride = static_cast<long>(args.h_v) * DV;
+  return ch;
+}
+
+template <int DV>
+__global__ __launch_bounds__(kThreads, 1) void diag_pipe_kernel(FamArgs args) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int lane = tid & 63;
+  const Chain ch = make_chain<DV>(args);
+  const int cb = ch.cb;
 
   if (wave < 2)
     state_wave<DV>(args, ch, smem, lane, cb * NCOL + 32 * wave);
@@ -601,10 +608,403 @@ hipError_t launch_t(const FamArgs& a, int n_items, hipStream_t s) {
   return hipGetLastError();
 }
 
+// #############################################################################
+// The scalar family (RetNet, Lightning-2, Mamba2 rows of Tab. 1):
+//   S_t = exp(a_t) S_{t-1} + k_t v_t^T,   o_t = S_t^T q_t,
+// per chunk (b = prefix of the gate inside the chunk, gamma = exp(b)):
+//   O = diag(gamma) Q S0 + (tril(Q K^T) . Gamma) V,  Gamma_ti = exp(b_t - b_i)
+//   S <- gamma_last S0 + K^T diag(exp(b_last - b)) V.
+// A scalar gate factors out of the scores, so q and k enter the matrix cores
+// exactly and every score tile is one bf16 pass over all of d_k: the producers
+// split the ten tiles among them whole, with no partial sums.  The state waves
+// apply gamma to Q S0 and exp(b_last - b) to V, as the GDN state update does.
+// Same organisation as the diagonal kernel: waves 0-1 state columns of chunk
+// c, waves 2-3 loaders (q and k rows of chunk c + 2, the gate prefix), waves
+// 4-7 producers of chunk c + 1; barriers P0, then R0, R1, B2 per iteration.
+// #############################################################################
+struct SLds {
+  static constexpr int FB = FR * 2;
+  static constexpr int NW = 2 * NU;        // Q fragments: (32-token tile, 16-deep step)
+  static constexpr int NKT = NM * 4;       // K^T fragments: (rho tile, token step)
+  static constexpr int O_Q = 0;
+  static constexpr int O_KT = O_Q + NW * FB;
+  static constexpr int O_QK = O_KT + NKT * FB;  // (tril(Q K^T) . Gamma)^T as B fragments
+  // gate ring, one entry per chunk mod 3 (a chunk's gates are read by the
+  // producers one iteration and by the state waves the next): b (log2 units),
+  // gamma = exp(b), dec = exp(b_last - b)
+  static constexpr int GE = 3 * C * 4;     // bytes of one entry
+  static constexpr int O_GR = O_QK + 6 * FB;
+  static constexpr int RQK = DK * 2 + 16;  // bytes per staged q / k row
+  static constexpr int O_SK = O_GR + 3 * GE;
+  static constexpr int O_SQ = O_SK + C * RQK;
+  static constexpr int TOTAL = O_SQ + C * RQK;
+  static_assert(TOTAL <= 160 * 1024, "LDS budget");
+};
+
+// ---- waves 2-3: q and k rows of tokens 32w .. 32w + 31; wave 2 also the gates
+__device__ __forceinline__ void sloader_load(u32x4 (&buf)[16], float& ga, const FamArgs& args,
+                                             const Chain& ch, int c, int lane, int w) {
+  const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+  const u16* kb = static_cast<const u16*>(args.k) + ch.hk * DK + 8 * (lane & 15);
+  const u16* qb = static_cast<const u16*>(args.q) + ch.hk * DK + 8 * (lane & 15);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int tok = 32 * w + 4 * i + (lane >> 4);
+    const long row = c0 + ((tok < n) ? tok : n - 1);
+    buf[i] = *reinterpret_cast<const u32x4*>(kb + row * ch.qk_stride);
+    buf[8 + i] = *reinterpret_cast<const u32x4*>(qb + row * ch.qk_stride);
+  }
+  if (w == 0) {
+    const long row = c0 + ((lane < n) ? lane : n - 1);
+    ga = (lane < n) ? args.gate[row * args.h_v + ch.h] : 0.f;
+  }
+}
+
+// stage the rows; wave 2 writes the chunk's gate entry and returns its gate
+// sum (natural log)
+__device__ __forceinline__ float sloader_stage(const u32x4 (&buf)[16], float ga,
+                                               unsigned char* smem, int c, int lane, int w) {
+  using LP = SLds;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int off = (32 * w + 4 * i + (lane >> 4)) * LP::RQK + 16 * (lane & 15);
+    *reinterpret_cast<u32x4*>(smem + LP::O_SK + off) = buf[i];
+    *reinterpret_cast<u32x4*>(smem + LP::O_SQ + off) = buf[8 + i];
+  }
+  if (w != 0) return 0.f;
+  float b = ga * kLog2e;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const float x = __shfl_up(b, off, 64);
+    if (lane >= off) b += x;
+  }
+  const float b_last = __shfl(b, 63, 64);
+  float* ge = reinterpret_cast<float*>(smem + LP::O_GR + (c % 3) * LP::GE);
+  ge[lane] = b;
+  ge[C + lane] = __builtin_amdgcn_exp2f(b);
+  ge[2 * C + lane] = __builtin_amdgcn_exp2f(b_last - b);
+  return b_last * kLn2;
+}
+
+__device__ __forceinline__ void sloader_wave(const FamArgs& args, const Chain& ch,
+                                             unsigned char* smem, int lane, int w) {
+  u32x4 buf[16];
+  float ga = 0.f, ld = 0.f;
+  if (ch.nc > 0) {
+    sloader_load(buf, ga, args, ch, 0, lane, w);
+    ld += sloader_stage(buf, ga, smem, 0, lane, w);
+    if (ch.nc > 1) sloader_load(buf, ga, args, ch, 1, lane, w);
+  }
+  lds_barrier();  // P0
+  for (int it = -1; it < ch.nc; ++it) {
+    lds_barrier();  // R0: the producers hold chunk it + 1's rows
+    if (it + 2 < ch.nc) {
+      ld += sloader_stage(buf, ga, smem, it + 2, lane, w);
+      if (it + 3 < ch.nc) sloader_load(buf, ga, args, ch, it + 3, lane, w);
+    }
+    lds_barrier();  // R1
+    lds_barrier();  // B2
+  }
+  if (w == 0 && lane == 0 && args.log_decay != nullptr && ch.cb == 0) args.log_decay[ch.sh] = ld;
+}
+
+// ---- waves 4-7: chunk c + 1.  Producer U: the K^T fragments and the Q
+// fragments of channels 32U .. 32U + 31, and whole score tiles (query tile
+// tq, key tile tk): U = 0: (0,0) (1,0) (1,1); 1: (2,0) (2,1) (2,2); 2: (3,0)
+// (3,1); 3: (3,2) (3,3).
+template <int U>
+struct STiles {
+  static constexpr int N = (U < 2) ? 3 : 2;
+  static constexpr int first = (U < 2) ? 3 * U : 6 + 2 * (U - 2);  // pair index of the first
+  static constexpr int TQ0 = (U == 0) ? 0 : ((U == 1) ? 2 : 3);    // lowest query tile
+  static constexpr int NQT = (U == 0) ? 2 : 1;                      // query tiles
+  static constexpr int TK0 = (U == 3) ? 2 : 0;                      // lowest key tile
+  static constexpr int NKT = (U == 0) ? 2 : ((U == 1) ? 3 : 2);     // key tiles
+};
+__device__ __forceinline__ constexpr int pair_tq(int i) {
+  return (i < 1) ? 0 : ((i < 3) ? 1 : ((i < 6) ? 2 : 3));
+}
+
+template <int DV, int U>
+__device__ __forceinline__ void sproducer_wave(const FamArgs& args, const Chain& ch,
+                                               unsigned char* smem, int lane) {
+  using LP = SLds;
+  using TL = STiles<U>;
+  const int g = lane >> 4, r = lane & 15;
+  u16* fQ = reinterpret_cast<u16*>(smem + LP::O_Q);
+  u16* fKt = reinterpret_cast<u16*>(smem + LP::O_KT);
+  u16* fQK = reinterpret_cast<u16*>(smem + LP::O_QK);
+  const unsigned char* sk = smem + LP::O_SK;
+  const unsigned char* sq = smem + LP::O_SQ;
+  if (U == 0) {
+    // the score tiles (query tile 0, key tile 1) and (2, 3) lie above the
+    // diagonal inside fragments that are read; they stay zero
+    *reinterpret_cast<u16x4*>(fQK + scatter_off(tri_idx(0, 1), 0, lane)) = pack4(0.f, 0.f, 0.f, 0.f);
+    *reinterpret_cast<u16x4*>(fQK + scatter_off(tri_idx(1, 3), 0, lane)) = pack4(0.f, 0.f, 0.f, 0.f);
+  }
+  // selectors of the K^T transposes (rho order, as in the diagonal kernel)
+  bf16x8 esel[2];
+  {
+    const int pn = (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        esel[h][j] = static_cast<__bf16>((8 * g + j == 16 * h + pn) ? 1.f : 0.f);
+  }
+  lds_barrier();  // P0
+  for (int it = -1; it < ch.nc; ++it) {
+    const int p = it + 1;
+    const bool active = p < ch.nc;
+    // lane (g, r) of a 16-token tile t and 32-channel step kk: token 16t + r,
+    // channels 32kk + 8g .. +7 of the staged rows
+    uint4 ks[4], qs[4];                       // this wave's channel slice, tiles 0-3
+    uint4 qt[TL::NQT][4], kt[TL::NKT][4];     // the score tiles' rows, all d_k
+    if (active) {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        ks[t] = *reinterpret_cast<const uint4*>(sk + (16 * t + r) * LP::RQK + (32 * U + 8 * g) * 2);
+        qs[t] = *reinterpret_cast<const uint4*>(sq + (16 * t + r) * LP::RQK + (32 * U + 8 * g) * 2);
+      }
+#pragma unroll
+      for (int i = 0; i < TL::NQT; ++i)
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          qt[i][kk] = *reinterpret_cast<const uint4*>(sq + (16 * (TL::TQ0 + i) + r) * LP::RQK +
+                                                      (32 * kk + 8 * g) * 2);
+#pragma unroll
+      for (int i = 0; i < TL::NKT; ++i)
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          kt[i][kk] = *reinterpret_cast<const uint4*>(sk + (16 * (TL::TK0 + i) + r) * LP::RQK +
+                                                      (32 * kk + 8 * g) * 2);
+    }
+    lds_barrier();  // R0: the staged rows are in registers
+    u16x4 kd[4][2];    // K^T tiles (token tile t, rho half h)
+    u16x4 sc[TL::N];   // the score tiles, masked and packed
+    if (active) {
+      const int n = chunk_len(ch, p);
+      const float* gb = reinterpret_cast<const float*>(smem + LP::O_GR + (p % 3) * LP::GE);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const bool keep = 16 * t + r < n;
+        ks[t] = mask4(ks[t], keep);
+        qs[t] = mask4(qs[t], keep);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const f32x4 x4 = mma16(as_bf(ks[t]), esel[h], f32x4{0.f, 0.f, 0.f, 0.f});
+          kd[t][h] = pack4(x4[0], x4[1], x4[2], x4[3]);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < TL::N; ++j) {
+        const int i = TL::first + j;
+        const int tq = pair_tq(i), tk = i - tq * (tq + 1) / 2;
+        const bool kq = 16 * tq + r < n;
+        // A = key rows, B = query rows: lane (g, r) holds (Q K^T)[16tq + r][16tk + 4g + e]
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+          acc = mma16(as_bf(kt[tk - TL::TK0][kk]), masked(qt[tq - TL::TQ0][kk], kq), acc);
+        const float bq = gb[16 * tq + r];
+        const float4 bk = *reinterpret_cast<const float4*>(gb + 16 * tk + 4 * g);
+        const float bkv[4] = {bk.x, bk.y, bk.z, bk.w};
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          // keys past the chunk have zero rows... unless repeated: masked by position
+          const bool ok = (tk < tq || 4 * g + e <= r) && (16 * tk + 4 * g + e < n);
+          const float x = acc[e] * __builtin_amdgcn_exp2f(bq - bkv[e]);
+          v[e] = ok ? x : 0.f;
+        }
+        sc[j] = pack4(v[0], v[1], v[2], v[3]);
+      }
+    }
+    lds_barrier();  // R1: the state waves are done with chunk c's operands
+    if (active) {
+      // Q fragments (the diagonal kernel's layout, unscaled)
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        *reinterpret_cast<uint4*>(fQ + ((t >> 1) * NU + 2 * U + (g >> 1)) * FR +
+                                  (32 * (g & 1) + 16 * (t & 1) + r) * 8) = qs[t];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          *reinterpret_cast<u16x4*>(fKt + scatter_off(U * 4 + t, h, lane)) = kd[t][h];
+#pragma unroll
+      for (int j = 0; j < TL::N; ++j) {
+        const int i = TL::first + j;
+        const int tq = pair_tq(i), tk = i - tq * (tq + 1) / 2;
+        *reinterpret_cast<u16x4*>(fQK + scatter_off(tri_idx(tq >> 1, tk), tq & 1, lane)) = sc[j];
+      }
+    }
+    lds_barrier();  // B2
+  }
+}
+
+// ---- waves 0-1: the state update of chunk c -----------------------------------
+template <int DV>
+__device__ __forceinline__ void sstate_wave(const FamArgs& args, const Chain& ch,
+                                            unsigned char* smem, int lane, int col0) {
+  using LP = SLds;
+  const int g2 = lane >> 5, n32 = lane & 31;
+  const u16* fQ = reinterpret_cast<const u16*>(smem + LP::O_Q);
+  const u16* fKt = reinterpret_cast<const u16*>(smem + LP::O_KT);
+  const u16* fQK = reinterpret_cast<const u16*>(smem + LP::O_QK);
+  const u16* vg = static_cast<const u16*>(args.v) + ch.h * DV + col0;
+  u16* og = static_cast<u16*>(args.o);
+
+  f32x16 st[NM];
+#pragma unroll
+  for (int m = 0; m < NM; ++m) st[m] = zero16();
+  bf16x8 isel[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      isel[u][j] = static_cast<__bf16>((16 * u + 8 * g2 + j == n32) ? 1.f : 0.f);
+  uint4 vr[2][2];
+  auto prefetch = [&](int c) __attribute__((always_inline)) {
+    const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+    load_tile32<2>(vr[0], vg, ch.v_stride, c0, n, 0, lane);
+    load_tile32<2>(vr[1], vg, ch.v_stride, c0, n, 1, lane);
+  };
+  if (ch.nc > 0) prefetch(0);
+  lds_barrier();  // P0
+
+  // V^T of the chunk as fragments over tokens (lane (g2, n) holds
+  // V[slot][col0 + n], exact products with the identity) and S0 as bf16
+  // operands: prepared between R1 and B2 of the previous iteration, while the
+  // producers store
+  bf16x8 vB[4], s0[NU];
+  auto prepare = [&](int c) __attribute__((always_inline)) {
+    const int n = chunk_len(ch, c);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const bool keep = n == C || 32 * t + n32 < n;
+      f32x16 acc = mma32(masked(vr[t][0], keep), isel[0], zero16());
+      acc = mma32(masked(vr[t][1], keep), isel[1], acc);
+      vB[2 * t] = frag_of(acc, 0);
+      vB[2 * t + 1] = frag_of(acc, 1);
+    }
+    if (c + 1 < ch.nc) prefetch(c + 1);
+#pragma unroll
+    for (int u = 0; u < NU; ++u) s0[u] = frag_of(st[u >> 1], u & 1);
+  };
+  // O^T = (S0^T Q^T) diag(gamma) + V^T A^T for query tile tq; lane (g2, n)
+  // holds O[token 32tq + n][col0 + 8b + 4g2 + i]
+  auto outputs = [&](int c, int tq) __attribute__((always_inline)) {
+    const int c0 = ch.lo + c * C, n = chunk_len(ch, c);
+    const float* ggam = reinterpret_cast<const float*>(smem + LP::O_GR + (c % 3) * LP::GE) + C;
+    f32x16 acc = zero16();
+#pragma unroll
+    for (int u = 0; u < NU; ++u) acc = mma32(s0[u], ldf(fQ, tq * NU + u, lane), acc);
+    acc *= ggam[32 * tq + n32];
+#pragma unroll
+    for (int s = 0; s < 2 * tq + 2; ++s) acc = mma32(vB[s], ldf(fQK, tri_idx(tq, s), lane), acc);
+    const int row = 32 * tq + n32;
+    if (og != nullptr && row < n) {
+      u16* dst = og + (static_cast<long>(c0) + row) * ch.v_stride + ch.h * DV + col0 + 4 * g2;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        u16x4 o4;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o4[i] = bf16_bits(acc[4 * b + i]);
+        *reinterpret_cast<u16x4*>(dst + 8 * b) = o4;
+      }
+    }
+  };
+
+  for (int it = -1; it < ch.nc; ++it) {
+    const int c = it;
+    const bool active = c >= 0;
+    // the first output tile while the producers move their staged rows
+    if (active) outputs(c, 0);
+    lds_barrier();  // R0
+    if (active) {
+      outputs(c, 1);
+      // S <- gamma_last S0 + K^T diag(exp(b_last - b)) V
+      const float* gb = reinterpret_cast<const float*>(smem + LP::O_GR + (c % 3) * LP::GE);
+      const float* gdec = gb + 2 * C;
+      bf16x8 dv[4];
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        const float4 d0 = *reinterpret_cast<const float4*>(gdec + 16 * s + 4 * g2);
+        const float4 d1 = *reinterpret_cast<const float4*>(gdec + 16 * s + 8 + 4 * g2);
+        const float dd[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          dv[s][j] = static_cast<__bf16>(static_cast<float>(vB[s][j]) * dd[j]);
+      }
+      const float g_last = gb[C + C - 1];
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        f32x16 acc = st[m] * g_last;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) acc = mma32(ldf(fKt, m * 4 + s, lane), dv[s], acc);
+        st[m] = acc;
+      }
+    }
+    lds_barrier();  // R1
+    if (c + 1 < ch.nc) prepare(c + 1);
+    lds_barrier();  // B2
+  }
+
+  if (args.S_out != nullptr) {
+    float* so = args.S_out + ch.sh * DK * DV + col0 + n32;
+#pragma unroll
+    for (int m = 0; m < NM; ++m)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) so[true_row(m, e, g2) * DV] = st[m][e];
+  }
+}
+
+template <int DV>
+__global__ __launch_bounds__(kThreads, 1) void scalar_pipe_kernel(FamArgs args) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int lane = tid & 63;
+  const Chain ch = make_chain<DV>(args);
+  if (wave < 2)
+    sstate_wave<DV>(args, ch, smem, lane, ch.cb * NCOL + 32 * wave);
+  else if (wave < 4)
+    sloader_wave(args, ch, smem, lane, wave - 2);
+  else if (wave == 4)
+    sproducer_wave<DV, 0>(args, ch, smem, lane);
+  else if (wave == 5)
+    sproducer_wave<DV, 1>(args, ch, smem, lane);
+  else if (wave == 6)
+    sproducer_wave<DV, 2>(args, ch, smem, lane);
+  else
+    sproducer_wave<DV, 3>(args, ch, smem, lane);
+}
+
+template <int DV>
+hipError_t launch_s(const FamArgs& a, int n_items, hipStream_t s) {
+  constexpr int bytes = SLds::TOTAL;
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(&scalar_pipe_kernel<DV>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(scalar_pipe_kernel<DV>, dim3(n_items), dim3(kThreads), bytes, s, a);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 bool diag_pipe_supported(int bf16, int d_k, int d_v, int mode) {
   return bf16 && mode == 0 && d_k == DK && (d_v == 64 || d_v == 128);
+}
+
+hipError_t launch_scalar_pipe(const FamArgs& a, int d_v, int n_chains, hipStream_t s) {
+  const int64_t n_items = static_cast<int64_t>(n_chains) * a.h_v * (d_v / NCOL);
+  if (n_items <= 0) return hipSuccess;
+  if (n_items > 0x7fffffff || a.mode != 0) return hipErrorInvalidValue;
+  const int n = static_cast<int>(n_items);
+  if (d_v == 64) return launch_s<64>(a, n, s);
+  return launch_s<128>(a, n, s);
 }
 
 hipError_t launch_diag_pipe(const FamArgs& a, int d_v, int n_chains, hipStream_t s) {
