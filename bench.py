@@ -84,7 +84,7 @@ MFMA_FILE = os.path.join(HERE, "profiles", "mfma_counters.json")
 KERNEL_SOURCES = {
     "scan_bf16": ["scan_bf16.hip", "mfma.hpp", "scan.hpp"],
     "compose": ["compose.hip", "mfma.hpp", "scan.hpp"],
-    "family_scalar_build": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
+    "family_scalar_build": ["gated_pipe.hip", "frag32.hpp", "mfma.hpp", "family.hpp", "scan.hpp"],
     "family_diagonal_build": ["gated_pipe.hip", "frag32.hpp", "mfma.hpp", "family.hpp", "scan.hpp"],
     "family_scalar_compose": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
     "family_diagonal_compose": ["family.hip", "mfma.hpp", "family.hpp", "scan.hpp", "frag_common.hpp"],
@@ -602,7 +602,7 @@ def bench_families(torch, steps, warmup, seam_w):
                               "re-reads served by L2 and the memory-side cache are the gap "
                               "to frac_algorithmic"})
         broof = hbm_roofline(byts, build_ms, "family_%s_build" % family, FAMILY_WORKLOAD)
-        broof["kernel"] = ("family_pipe_kernel (build)" if family == "scalar"
+        broof["kernel"] = ("scalar_pipe_kernel (build)" if family == "scalar"
                            else "diag_pipe_kernel (build)")
         out[family] = {
             "tokens_per_s": T / dt,
