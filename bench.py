@@ -82,7 +82,7 @@ CSRC = os.path.join(HERE, "paper_2607_01299_amd", "csrc")
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "hbm_traffic.json")
 MFMA_FILE = os.path.join(HERE, "profiles", "mfma_counters.json")
 KERNEL_SOURCES = {
-    "scan_bf16": ["scan_bf16.hip", "mfma.hpp", "scan.hpp"],
+    "scan_bf16": ["scan_bf16.hip", "frag32.hpp", "mfma.hpp", "scan.hpp"],
     "compose": ["compose.hip", "mfma.hpp", "scan.hpp"],
     "family_scalar_build": ["gated_pipe.hip", "frag32.hpp", "mfma.hpp", "family.hpp", "scan.hpp"],
     "family_diagonal_build": ["gated_pipe.hip", "frag32.hpp", "mfma.hpp", "family.hpp", "scan.hpp"],

@@ -64,6 +64,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "frag32.hpp"
 #include "mfma.hpp"
 #include "scan.hpp"
 
@@ -71,27 +72,12 @@ namespace hypic {
 
 namespace {
 
+using namespace f32frag;
+
 constexpr int kThreads = 512;
 constexpr int C = 64;     // tokens per chunk
 constexpr int NCOL = 64;  // state / operator columns per workgroup (with the operator)
-constexpr int FR = 512;   // u16 elements of one fragment (64 lanes x 8 bf16)
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef unsigned short u16;
-typedef u16 u16x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ f32x16 zero16() {
-  f32x16 z;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) z[i] = 0.f;
-  return z;
-}
-__device__ __forceinline__ f32x16 mma32(bf16x8 a, bf16x8 b, f32x16 c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
-__device__ __forceinline__ f32x4 mma16(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 // 16 x 16 x 16 product of float32 operands on the bf16 matrix cores, split
 // into hi + lo terms (hi*hi + hi*lo + lo*hi): a[s] = A[r][4g + s],
@@ -119,52 +105,6 @@ __device__ __forceinline__ f32x4 mma16_x3(const Split4& a, const Split4& b, f32x
   return c;
 }
 
-// elements 8h .. 8h+7 of a 32 x 32 accumulator: one 16-deep operand step
-__device__ __forceinline__ bf16x8 frag_of(const f32x16& a, int h) {
-  bf16x8 r;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) r[j] = static_cast<__bf16>(a[8 * h + j]);
-  return r;
-}
-__device__ __forceinline__ void split_of(const f32x16& a, int h, bf16x8& hi, bf16x8& lo) {
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const float x = a[8 * h + j];
-    hi[j] = static_cast<__bf16>(x);
-    lo[j] = static_cast<__bf16>(x - static_cast<float>(hi[j]));
-  }
-}
-
-__device__ __forceinline__ bf16x8 ldf(const u16* base, int f, int lane) {
-  return *reinterpret_cast<const bf16x8*>(base + f * FR + lane * 8);
-}
-__device__ __forceinline__ void stf(u16* base, int f, int lane, bf16x8 v) {
-  *reinterpret_cast<bf16x8*>(base + f * FR + lane * 8) = v;
-}
-
-__device__ __forceinline__ uint4 mask4(uint4 w, bool keep) {
-  const uint32_t m = keep ? 0xffffffffu : 0u;
-  return make_uint4(w.x & m, w.y & m, w.z & m, w.w & m);
-}
-__device__ __forceinline__ bf16x8 as_bf(uint4 w) { return __builtin_bit_cast(bf16x8, w); }
-__device__ __forceinline__ bf16x8 masked(uint4 w, bool keep) { return as_bf(mask4(w, keep)); }
-
-__device__ __forceinline__ u16 bf16_bits(float x) {
-  __bf16 h = static_cast<__bf16>(x);
-  return __builtin_bit_cast(u16, h);
-}
-
-// true row of element (tile m, element e) held by lane group g2 of a state or
-// operator accumulator: rho = 32m + 8(e/4) + 4 g2 + e%4 with bits 2, 3 swapped
-__device__ __forceinline__ int true_row(int m, int e, int g2) {
-  const int b = e >> 2;
-  return 32 * m + 16 * (b >> 1) + 8 * g2 + 4 * (b & 1) + (e & 3);
-}
-// token (or contraction index) carried by slot j of lane group g2 in step s
-__device__ __forceinline__ int slot_idx(int s, int g2, int j) {
-  return 16 * s + 8 * (j >> 2) + 4 * g2 + (j & 3);
-}
-
 // Step I of the column-parallel unit-lower substitution on 16-lane rows: lane
 // 16b + c holds column c of the solution (x) and column c of -L (lcol); the
 // coefficient -L[r][I] comes from lane I of the same row (DPP row_newbcast:I).
@@ -183,9 +123,6 @@ __device__ __forceinline__ void unit_lower_solve_step(float (&x)[16], const floa
   }
 }
 
-// index of fragment (row tile t, step s) in the 6-fragment lower-triangular
-// sets (t = 0: s = 0, 1; t = 1: s = 0..3)
-__device__ __forceinline__ int tri_idx(int t, int s) { return (t == 0) ? s : 2 + s; }
 
 // ---- LDS plan (bytes) --------------------------------------------------------
 template <int DK>
@@ -366,19 +303,6 @@ __device__ __forceinline__ void producer_compose(PShare<DK, SLOT>& sh, const Sca
     }
     if (it + 1 >= 0 && it + 1 < ch.nc) share_load<DK, SLOT>(sh, args, ch, it + 1, lane);
   }
-}
-
-// raw 16-byte loads of the 32x32-layout fragments of one token tile of a
-// token-major bf16 matrix: lane (g2, r) gets row 32t + r, columns 16u + 8g2 ..
-// +7 for u = 0 .. NU-1 (rows past the chunk are clamped; zeroed at use)
-template <int NU>
-__device__ __forceinline__ void load_tile32(uint4 (&dst)[NU], const u16* base, long rs, int c0,
-                                            int n, int t, int lane) {
-  const int tok = 32 * t + (lane & 31);
-  const int tc = (tok < n) ? tok : n - 1;
-  const u16* p = base + static_cast<long>(c0 + tc) * rs + 8 * (lane >> 5);
-#pragma unroll
-  for (int u = 0; u < NU; ++u) dst[u] = *reinterpret_cast<const uint4*>(p + 16 * u);
 }
 
 // =============================================================================
@@ -630,23 +554,6 @@ __device__ __forceinline__ void load_tile16(uint4 (&dst)[NB], const u16* base, l
   const u16* p = base + static_cast<long>(c0 + tc) * rs + 8 * (lane >> 4);
 #pragma unroll
   for (int u = 0; u < NB; ++u) dst[u] = *reinterpret_cast<const uint4*>(p + 32 * u);
-}
-
-// u16 offset of the four slots 4(g/2) .. +3 of lane 32(g%2) + 16h + n in
-// fragment f: where lane (g, n) of a 16 x 16 accumulator tile (rows 4g + e)
-// lands in a 32x32-layout operand fragment whose 16-deep step is that tile's
-// rows and whose 32-wide side holds the tile's columns at offset 16h
-__device__ __forceinline__ int scatter_off(int f, int h, int lane) {
-  const int g = lane >> 4, n = lane & 15;
-  return f * FR + (32 * (g & 1) + 16 * h + n) * 8 + 4 * (g >> 1);
-}
-__device__ __forceinline__ u16x4 pack4(float a, float b, float c, float d) {
-  u16x4 r;
-  r[0] = bf16_bits(a);
-  r[1] = bf16_bits(b);
-  r[2] = bf16_bits(c);
-  r[3] = bf16_bits(d);
-  return r;
 }
 
 // Wave 5: loads all of K and Q of the chunk (one copy per workgroup) and the
