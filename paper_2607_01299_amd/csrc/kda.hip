@@ -371,7 +371,18 @@ __global__ __launch_bounds__(kKT) void kda_scan_kernel(KdaArgs args) {
   if (lo < hi) prefetch(lo, (hi - lo < KC) ? hi - lo : KC);
   float ld_acc = 0.f;
 
+  const int tid_in = tid;
   for (int c0 = lo; c0 < hi; c0 += KC) {
+    // an opaque copy of the thread index keeps the compiler from hoisting the
+    // loop-invariant LDS addresses out of the chunk loop (they would not all
+    // fit in registers and were spilled to scratch); they are cheap to
+    // recompute per chunk
+    int tid_v = tid_in;
+    asm volatile("" : "+v"(tid_v));
+    const int tid = tid_v;
+    const int lane = tid & 63;
+    const int g = lane >> 4, ln = lane & 15;
+    const int pc = tid % DK, pt = tid / DK;
     const int n = (hi - c0 < KC) ? hi - c0 : KC;
     lds_barrier();  // the previous chunk is done with every LDS buffer
 
