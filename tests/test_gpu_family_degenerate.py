@@ -9,7 +9,11 @@ float64 oracle and closed forms of the Tab. 1 recurrences:
 * zero gates: no decay, so log_decay is exactly zero and the state is the
   plain sum of k_t v_t^T;
 * the strongest per-token decay the 16-token tile references take (-5 on
-  every channel, 80 over a tile): finite, and the oracle's outputs.
+  every channel, 80 over a tile): finite, and the oracle's outputs;
+* 150 segments, past the 128 whose longest-first order travels in the kernel
+  arguments (the order is then ranked on the device);
+* no outputs requested (o = NULL): the state and log_decay unchanged bit for
+  bit.
 """
 
 import numpy as np
@@ -124,3 +128,42 @@ def test_diagonal_strongest_decay(hy):
     res, host, gate, cu = _run(hy, "diagonal", lengths, gate_fn, 33)
     ref = F.family_build_segments("diagonal", host["q"], host["k"], host["v"], gate, cu)
     _check(res, ref, cu, "diagonal gate -5")
+
+
+@pytest.mark.parametrize("family", ["scalar", "diagonal"])
+def test_more_segments_than_the_inline_order(hy, family):
+    """150 segments: past 128 the longest-first order is ranked on the device
+    into the workspace instead of travelling in the kernel arguments; every
+    (segment, head) must still land on its own rows."""
+    rng = np.random.default_rng(35)
+    lengths = [int(x) for x in rng.integers(0, 131, size=150)]
+    lengths[7] = 0
+    lengths[100] = 130
+    _say("family %s bf16 d_k=128, %d segments (%d tokens)" % (family, len(lengths), sum(lengths)))
+
+    def gate_fn(T, h_v):
+        return W.family_gate(family, T, h_v, 128, 92)
+
+    res, host, gate, cu = _run(hy, family, lengths, gate_fn, 36)
+    ref = F.family_build_segments(family, host["q"], host["k"], host["v"], gate, cu)
+    _check(res, ref, cu, "%s 150 segments" % family)
+
+
+@pytest.mark.parametrize("family", ["scalar", "diagonal"])
+def test_without_outputs(hy, family):
+    """o = NULL: the build skips the output stores only; S_seg and log_decay
+    are bit for bit those of the build that writes o."""
+    lengths = [190, 1, 64]
+    _say("family %s bf16 d_k=128 without outputs, lengths %s" % (family, lengths))
+    rng = np.random.default_rng(37)
+    T = int(sum(lengths))
+    cu = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int32)
+    q, k, v = [torch.from_numpy(rng.standard_normal(s).astype(np.float32)).cuda()
+               .to(torch.bfloat16).contiguous() for s in ((T, 2, 128), (T, 2, 128), (T, 4, 128))]
+    gate = torch.from_numpy(W.family_gate(family, T, 4, 128, 93)).cuda().contiguous()
+    full = hy.family_build(family, q, k, v, gate, cu)
+    bare = hy.family_build(family, q, k, v, gate, cu, want_o=False)
+    torch.cuda.synchronize()
+    assert bare["o"] is None
+    assert torch.equal(full["S_seg"], bare["S_seg"])
+    assert torch.equal(full["log_decay"], bare["log_decay"])
