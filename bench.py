@@ -247,7 +247,7 @@ def cpu_baseline(build_w, pool_w, build_s=12.0, burst_s=6.0):
     forked with the workloads in memory, one BLAS thread each."""
     import multiprocessing as mp
     affinity = len(os.sched_getaffinity(0))
-    # the GPU box allots 16 host cores to its one GPU, whatever the affinity mask shows
+    # a one-GPU host share is 16 cores, whatever the affinity mask shows
     workers = max(1, min(affinity, 16))
     for var in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
         os.environ[var] = "1"
@@ -723,8 +723,8 @@ def main():
                     help="run only a plain 1 GiB device copy (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
-              "(segments shard across GPUs with no exchange; see the design notes). "
+        print("bench.py measures one GPU: the library has no multi-GPU path "
+              "(segments would shard across GPUs with no exchange). "
               "Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:

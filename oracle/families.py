@@ -20,7 +20,7 @@ underflow on long segments.
 
 RoPE (Eq. (7), Eq. (8)): ``R(p)`` rotates channel pairs (2i, 2i+1) by the angle
 ``p * theta_i`` with ``theta_i = base^(-2i/d)``, the pairing of the RoPE paper
-the text cites (the paper does not fix a pairing; see the design notes).
+the text cites (the paper does not fix a pairing).
 
 Conv warm-up (Sec. 4.2): a depthwise causal convolution of width K over the
 hidden channels, ``y[t, c] = silu(sum_j w[c, j] x[t - K + 1 + j, c])``, whose

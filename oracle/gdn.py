@@ -14,7 +14,7 @@ Notation follows the paper (Hypic, arXiv 2607.01299):
   ``S_t = T_t S_{t-1} + u_t`` and ``o_t = S_t^T q_t`` (the token reads the state
   after its own write; no scale factor is applied).
 
-Readings of points the paper leaves open (each is listed in the design doc):
+Readings of points the paper leaves open:
 
 * the segment operator ``T_C`` multiplies later tokens on the left, as in Eq. (4)
   and the product convention stated under Eq. (6);
