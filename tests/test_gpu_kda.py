@@ -161,6 +161,26 @@ def test_kda_build_compose_seam(hy, dt, d, heads, kind):
                 assert rel(Sp[e, h], R_post[e, h]) <= tol, (sw, e, h)
 
 
+def test_kda_more_segments_than_the_inline_order(hy):
+    """150 segments: past 128 the longest-first order of both launches is
+    ranked on the device into the workspace; every (segment, head) lands on
+    its own rows, operator included."""
+    rng = np.random.default_rng(38)
+    lengths = [int(x) for x in rng.integers(0, 131, size=150)]
+    lengths[3] = 0
+    lengths[120] = 130
+    _say("kda bf16 d=128 heads=(1, 2), %d segments (%d tokens)" % (len(lengths), sum(lengths)))
+    w = W.segment_workload(2, lengths=lengths, heads=(1, 2), d=128, dtype=W.BF16, seed=39)
+    T = int(w["cu_seqlens"][-1])
+    w["gate"] = W.family_gate("diagonal", T, 2, 128, 1039)
+    q, k, v, beta, gate = _dev(w, W.BF16)
+    res = hy.kda_build(q, k, v, beta, gate, w["cu_seqlens"])
+    torch.cuda.synchronize()
+    ref = K.kda_build_segments(w["q"], w["k"], w["v"], w["beta"], w["gate"], w["cu_seqlens"])
+    pairs = [(s, h) for s in range(len(lengths)) for h in range(2)]
+    _check_build(res, ref, w["cu_seqlens"], pairs, TOL[W.BF16], "kda 150 segments", w["gate"])
+
+
 def test_kda_without_operator_matches_with(hy):
     """P_hat = NULL skips the operator columns; o and S_seg are unchanged."""
     _say("kda bf16 d=128 build without the operator")
