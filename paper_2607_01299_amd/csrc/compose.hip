@@ -127,7 +127,7 @@ __global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
   lds_barrier();  // (no wave reads what another writes to HBM: loads stay in flight)
 
   // Pool tuple of one step: this lane's row of P_hat as A fragments (k slots
-  // kap(g, .) of each 32-block), the S_seg tile elements and exp(log_decay).
+  // kap(g, .) of each 32-block), the S_seg tile elements and log_decay.
   // LOOK register sets: the tuple of step j + LOOK is loaded while step j
   // computes.  Split grids are latency-bound and look two steps ahead; the
   // full-width state of an unsplit grid leaves registers for one.
@@ -157,7 +157,10 @@ __global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
     for (int mt = 0; mt < NT; ++mt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) t.s[mt][i] = tile_ptr(Si, mt)[i * DV];
-    t.e = __expf(args.log_decay[sh]);
+    // the exponential is taken when the step uses it: taking it here would
+    // make the wave wait for this load, and with it (loads complete in order)
+    // for every row of the tuple just requested
+    t.e = args.log_decay[sh];
   };
   // one composition step with the tuple t (step j), then the load of step
   // j + LOOK into t
@@ -181,7 +184,7 @@ __global__ __launch_bounds__(DK * 4) void compose_kernel(ComposeArgs args) {
     f32x4 cS[NT];
 #pragma unroll
     for (int mt = 0; mt < NT; ++mt) cS[mt] = t.s[mt];
-    const float e = t.e;
+    const float e = __expf(t.e);
     if (j + LOOK < j1) load_step(t, j + LOOK);
     if (args.S_incoming != nullptr) {
       float* dst = args.S_incoming + (static_cast<long>(j) * args.h_v + h) * state_sz;
